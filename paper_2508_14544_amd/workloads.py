@@ -1,0 +1,329 @@
+"""Seeded synthetic request instances for the scheduling simulator.
+
+This module only draws inputs: arrival steps ``a``, prompt sizes ``s``, true
+output lengths ``o`` and predicted intervals ``[l, u]`` (problem statement,
+Section 2: a worker with a KV cache of ``M`` tokens, ``n`` prompts, each with a
+prompt size and an output length predicted to lie in an interval).  It holds
+none of the schedulers' arithmetic; the CPU oracle and the HIP path both read
+what it produces, and neither imports the other.
+
+Random numbers come from a counter-based generator: the SplitMix64 output
+function (Steele, Lea and Flood, "Fast splittable pseudorandom number
+generators", OOPSLA 2014) applied to ``key + (j+1) * 0x9E3779B97F4A7C15``, where
+the key is derived from (seed, workload, field, instance).  Every instance is
+therefore reproducible on its own, which lets tests regenerate a sampled
+instance of a large batch without generating the rest.
+
+Bounded integers use the high 64 bits of ``r * range`` (Lemire's
+multiply-shift, without the rejection step; the bias is below range/2**64).
+Normals use the Box-Muller transform, exponentials the inversion method.
+
+Interval recipe (Section 4.2 heterogeneous intervals): geometric bins start at
+1, ``u_k = ceil(l_k * (1 + alpha))`` computed in exact integer arithmetic with
+``alpha = num/den``, next bin starts at ``u_k + 1``; a request gets the bin that
+contains its true ``o``.  ``alpha = 0`` gives exact predictions ``[o, o]``.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from fractions import Fraction
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+_G = np.uint64(0x9E3779B97F4A7C15)
+_M1 = np.uint64(0xBF58476D1CE4E5B9)
+_M2 = np.uint64(0x94D049BB133111EB)
+_U64 = np.uint64
+
+# field identifiers of the random streams
+F_ARRIVAL, F_PROMPT, F_OUTPUT, F_OUTPUT2, F_MIX, F_U1, F_U2, F_NORM2 = range(8)
+
+
+def _mix(z: np.ndarray) -> np.ndarray:
+    """SplitMix64 output function on uint64 (wrapping arithmetic)."""
+    z = (z ^ (z >> _U64(30))) * _M1
+    z = (z ^ (z >> _U64(27))) * _M2
+    return z ^ (z >> _U64(31))
+
+
+def _stream_keys(seed: int, workload_id: int, fld: int, instances: np.ndarray) -> np.ndarray:
+    with np.errstate(over="ignore"):
+        k0 = _mix(np.array([seed], dtype=np.uint64) + _G * _U64(workload_id + 1))
+        k1 = _mix(k0 ^ (_U64(0xD1B54A32D192ED03) * _U64(fld + 1)))
+        return _mix(k1 + _G * (instances.astype(np.uint64) + _U64(1)))
+
+
+def raw64(seed: int, workload_id: int, fld: int, instances: np.ndarray, n: int) -> np.ndarray:
+    """uint64 draws, shape (len(instances), n)."""
+    keys = _stream_keys(seed, workload_id, fld, instances)
+    j = np.arange(1, n + 1, dtype=np.uint64)
+    with np.errstate(over="ignore"):
+        return _mix(keys[:, None] + _G * j[None, :])
+
+
+def uniform_int(r: np.ndarray, lo: int, hi: int) -> np.ndarray:
+    """Integers in [lo, hi] from uint64 draws: high word of r * (hi-lo+1)."""
+    rng = _U64(hi - lo + 1)
+    rh = r >> _U64(32)
+    rl = r & _U64(0xFFFFFFFF)
+    with np.errstate(over="ignore"):
+        hi64 = (rh * rng + ((rl * rng) >> _U64(32))) >> _U64(32)
+    return (hi64.astype(np.int64) + lo)
+
+
+def uniform01(r: np.ndarray) -> np.ndarray:
+    """Doubles in [0, 1)."""
+    return (r >> _U64(11)).astype(np.float64) * (1.0 / 9007199254740992.0)
+
+
+def uniform01_open0(r: np.ndarray) -> np.ndarray:
+    """Doubles in (0, 1]."""
+    return ((r >> _U64(11)).astype(np.float64) + 1.0) * (1.0 / 9007199254740992.0)
+
+
+def geometric_bins(alpha: Fraction, max_o: int) -> np.ndarray:
+    """Table ``lo[o]`` / ``hi[o]`` of the geometric bin containing each o in [1, max_o].
+
+    Returns int64 array of shape (2, max_o + 1); column 0 is unused.
+    """
+    alpha = Fraction(alpha)
+    num, den = alpha.numerator, alpha.denominator
+    lo = np.zeros(max_o + 1, dtype=np.int64)
+    hi = np.zeros(max_o + 1, dtype=np.int64)
+    l = 1
+    while l <= max_o:
+        u = (l * (den + num) + den - 1) // den  # ceil(l * (1 + alpha)), exact
+        top = min(u, max_o)
+        lo[l:top + 1] = l
+        hi[l:top + 1] = u
+        l = u + 1
+    return np.stack([lo, hi])
+
+
+@dataclass
+class Instances:
+    """A batch of independent instances in CSR layout (int32 request fields)."""
+    name: str
+    M: int
+    offsets: np.ndarray           # int64 [K+1]
+    arrival: np.ndarray           # int32 [N]
+    prompt: np.ndarray            # int32 [N]
+    output: np.ndarray            # int32 [N]
+    lower: Optional[np.ndarray]   # int32 [N]
+    upper: Optional[np.ndarray]   # int32 [N]
+    instance_ids: np.ndarray      # int64 [K] ids within the full workload
+    meta: Dict[str, object] = field(default_factory=dict)
+
+    @property
+    def num_instances(self) -> int:
+        return int(self.offsets.shape[0] - 1)
+
+    @property
+    def total_requests(self) -> int:
+        return int(self.offsets[-1])
+
+    @property
+    def max_requests(self) -> int:
+        if self.num_instances == 0:
+            return 0
+        return int(np.max(np.diff(self.offsets)))
+
+    def instance(self, k: int) -> Dict[str, np.ndarray]:
+        b, e = int(self.offsets[k]), int(self.offsets[k + 1])
+        d = {"arrival": self.arrival[b:e], "prompt": self.prompt[b:e], "output": self.output[b:e]}
+        d["lower"] = None if self.lower is None else self.lower[b:e]
+        d["upper"] = None if self.upper is None else self.upper[b:e]
+        return d
+
+    def subset(self, ks: Sequence[int]) -> "Instances":
+        ks = list(ks)
+        parts = {f: [] for f in ("arrival", "prompt", "output", "lower", "upper")}
+        offs = [0]
+        for k in ks:
+            d = self.instance(k)
+            for f in parts:
+                if d[f] is not None:
+                    parts[f].append(d[f])
+            offs.append(offs[-1] + int(self.offsets[k + 1] - self.offsets[k]))
+        cat = lambda f: (np.concatenate(parts[f]).astype(np.int32) if parts[f] else np.zeros(0, np.int32))
+        return Instances(self.name, self.M, np.array(offs, dtype=np.int64), cat("arrival"), cat("prompt"),
+                         cat("output"), None if self.lower is None else cat("lower"),
+                         None if self.upper is None else cat("upper"),
+                         self.instance_ids[ks].copy(), dict(self.meta))
+
+
+# ---------------------------------------------------------------------------
+# Workload registry.  Each entry is named by what it is and its sizes.
+# ---------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    workload_id: int
+    num_instances: int
+    n: int
+    M: int
+    description: str
+
+
+WORKLOADS: Dict[str, Workload] = {
+    w.name: w for w in [
+        Workload("single_n200_m512", 1, 1, 200, 512,
+                 "1 instance, n=200 at t=0; s~U{1..16}, o~U{1..64}; geometric bins alpha=0.5; M=512"),
+        Workload("batch4096_n1000_m16384", 2, 4096, 1000, 16384,
+                 "4096 instances, n=1000 at t=0; s~U{1..64}, o~U{1..512}; geometric bins alpha in "
+                 "{0.1,0.5,1.0} (1365/1365/1366 instances); M=16384"),
+        Workload("online1024_n10000_m65536", 3, 1024, 10000, 65536,
+                 "1024 instances, n=10000, Poisson arrivals 4/step; s~U{8..256}; o=clamp(round(exp(5+Z)),1,2048); "
+                 "l=max(1,floor(o*U1)), u=ceil(o*(1+U2)), U1~U[0.5,1), U2~U[0,1); M=65536"),
+        Workload("single_n100000_m1048576", 4, 1, 100000, 1 << 20,
+                 "1 instance, n=100000 arriving over 20000 steps (sorted i.i.d. U{0..19999}); s~U{16..2048}, "
+                 "o~U{1..4096}; geometric bins alpha=0.5; M=2^20"),
+        Workload("sweep65536_n2000_m32768", 5, 65536, 2000, 32768,
+                 "65536 instances, n=2000 at t=0; s~U{1..128}; o: 70% U{1..64}, 30% U{512..1024}; geometric "
+                 "bins alpha in {0,0.25,...,2.0} (8 blocks of 7281, last 7288); M=32768"),
+    ]
+}
+
+
+def _alpha_blocks(num_instances: int, alphas: Sequence[Fraction]) -> np.ndarray:
+    """Alpha index per instance: contiguous blocks of floor(K/len), remainder to the last block."""
+    b = num_instances // len(alphas)
+    idx = np.minimum(np.arange(num_instances) // max(b, 1), len(alphas) - 1)
+    return idx
+
+
+_ALPHAS = {
+    2: [Fraction(1, 10), Fraction(1, 2), Fraction(1, 1)],
+    5: [Fraction(k, 4) for k in range(9)],
+}
+
+
+def _bins_for(alpha: Fraction, o: np.ndarray, max_o: int):
+    tab = geometric_bins(alpha, max_o)
+    return tab[0][o], tab[1][o]
+
+
+def generate(name: str, seed: int = 0, instance_ids: Optional[Sequence[int]] = None,
+             with_upper: bool = True) -> Instances:
+    """Generate a workload (or a subset of its instances) deterministically."""
+    w = WORKLOADS[name]
+    if instance_ids is None:
+        ids = np.arange(w.num_instances, dtype=np.int64)
+    else:
+        ids = np.asarray(list(instance_ids), dtype=np.int64)
+        if ids.size and (ids.min() < 0 or ids.max() >= w.num_instances):
+            raise ValueError("instance id out of range")
+    K, n, wid = ids.size, w.n, w.workload_id
+    R = lambda fld: raw64(seed, wid, fld, ids, n)
+    meta: Dict[str, object] = {"seed": seed, "workload": name}
+
+    if wid == 1:
+        arr = np.zeros((K, n), np.int64)
+        s = uniform_int(R(F_PROMPT), 1, 16)
+        o = uniform_int(R(F_OUTPUT), 1, 64)
+        l, u = _bins_for(Fraction(1, 2), o, 64)
+    elif wid == 2:
+        arr = np.zeros((K, n), np.int64)
+        s = uniform_int(R(F_PROMPT), 1, 64)
+        o = uniform_int(R(F_OUTPUT), 1, 512)
+        aidx = _alpha_blocks(w.num_instances, _ALPHAS[2])[ids]
+        l = np.empty_like(o)
+        u = np.empty_like(o)
+        for k, al in enumerate(_ALPHAS[2]):
+            m = aidx == k
+            if m.any():
+                l[m], u[m] = _bins_for(al, o[m], 512)
+        meta["alpha"] = [str(_ALPHAS[2][i]) for i in aidx]
+    elif wid == 3:
+        gaps = -np.log(uniform01_open0(R(F_ARRIVAL))) / 4.0
+        arr = np.floor(np.cumsum(gaps, axis=1)).astype(np.int64)
+        s = uniform_int(R(F_PROMPT), 8, 256)
+        z = np.sqrt(-2.0 * np.log(uniform01_open0(R(F_OUTPUT)))) * np.cos(2.0 * np.pi * uniform01(R(F_NORM2)))
+        o = np.clip(np.rint(np.exp(5.0 + z)), 1, 2048).astype(np.int64)
+        u1 = 0.5 + 0.5 * uniform01(R(F_U1))
+        u2 = uniform01(R(F_U2))
+        l = np.maximum(1, np.floor(o * u1)).astype(np.int64)
+        u = np.ceil(o * (1.0 + u2)).astype(np.int64)
+    elif wid == 4:
+        arr = np.sort(uniform_int(R(F_ARRIVAL), 0, 19999), axis=1)
+        s = uniform_int(R(F_PROMPT), 16, 2048)
+        o = uniform_int(R(F_OUTPUT), 1, 4096)
+        l, u = _bins_for(Fraction(1, 2), o, 4096)
+    elif wid == 5:
+        arr = np.zeros((K, n), np.int64)
+        s = uniform_int(R(F_PROMPT), 1, 128)
+        short = uniform01(R(F_MIX)) < 0.7
+        o = np.where(short, uniform_int(R(F_OUTPUT), 1, 64), uniform_int(R(F_OUTPUT2), 512, 1024))
+        aidx = _alpha_blocks(w.num_instances, _ALPHAS[5])[ids]
+        l = np.empty_like(o)
+        u = np.empty_like(o)
+        for k, al in enumerate(_ALPHAS[5]):
+            m = aidx == k
+            if m.any():
+                l[m], u[m] = _bins_for(al, o[m], 1024)
+        meta["alpha"] = [str(_ALPHAS[5][i]) for i in aidx]
+    else:  # pragma: no cover
+        raise ValueError(name)
+
+    offsets = np.arange(K + 1, dtype=np.int64) * n
+    c32 = lambda x: np.ascontiguousarray(x.reshape(-1), dtype=np.int32)
+    return Instances(name, w.M, offsets, c32(arr), c32(s), c32(o), c32(l),
+                     c32(u) if with_upper else None, ids, meta)
+
+
+def from_lists(M: int, instances: List[Dict[str, Sequence[int]]], name: str = "custom") -> Instances:
+    """Pack hand-written instances (dicts with keys arrival/prompt/output/lower/upper) into CSR."""
+    offs = [0]
+    cols: Dict[str, list] = {f: [] for f in ("arrival", "prompt", "output", "lower", "upper")}
+    has = {f: True for f in cols}
+    for d in instances:
+        n = len(d["output"])
+        offs.append(offs[-1] + n)
+        for f in cols:
+            v = d.get(f)
+            if v is None:
+                if f == "arrival":
+                    v = [0] * n
+                else:
+                    has[f] = False
+                    continue
+            if len(v) != n:
+                raise ValueError(f"field {f} has wrong length")
+            cols[f].extend(int(x) for x in v)
+    arr = lambda f: np.array(cols[f], dtype=np.int32) if has[f] else None
+    K = len(instances)
+    return Instances(name, int(M), np.array(offs, dtype=np.int64), arr("arrival"), arr("prompt"),
+                     arr("output"), arr("lower"), arr("upper"), np.arange(K, dtype=np.int64))
+
+
+def random_small(seed: int, num_instances: int, n_max: int, *, s_max: int = 6, o_max: int = 8,
+                 M: int = 24, arrivals: bool = True, alpha: Optional[Fraction] = None) -> Instances:
+    """Small random instances (for fuzzing the oracles against each other).
+
+    Every request satisfies s + u <= M so that all three schedulers accept it.
+    """
+    ids = np.arange(num_instances, dtype=np.int64)
+    wid = 100
+    ns = uniform_int(raw64(seed, wid, 0, ids, 1), 1, n_max)[:, 0]
+    rs = raw64(seed, wid, 1, ids, n_max)
+    ro = raw64(seed, wid, 2, ids, n_max)
+    ra = raw64(seed, wid, 3, ids, n_max)
+    rl = raw64(seed, wid, 4, ids, n_max)
+    ru = raw64(seed, wid, 5, ids, n_max)
+    out = []
+    for k in range(num_instances):
+        n = int(ns[k])
+        o = uniform_int(ro[k, :n], 1, o_max)
+        if alpha is None:
+            l = np.maximum(1, o - uniform_int(rl[k, :n], 0, o_max))
+            l = np.minimum(l, o)
+            u = o + uniform_int(ru[k, :n], 0, o_max)
+        else:
+            l, u = _bins_for(alpha, o, o_max)
+        s_hi = np.maximum(0, M - u)
+        s = np.minimum(uniform_int(rs[k, :n], 0, s_max), s_hi)
+        a = np.sort(uniform_int(ra[k, :n], 0, 2 * o_max)) if arrivals else np.zeros(n, np.int64)
+        out.append({"arrival": a, "prompt": s, "output": o, "lower": l, "upper": u})
+    return from_lists(M, out, name=f"random_small_{seed}")

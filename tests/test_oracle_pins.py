@@ -1,0 +1,223 @@
+"""Pins of the CPU oracle to things other than itself (no GPU needed).
+
+* worked examples the paper prints (Example 1, Example 2) and two examples
+  derived by hand from Algorithms 2/4 (tests/golden/*.json);
+* a closed form the paper states: H-SF's total latency on the instance built in
+  the proof of Theorem 3.2;
+* a closed form of the memory model: identical requests with s >= 1 run in
+  batches that restart one step after completion (a completing run still
+  holds s+o at its completion step);
+* a second, independently written step loop that evaluates equation (2)
+  densely at every step (``literal_simulate``), fuzzed against the C oracle;
+* brute-force hindsight optimum on tiny instances (OPT <= every algorithm);
+* an event-log auditor (memory <= M before and after evictions at every step,
+  completion = start + o, equation (3), evictions only on overflow);
+* reductions: exact predictions make A_min = A_max = H-SF; l = o makes
+  A_min = H-SF; a huge M makes every completion a + o.
+"""
+import glob
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2508_14544_amd import workloads as W
+
+FIELDS_I = ("status", "tel", "makespan", "request_steps", "total_evictions")
+FIELDS_A = ("completion", "evictions")
+
+
+def same(r1, r2):
+    return all(r1[f] == r2[f] for f in FIELDS_I) and all(np.array_equal(r1[f], r2[f]) for f in FIELDS_A)
+
+
+def _golden_files():
+    here = os.path.join(os.path.dirname(__file__), "golden")
+    return sorted(glob.glob(os.path.join(here, "*.json")))
+
+
+@pytest.mark.parametrize("path", _golden_files(), ids=lambda p: os.path.basename(p))
+def test_golden_examples(path):
+    g = json.load(open(path))
+    inst, M = g["instance"], g["M"]
+    for name, exp in g["expected"].items():
+        algo = O.ALGOS[name]
+        r = O.simulate(inst, algo, M, events=True)
+        assert r["status"] == O.OK
+        for k, v in exp.items():
+            if k == "starts":
+                starts = {}
+                for (t, kind, i) in r["events"]:
+                    if kind == O.EV_START:
+                        starts[i] = t
+                assert [starts[i] for i in range(len(v))] == v
+            elif k in FIELDS_A:
+                assert r[k].tolist() == v, (name, k)
+            else:
+                assert r[k] == v, (name, k)
+        O.audit(inst, algo, M, r)
+        assert same(r, O.literal_simulate(inst, algo, M))
+    if "opt_tel" in g:
+        assert O.opt_tel(inst, M) == g["opt_tel"]
+
+
+@pytest.mark.parametrize("l,u,a,b,seed", [(2, 8, 10, 20, 0), (3, 12, 15, 30, 2), (4, 9, 12, 18, 3), (1, 4, 5, 10, 4)])
+def test_hsf_closed_form_theorem32_instance(l, u, a, b, seed):
+    # Proof of Theorem 3.2: s=0, M=l*u, a*u jobs of length l and b*l of length u.
+    # H-SF runs the short jobs in a batches of u and then the long ones in b
+    # batches of l:  TEL = u*l*(1+..+a) + b*l*a*l + u*l*(1+..+b).
+    rng = np.random.default_rng(seed)
+    o = np.array([l] * (a * u) + [u] * (b * l))
+    rng.shuffle(o)
+    n = len(o)
+    inst = {"prompt": np.zeros(n, int), "output": o, "lower": np.full(n, l), "upper": np.full(n, u)}
+    r = O.simulate(inst, O.HSF, l * u)
+    assert r["tel"] == u * l * a * (a + 1) // 2 + b * l * a * l + u * l * b * (b + 1) // 2
+
+
+@pytest.mark.parametrize("s,k,m,B", [(1, 3, 4, 5), (2, 5, 3, 7), (4, 1, 6, 4)])
+def test_identical_requests_batches(s, k, m, B):
+    # n = m*B identical requests (prompt s>=1, output k, exact prediction), M = m*(s+k).
+    # A batch of m fills M exactly at its completion step k, so the next batch
+    # can only start one step later: batch j completes at j*(k+1) + k.
+    n = m * B
+    inst = {"prompt": [s] * n, "output": [k] * n, "lower": [k] * n, "upper": [k] * n}
+    expect = np.repeat(np.arange(B) * (k + 1) + k, m)
+    for algo in (O.AMAX, O.AMIN, O.HSF):
+        r = O.simulate(inst, algo, m * (s + k))
+        assert r["completion"].tolist() == expect.tolist()
+        assert r["tel"] == int(expect.sum())
+        assert r["request_steps"] == n * k
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_c_oracle_equals_literal_dense_eq2(seed):
+    b = W.random_small(seed, 120, 7, s_max=5, o_max=8, M=20, arrivals=(seed % 2 == 0))
+    n_ev = 0
+    for k in range(b.num_instances):
+        inst = b.instance(k)
+        for algo in (O.AMAX, O.AMIN, O.HSF):
+            r = O.simulate(inst, algo, b.M)
+            assert same(r, O.literal_simulate(inst, algo, b.M)), (k, algo)
+            n_ev += r["total_evictions"]
+    assert n_ev > 0  # the eviction path was exercised
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_audit_invariants(seed):
+    b = W.random_small(10 + seed, 150, 10, s_max=6, o_max=10, M=30, arrivals=(seed != 1))
+    for k in range(b.num_instances):
+        inst = b.instance(k)
+        for algo in (O.AMAX, O.AMIN, O.HSF):
+            O.audit(inst, algo, b.M, O.simulate(inst, algo, b.M, events=True))
+
+
+def test_audit_on_generated_workloads():
+    for name, ids in (("single_n200_m512", [0]), ("batch4096_n1000_m16384", [2731])):
+        b = W.generate(name, 0, instance_ids=ids)
+        inst = b.instance(0)
+        for algo in (O.AMAX, O.AMIN, O.HSF):
+            O.audit(inst, algo, b.M, O.simulate(inst, algo, b.M, events=True))
+
+
+def test_audit_rejects_planted_overflow():
+    # The auditor must notice a schedule that breaks equation (1).
+    inst = {"prompt": [1, 1], "output": [3, 3], "lower": [1, 1], "upper": [3, 3]}
+    r = O.simulate(inst, O.HSF, 4, events=True)
+    bad = dict(r)
+    bad["events"] = [(0, O.EV_START, 0), (0, O.EV_START, 1), (3, O.EV_COMPLETE, 0), (3, O.EV_COMPLETE, 1)]
+    bad["completion"] = np.array([3, 3], np.int32)
+    bad["tel"], bad["makespan"], bad["request_steps"] = 6, 3, 6
+    with pytest.raises(AssertionError):
+        O.audit(inst, O.HSF, 4, bad)
+
+
+@pytest.mark.parametrize("seed", range(2))
+def test_opt_is_a_lower_bound(seed):
+    b = W.random_small(100 + seed, 40, 5, s_max=3, o_max=4, M=10, arrivals=(seed == 0))
+    for k in range(b.num_instances):
+        inst = b.instance(k)
+        opt = O.opt_tel(inst, b.M)
+        for algo in (O.AMAX, O.AMIN, O.HSF):
+            assert opt <= O.simulate(inst, algo, b.M)["tel"]
+
+
+def test_reduction_exact_predictions_all_equal():
+    from fractions import Fraction
+    b = W.random_small(7, 100, 10, s_max=6, o_max=10, M=30, alpha=Fraction(0))
+    for k in range(b.num_instances):
+        inst = b.instance(k)
+        rs = [O.simulate(inst, a, b.M) for a in (O.AMAX, O.AMIN, O.HSF)]
+        assert same(rs[0], rs[2]) and same(rs[1], rs[2])
+    # a generated batch instance with alpha = 0
+    g = W.generate("sweep65536_n2000_m32768", 0, instance_ids=[3])
+    inst = g.instance(0)
+    assert np.array_equal(inst["lower"], inst["output"])
+    rs = [O.simulate(inst, a, g.M) for a in (O.AMAX, O.AMIN, O.HSF)]
+    assert same(rs[0], rs[2]) and same(rs[1], rs[2])
+
+
+def test_reduction_lower_equals_output_amin_is_hsf():
+    b = W.random_small(8, 100, 10, s_max=6, o_max=10, M=30)
+    for k in range(b.num_instances):
+        inst = dict(b.instance(k))
+        inst["lower"] = inst["output"]
+        assert same(O.simulate(inst, O.AMIN, b.M), O.simulate(inst, O.HSF, b.M))
+
+
+def test_reduction_huge_memory_and_single_request():
+    b = W.random_small(9, 50, 10, s_max=6, o_max=10, M=30)
+    for k in range(b.num_instances):
+        inst = b.instance(k)
+        for algo in (O.AMAX, O.AMIN, O.HSF):
+            r = O.simulate(inst, algo, 10 ** 6)
+            assert r["completion"].tolist() == (inst["arrival"] + inst["output"]).tolist()
+            one = {f: (None if v is None else v[:1]) for f, v in inst.items()}
+            r1 = O.simulate(one, algo, b.M)
+            assert r1["completion"].tolist() == [int(inst["arrival"][0] + inst["output"][0])]
+
+
+def test_step_cap_and_error_codes():
+    inst = {"prompt": [1, 1], "output": [3, 3], "lower": [1, 1], "upper": [3, 3]}
+    r = O.simulate(inst, O.AMIN, 4, step_cap=5)
+    assert r["status"] == O.E_STEP_CAP and r["completion"].tolist() == [-1, 3]
+    assert same(r, O.literal_simulate(inst, O.AMIN, 4, step_cap=5))
+    assert O.simulate(inst, O.AMIN, 4, step_cap=7)["status"] == O.OK
+    base = {"arrival": [0, 1], "prompt": [1, 1], "output": [3, 3], "lower": [1, 1], "upper": [3, 3]}
+    cases = [
+        (dict(base, lower=[4, 1]), O.AMIN, O.E_INTERVAL),   # l > o
+        (dict(base, lower=[0, 1]), O.AMIN, O.E_INTERVAL),   # l < 1
+        (dict(base, upper=[2, 3]), O.AMAX, O.E_INTERVAL),   # u < o
+        (dict(base, output=[0, 3]), O.HSF, O.E_INTERVAL),   # o < 1
+        (dict(base, prompt=[-1, 1]), O.HSF, O.E_INTERVAL),  # s < 0
+        (dict(base, prompt=[2, 1]), O.HSF, O.E_TOO_BIG),    # s + o > M
+        (dict(base, upper=[3, 4]), O.AMAX, O.E_TOO_BIG),    # s + u > M
+        (dict(base, arrival=[1, 0]), O.HSF, O.E_ARRIVAL),   # not sorted
+        (dict(base, arrival=[-1, 0]), O.HSF, O.E_ARRIVAL),  # negative
+        (dict(base, arrival=[1, 0], lower=[4, 1]), O.AMIN, O.E_ARRIVAL),  # priority
+        (dict(base, prompt=[2, 1], lower=[4, 1]), O.AMIN, O.E_INTERVAL),  # priority
+    ]
+    for inst_, algo, code in cases:
+        r = O.simulate(inst_, algo, 4)
+        assert r["status"] == code, (inst_, algo)
+        assert r["completion"].tolist() == [-1, -1] and r["tel"] == 0 and r["request_steps"] == 0
+    e = O.simulate({"prompt": [], "output": [], "lower": [], "upper": []}, O.AMIN, 4)
+    assert e["status"] == O.OK and e["tel"] == 0 and e["makespan"] == 0
+
+
+@pytest.mark.parametrize("l,u", [(2, 8), (3, 6), (5, 10)])
+def test_theorem31_upper_bound_soft(l, u):
+    # Theorem 3.1: CR(A_max) <= alpha^-1 (1 + alpha^-1) / 2 + O(1/M), alpha = l/u,
+    # with one interval [l, u] shared by all jobs.  Checked on random outputs.
+    rng = np.random.default_rng(l * 100 + u)
+    alpha = l / u
+    bound = (1 / alpha) * (1 + 1 / alpha) / 2
+    for trial in range(5):
+        n = 300
+        o = rng.integers(l, u + 1, n)
+        inst = {"prompt": np.ones(n, int), "output": o, "lower": np.full(n, l), "upper": np.full(n, u)}
+        M = 40 * (1 + u)
+        ratio = O.simulate(inst, O.AMAX, M)["tel"] / O.simulate(inst, O.HSF, M)["tel"]
+        assert ratio <= bound

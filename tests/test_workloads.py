@@ -1,0 +1,92 @@
+"""The seeded input generator: determinism, per-instance independence, ranges, bins."""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from paper_2508_14544_amd import workloads as W
+
+
+def test_bins_match_exact_ceil_and_known_tables():
+    # bins start at 1; u = ceil(l * (1 + alpha)) exactly; the next bin starts at u + 1
+    known = {
+        Fraction(1, 2): [(1, 2), (3, 5), (6, 9), (10, 15), (16, 24), (25, 38), (39, 59), (60, 90)],
+        Fraction(1, 1): [(1, 2), (3, 6), (7, 14), (15, 30), (31, 62), (63, 126), (127, 254), (255, 510)],
+        Fraction(1, 10): [(1, 2), (3, 4), (5, 6), (7, 8), (9, 10), (11, 13), (14, 16), (17, 19)],
+        Fraction(2, 1): [(1, 3), (4, 12), (13, 39), (40, 120), (121, 363), (364, 1092)],
+        Fraction(1, 4): [(1, 2), (3, 4), (5, 7), (8, 10), (11, 14), (15, 19), (20, 25), (26, 33)],
+    }
+    for alpha, bins in known.items():
+        tab = W.geometric_bins(alpha, 2000)
+        for lo, hi in bins:
+            assert tab[0][lo] == lo and tab[1][lo] == hi and tab[0][min(hi, 2000)] == lo
+    for alpha in [Fraction(k, 20) for k in range(0, 41)]:
+        tab = W.geometric_bins(alpha, 5000)
+        for o in range(1, 5001):
+            l, u = int(tab[0][o]), int(tab[1][o])
+            assert l <= o <= u
+            assert Fraction(u) >= l * (1 + alpha) > u - 1  # u = ceil(l (1 + alpha))
+    # the exact rule differs from a float ceil(l * 1.1) on some bin starts
+    import math
+    tab = W.geometric_bins(Fraction(1, 10), 5000)
+    starts = sorted(set(int(x) for x in tab[0][1:]))
+    assert any(math.ceil(l * 1.1) != int(tab[1][l]) for l in starts)
+
+
+def test_deterministic_and_subset_independent():
+    a = W.generate("batch4096_n1000_m16384", 0, instance_ids=[5, 1400, 4095])
+    b = W.generate("batch4096_n1000_m16384", 0, instance_ids=[4095])
+    assert np.array_equal(a.instance(2)["output"], b.instance(0)["output"])
+    c = W.generate("batch4096_n1000_m16384", 0, instance_ids=[5, 1400, 4095])
+    for f in ("arrival", "prompt", "output", "lower", "upper"):
+        assert np.array_equal(getattr(a, f), getattr(c, f))
+    d = W.generate("batch4096_n1000_m16384", 1, instance_ids=[5])
+    assert not np.array_equal(a.instance(0)["output"], d.instance(0)["output"])
+
+
+@pytest.mark.parametrize("name,ids", [
+    ("single_n200_m512", [0]),
+    ("batch4096_n1000_m16384", [0, 1365, 4095]),
+    ("online1024_n10000_m65536", [0, 1023]),
+    ("single_n100000_m1048576", [0]),
+    ("sweep65536_n2000_m32768", [0, 7281, 65535]),
+])
+def test_ranges(name, ids):
+    w = W.WORKLOADS[name]
+    b = W.generate(name, 0, instance_ids=ids)
+    assert b.M == w.M and b.max_requests == w.n and b.num_instances == len(ids)
+    assert np.all(b.lower >= 1) and np.all(b.lower <= b.output) and np.all(b.output <= b.upper)
+    assert np.all(b.prompt + b.upper <= b.M)
+    for k in range(b.num_instances):
+        a = b.instance(k)["arrival"]
+        assert np.all(a >= 0) and np.all(np.diff(a) >= 0)
+    ranges = {
+        "single_n200_m512": ((1, 16), (1, 64)),
+        "batch4096_n1000_m16384": ((1, 64), (1, 512)),
+        "online1024_n10000_m65536": ((8, 256), (1, 2048)),
+        "single_n100000_m1048576": ((16, 2048), (1, 4096)),
+        "sweep65536_n2000_m32768": ((1, 128), (1, 1024)),
+    }[name]
+    assert ranges[0][0] <= b.prompt.min() and b.prompt.max() <= ranges[0][1]
+    assert ranges[1][0] <= b.output.min() and b.output.max() <= ranges[1][1]
+
+
+def test_distribution_shapes():
+    b = W.generate("online1024_n10000_m65536", 0, instance_ids=[3])
+    a = b.arrival
+    rate = len(a) / (a[-1] + 1)
+    assert 3.8 < rate < 4.2                          # Poisson arrivals, 4 per step
+    assert 120 < np.median(b.output) < 180           # lognormal(5, 1): median e^5 ~ 148
+    s = W.generate("sweep65536_n2000_m32768", 0, instance_ids=[9000])
+    short = np.mean(s.output <= 64)
+    assert 0.67 < short < 0.73                       # 70 % short outputs
+    assert np.all((s.output <= 64) | (s.output >= 512))
+    g = W.generate("single_n100000_m1048576", 0)
+    assert g.arrival.max() <= 19999 and abs(g.prompt.mean() - 1032) < 10
+
+
+def test_alpha_blocks():
+    idx = W._alpha_blocks(4096, [0, 1, 2])
+    assert np.bincount(idx).tolist() == [1365, 1365, 1366]
+    idx = W._alpha_blocks(65536, list(range(9)))
+    assert np.bincount(idx).tolist() == [7281] * 8 + [7288]
