@@ -1,0 +1,122 @@
+/*
+ * schedsim.h -- C ABI of the MI355X (gfx950) simulator of the memory-constrained
+ * LLM-inference schedulers A_max, A_min and H-SF (arXiv 2508.14544).
+ *
+ * Problem (Section 2): one worker with a KV cache of M tokens serves n
+ * requests; request i has prompt size s_i, true output length o_i (revealed
+ * only by running it) and a predicted interval [l_i, u_i] containing o_i.
+ * Time is discrete.  A request started at step p holds s_i + (tau - p) tokens
+ * at every step tau in [p, p + o_i] and completes at C_i = p + o_i.  Memory in
+ * use may never exceed M (equation (1)).  A running request may be cancelled;
+ * it then loses its generated tokens and waits again (Section 2, cancellation).
+ * The metric is the total end-to-end latency, equation (3): sum of C_i - a_i.
+ *
+ * Policies (one per call):
+ *   SCHED_AMAX  Algorithm 1: plan every request with length u_i; admit while
+ *               equation (2) holds.  Never cancels.
+ *   SCHED_AMIN  Algorithms 2 and 4: plan with a lower bound o~_i (initially
+ *               l_i); when the running set's memory at t+1 would exceed M,
+ *               cancel runs in ascending (o~_i, i) until it fits and raise each
+ *               cancelled request's o~_i to the tokens it had generated.
+ *   SCHED_HSF   Algorithm 3 (hindsight shortest-first): plan with the true o_i.
+ * Each step, waiting requests are tried in ascending (planning length, index)
+ * order and the longest prefix that keeps equation (2) is started.  Ties break
+ * by ascending request index.  Requests arriving at step a_i join the waiting
+ * set at that step (the paper has every a_i = 0).
+ *
+ * All pointers in sched_instances_t and sched_results_t are DEVICE pointers
+ * (e.g. torch tensors on the GPU), allocated and owned by the caller; the
+ * library keeps none of them after the work queued on the stream completes.
+ * Calls are asynchronous on `stream` (a hipStream_t; NULL = default stream).
+ */
+#ifndef SCHEDSIM_H
+#define SCHEDSIM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { SCHED_AMAX = 0, SCHED_AMIN = 1, SCHED_HSF = 2 } sched_algo_t;
+
+/* Return codes of the calls (synchronous) and per-instance status values
+ * (written to results.status, valid once the stream has reached the call). */
+enum {
+  SCHED_OK = 0,
+  SCHED_E_INVAL = -1,       /* call: NULL/inconsistent arguments, M <= 0 or M >= 2^30.
+                               status: offsets out of range or n_k > max_requests */
+  SCHED_E_INTERVAL = -2,    /* status: o < 1, s < 0, or (A_min) l < 1 or l > o, or (A_max) u < o */
+  SCHED_E_TOO_BIG = -3,     /* status: s + o > M, or (A_max) s + u > M: can never run           */
+  SCHED_E_STEP_CAP = -4,    /* status: unfinished requests when the step cap was passed        */
+  SCHED_E_HIP = -5,         /* call: a HIP runtime call failed                                  */
+  SCHED_E_UNSUPPORTED = -6, /* call: capacity request beyond what the kernels hold.
+                               status: o, u or l >= 2^15, s >= 2^16, n >= 2^17, or the running
+                               or evicted set outgrew its capacity                              */
+  SCHED_E_ARRIVAL = -7      /* status: an arrival < 0 or arrivals not non-decreasing in index  */
+};
+
+/* A batch of K independent instances in CSR layout.  Instance k owns requests
+ * [offsets[k], offsets[k+1]); request fields are int32 arrays of length N. */
+typedef struct {
+  int32_t num_instances;    /* K >= 0                                                  */
+  int32_t max_requests;     /* upper bound on every n_k; sizes on-chip state (< 2^17)  */
+  int64_t total_requests;   /* N = offsets[K]                                          */
+  const int64_t* offsets;   /* [K+1], offsets[0] = 0, non-decreasing                    */
+  const int32_t* arrival;   /* [N] arrival step a_i, non-decreasing per instance; NULL = all 0 */
+  const int32_t* prompt;    /* [N] prompt size s_i                                      */
+  const int32_t* output;    /* [N] true output length o_i (the simulated world)         */
+  const int32_t* lower;     /* [N] l_i; required for SCHED_AMIN, unused otherwise       */
+  const int32_t* upper;     /* [N] u_i; required for SCHED_AMAX, unused otherwise       */
+} sched_instances_t;
+
+/* Outputs.  Per request: completion step C_i (-1 if it never completed) and
+ * the number of times it was cancelled.  Per instance: total latency
+ * sum(C_i - a_i) over completed requests (equation (3)), makespan max C_i,
+ * request-steps (sum over steps of the number of running requests, wasted
+ * work included), total cancellations and status.  Instances whose status is
+ * not SCHED_OK and not SCHED_E_STEP_CAP report C_i = -1 and zero counters. */
+typedef struct {
+  int32_t* completion;      /* [N] required     */
+  int32_t* evictions;       /* [N] or NULL      */
+  int64_t* total_latency;   /* [K] required     */
+  int32_t* makespan;        /* [K] or NULL      */
+  int64_t* request_steps;   /* [K] or NULL      */
+  int64_t* total_evictions; /* [K] or NULL      */
+  int32_t* status;          /* [K] required     */
+} sched_results_t;
+
+typedef struct {
+  int64_t step_cap;         /* last simulated step; <= 0: per instance
+                               min(2^30, 4*(max a + sum(o+1)) + 64)                       */
+  int32_t running_capacity; /* max concurrently running requests per instance, <= 1024;
+                               0: min(max_requests rounded up to 64, 1024)                */
+  int32_t evicted_capacity; /* max cancelled requests waiting at once (A_min); 0: default */
+  void* event_before;       /* hipEvent_t recorded just before the simulation kernel, or NULL */
+  void* event_after;        /* hipEvent_t recorded just after it, or NULL                  */
+} sched_options_t;
+
+/* Simulate every instance with the given policy and budget M (0 < M < 2^30).
+ * Returns SCHED_OK once the work is queued, or a call-level error code (then
+ * nothing was queued).  Per-instance problems are reported in results.status;
+ * other instances still run.  Scratch memory is allocated stream-ordered on
+ * `stream` and released after the kernels (stream-ordered). */
+int sched_simulate(const sched_instances_t* instances, sched_algo_t algo, int64_t M,
+                   const sched_results_t* results, void* stream);
+
+/* Same, with options (opts may be NULL = all defaults). */
+int sched_simulate_opts(const sched_instances_t* instances, sched_algo_t algo, int64_t M,
+                        const sched_results_t* results, void* stream,
+                        const sched_options_t* opts);
+
+/* Human-readable text for a return or status code (static storage). */
+const char* sched_strerror(int code);
+
+/* Library ABI version (major * 100 + minor). */
+int sched_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SCHEDSIM_H */

@@ -1,0 +1,788 @@
+// sched_kernels.hip -- gfx950 kernels of the scheduler simulator.
+//
+// One wave64 workgroup simulates one instance from t = 0 to its last
+// completion; nothing returns to the host between steps.
+//
+// k_prepare (per instance): validates the requests, computes the default step
+//   cap, initialises the per-request outputs, and ranks the requests by
+//   (initial planning length, index) with a stable two-pass LSD radix sort
+//   (8-bit digits, LDS histogram, ballot-based stable scatter).  The ranked
+//   records (key, s | o << 16) go to a workspace slice of the instance.
+//
+// k_simulate (per instance), state:
+//   running set R    -- ROWS x 64 register slots, row r lane j holds one run:
+//                       planned end Rend = p + est, x = s - p + t_r, completion
+//                       C = p + o, key = est << 17 | index, and h = f(Rend) +
+//                       Rend - t_r, where f(c) is the planned memory at step c of
+//                       all runs whose planned end is >= c (equation (2) summed
+//                       over the planned set).  t_r is a base step that keeps the
+//                       int32 values small (rebased every 2^16 steps).
+//   fresh waiting F  -- two-level bitmap over key ranks in LDS; the smallest
+//                       waiting key is the first set bit.
+//   evicted waiting V-- (A_min) unsorted (key, s | o << 16) array in LDS; the
+//                       smallest key is found by a wave min-reduction.
+// Per step: arrivals set bits of F; runs with C == t complete; for A_min the
+// projected memory P at t+1 is compared with M and runs are cancelled in
+// ascending key while P > M; then candidates (smallest key of F and V) are
+// admitted while equation (2) holds.  The admission test needs only O(1)
+// wave reductions because the planned set before the test is always feasible
+// (every checkpoint after the candidate's planned end was verified when its
+// runs were admitted), so it checks: step t (runs completing now hold s+o),
+// step t+1 when a run is already past its planned end, every existing planned
+// end <= the candidate's via max h, and the candidate's own planned end.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "schedsim.h"
+#include "wave.hpp"
+
+namespace sk {
+
+constexpr int kIdxBits = 17;
+constexpr uint32_t kIdxMask = (1u << kIdxBits) - 1u;
+constexpr int32_t kEstLimit = 1 << 15;
+constexpr int32_t kPromptLimit = 1 << 16;
+constexpr int32_t kRebase = 1 << 16;
+constexpr int64_t kCapLimit = int64_t(1) << 30;
+
+struct Params {
+  int32_t K;
+  int32_t max_requests;
+  int64_t N;
+  const int64_t* offsets;
+  const int32_t* arrival;
+  const int32_t* prompt;
+  const int32_t* output;
+  const int32_t* lower;
+  const int32_t* upper;
+  int32_t* completion;
+  int32_t* evictions;
+  int64_t* total_latency;
+  int32_t* makespan;
+  int64_t* request_steps;
+  int64_t* total_evictions;
+  int32_t* status;
+  int32_t M;
+  int64_t step_cap;      // > 0: user cap for every instance
+  // workspace
+  uint32_t* sort_a;
+  uint32_t* sort_b;
+  uint2* rec;
+  int32_t* rank_of;
+  int32_t* cap;
+  // LDS layout of k_simulate
+  int32_t nw_max;        // 64-bit words of the level-0 bitmap
+  int32_t nw1_max;       // 64-bit words of the level-1 bitmap
+  int32_t cap_v;         // evicted-set capacity
+};
+
+// ---------------------------------------------------------------------------
+// k_prepare
+// ---------------------------------------------------------------------------
+template <int ALGO>
+__global__ __launch_bounds__(64) void k_prepare(Params P) {
+  __shared__ uint32_t hist[256];
+  const int k = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int64_t b = P.offsets[k];
+  const int64_t e = P.offsets[k + 1];
+  int status = SCHED_OK;
+  if (b < 0 || e < b || e > P.N || e - b > P.max_requests) status = SCHED_E_INVAL;
+  const int n = (status == SCHED_OK) ? static_cast<int>(e - b) : 0;
+
+  bool arr_bad = false, int_bad = false, big_bad = false, unsup = (n >= (1 << kIdxBits));
+  int64_t max_a = 0, sum_o = 0;
+  int32_t prev_last = 0;
+  for (int c = 0; c < n; c += 64) {
+    const int i = c + lane;
+    const bool act = i < n;
+    int32_t a = 0, s = 0, o = 1, lo = 1, up = 1;
+    if (act) {
+      a = P.arrival ? P.arrival[b + i] : 0;
+      s = P.prompt[b + i];
+      o = P.output[b + i];
+      if (ALGO == SCHED_AMIN) lo = P.lower[b + i];
+      if (ALGO == SCHED_AMAX) up = P.upper[b + i];
+    }
+    int32_t ap = __shfl_up(a, 1, 64);
+    if (lane == 0) ap = prev_last;
+    prev_last = __shfl(a, 63, 64);
+    if (act) {
+      if (a < 0 || (i > 0 && a < ap)) arr_bad = true;
+      if (o < 1 || s < 0) int_bad = true;
+      if (ALGO == SCHED_AMIN && (lo < 1 || lo > o)) int_bad = true;
+      if (ALGO == SCHED_AMAX && up < o) int_bad = true;
+      if (static_cast<int64_t>(s) + o > P.M) big_bad = true;
+      if (ALGO == SCHED_AMAX && static_cast<int64_t>(s) + up > P.M) big_bad = true;
+      if (o >= kEstLimit || s >= kPromptLimit || (ALGO == SCHED_AMAX && up >= kEstLimit)) unsup = true;
+      max_a = a > max_a ? a : max_a;
+      sum_o += static_cast<int64_t>(o) + 1;
+    }
+  }
+  if (status == SCHED_OK) {
+    if (wave::ballot(arr_bad)) status = SCHED_E_ARRIVAL;
+    else if (wave::ballot(int_bad)) status = SCHED_E_INTERVAL;
+    else if (wave::ballot(big_bad)) status = SCHED_E_TOO_BIG;
+    else if (wave::ballot(unsup)) status = SCHED_E_UNSUPPORTED;
+  }
+  const int64_t max_a_all = wave::max_i64(max_a);
+  const int64_t sum_o_all = wave::sum_i64(sum_o);
+  int64_t cap = P.step_cap > 0 ? P.step_cap : 4 * (max_a_all + sum_o_all) + 64;
+  if (cap > kCapLimit) cap = kCapLimit;
+
+  // per-request outputs start as "not completed, never cancelled"
+  for (int c = 0; c < n; c += 64) {
+    const int i = c + lane;
+    if (i < n) {
+      P.completion[b + i] = -1;
+      if (P.evictions) P.evictions[b + i] = 0;
+    }
+  }
+  if (lane == 0) {
+    P.status[k] = status;
+    P.cap[k] = static_cast<int32_t>(cap);
+  }
+  if (status != SCHED_OK || n == 0) return;
+
+  // ---- keys (est0 << 17 | index), est0 = u (A_max), l (A_min), o (H-SF)
+  for (int c = 0; c < n; c += 64) {
+    const int i = c + lane;
+    if (i < n) {
+      int32_t est = (ALGO == SCHED_AMAX) ? P.upper[b + i] : (ALGO == SCHED_AMIN) ? P.lower[b + i] : P.output[b + i];
+      P.sort_a[b + i] = (static_cast<uint32_t>(est) << kIdxBits) | static_cast<uint32_t>(i);
+    }
+  }
+  // ---- stable LSD radix sort on bits 17..24 then 25..31
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int pass = 0; pass < 2; ++pass) {
+    const uint32_t* src = pass == 0 ? P.sort_a : P.sort_b;
+    uint32_t* dst = pass == 0 ? P.sort_b : P.sort_a;
+    const int shift = kIdxBits + 8 * pass;
+    for (int j = lane; j < 256; j += 64) hist[j] = 0;
+    __syncthreads();
+    for (int c = 0; c < n; c += 64) {
+      const int i = c + lane;
+      if (i < n) atomicAdd(&hist[(src[b + i] >> shift) & 0xFFu], 1u);
+    }
+    __syncthreads();
+    {
+      uint32_t h0 = hist[4 * lane], h1 = hist[4 * lane + 1], h2 = hist[4 * lane + 2], h3 = hist[4 * lane + 3];
+      int32_t tot = static_cast<int32_t>(h0 + h1 + h2 + h3);
+      int32_t ex = wave::inclusive_scan_i32(tot) - tot;
+      __syncthreads();
+      hist[4 * lane] = ex;
+      hist[4 * lane + 1] = ex + h0;
+      hist[4 * lane + 2] = ex + h0 + h1;
+      hist[4 * lane + 3] = ex + h0 + h1 + h2;
+    }
+    __syncthreads();
+    for (int c = 0; c < n; c += 64) {
+      const int i = c + lane;
+      const bool act = i < n;
+      const uint32_t key = act ? src[b + i] : 0u;
+      const uint32_t d = (key >> shift) & 0xFFu;
+      uint64_t eq = wave::ballot(act);
+      for (int bit = 0; bit < 8; ++bit) {
+        const uint64_t bal = wave::ballot(act && ((d >> bit) & 1u));
+        eq &= ((d >> bit) & 1u) ? bal : ~bal;
+      }
+      const int rank = __builtin_popcountll(eq & lt_mask);
+      const uint32_t base = act ? hist[d] : 0u;
+      __syncthreads();
+      if (act) {
+        dst[b + base + rank] = key;
+        if (rank == 0) hist[d] = base + static_cast<uint32_t>(__builtin_popcountll(eq));
+      }
+      __syncthreads();
+    }
+    __syncthreads();
+  }
+  // ---- ranked records and inverse ranks
+  for (int c = 0; c < n; c += 64) {
+    const int r = c + lane;
+    if (r < n) {
+      const uint32_t key = P.sort_a[b + r];
+      const uint32_t idx = key & kIdxMask;
+      const uint32_t s = static_cast<uint32_t>(P.prompt[b + idx]);
+      const uint32_t o = static_cast<uint32_t>(P.output[b + idx]);
+      P.rec[b + r] = make_uint2(key, s | (o << 16));
+      P.rank_of[b + idx] = r;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k_simulate
+// ---------------------------------------------------------------------------
+template <int ALGO, int ROWS>
+__global__ __launch_bounds__(64) void k_simulate(Params P) {
+  extern __shared__ uint64_t lds64[];
+  const int k = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int st0 = P.status[k];
+  const int64_t b = P.offsets[k];
+  const int n = (st0 == SCHED_OK) ? static_cast<int>(P.offsets[k + 1] - b) : 0;
+  const int32_t M = P.M;
+
+  int status = st0;
+  int64_t rsteps = 0, tot_ev = 0;
+
+  if (st0 == SCHED_OK && n > 0) {
+    uint64_t* L0 = lds64;
+    uint64_t* L1 = lds64 + P.nw_max;
+    uint32_t* vkey = reinterpret_cast<uint32_t*>(L1 + P.nw1_max);
+    uint32_t* vso = vkey + P.cap_v;
+    const int nw = (n + 63) >> 6;
+    const int nw1 = (nw + 63) >> 6;
+    for (int w = lane; w < nw; w += 64) L0[w] = 0;
+    for (int w = lane; w < nw1; w += 64) L1[w] = 0;
+    __syncthreads();
+
+    const int32_t cap = P.cap[k];
+    const uint2* rec = P.rec + b;
+    const int32_t* arrival = P.arrival ? P.arrival + b : nullptr;
+    const int32_t* rank_of = P.rank_of + b;
+    int32_t* completion = P.completion + b;
+    int32_t* evictions = P.evictions ? P.evictions + b : nullptr;
+
+    // running set
+    int32_t r_end[ROWS], r_x[ROWS], r_c[ROWS], r_h[ROWS];
+    uint32_t r_key[ROWS];
+    uint64_t vm[ROWS];
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+      r_end[r] = 0; r_x[r] = 0; r_c[r] = -1; r_h[r] = 0; r_key[r] = 0; vm[r] = 0;
+    }
+    int rows_hi = 0;      // rows [0, rows_hi) may hold runs
+    int32_t N = 0;        // number of runs
+    int32_t X = 0;        // sum of x over runs
+    int32_t t_r = 0;      // base step of x and h
+
+    // arrivals window: lane j holds request aw_base + j
+    int32_t aw_base = -64, aw_a = 0, aw_rank = 0;
+    int32_t arr_ptr = 0;
+    // fresh-waiting head and window of ranked records
+    int32_t f_rank = -1, fw_base = -1;
+    uint32_t f_key = 0, f_so = 0, fw_key = 0, fw_so = 0;
+    // evicted-waiting set
+    int32_t nV = 0, nVe = 0, v_pos = -1;
+    uint32_t v_key = 0xFFFFFFFFu, v_so = 0;
+    int32_t n_done = 0;
+
+    auto f_find = [&]() {
+      const uint64_t w1 = lane < nw1 ? L1[lane] : 0ull;
+      const uint64_t nz = wave::ballot(w1 != 0ull);
+      if (nz == 0ull) {
+        f_rank = -1;
+        return;
+      }
+      const int j1 = __builtin_ctzll(nz);
+      const uint64_t w1v = wave::readlane_u64(w1, j1);
+      const int j0 = j1 * 64 + __builtin_ctzll(w1v);
+      const uint64_t w0 = L0[j0];
+      f_rank = j0 * 64 + __builtin_ctzll(w0);
+      if (fw_base < 0 || f_rank < fw_base || f_rank >= fw_base + 64) {
+        fw_base = f_rank;
+        const int rr = fw_base + lane;
+        const uint2 rv = rr < n ? rec[rr] : make_uint2(0xFFFFFFFFu, 0u);
+        fw_key = rv.x;
+        fw_so = rv.y;
+      }
+      f_key = wave::readlane_u(fw_key, f_rank - fw_base);
+      f_so = wave::readlane_u(fw_so, f_rank - fw_base);
+    };
+    auto f_clear = [&](int r) {
+      const int j0 = r >> 6;
+      if (lane == 0) {
+        const uint64_t w = L0[j0] & ~(1ull << (r & 63));
+        L0[j0] = w;
+        if (w == 0ull) L1[j0 >> 6] &= ~(1ull << (j0 & 63));
+      }
+    };
+    auto v_find = [&]() {
+      uint32_t best = 0xFFFFFFFFu;
+      int32_t bp = -1;
+      for (int j = lane; j < nVe; j += 64) {
+        const uint32_t kv = vkey[j];
+        if (kv < best) {
+          best = kv;
+          bp = j;
+        }
+      }
+      v_key = wave::min_u32(best);
+      if (nVe == 0) {
+        v_pos = -1;
+        return;
+      }
+      const uint64_t who = wave::ballot(best == v_key && bp >= 0);
+      v_pos = wave::readlane(bp, __builtin_ctzll(who));
+      v_so = vso[v_pos];
+    };
+    // remove run at (row rr, lane ln): keep h exact for the others
+    auto remove_run = [&](int rr, int ln) {
+      int32_t xk = 0, ek = 0;
+#pragma unroll
+      for (int r = 0; r < ROWS; ++r)
+        if (r == rr) {
+          xk = wave::readlane(r_x[r], ln);
+          ek = wave::readlane(r_end[r], ln);
+        }
+#pragma unroll
+      for (int r = 0; r < ROWS; ++r)
+        if (r < rows_hi) {
+          const bool v = (vm[r] >> lane) & 1ull;
+          if (v && r_end[r] <= ek) r_h[r] -= xk + r_end[r] - t_r;
+        }
+#pragma unroll
+      for (int r = 0; r < ROWS; ++r)
+        if (r == rr) vm[r] &= ~(1ull << ln);
+      X -= xk;
+      N -= 1;
+      while (rows_hi > 0) {
+        bool empty = false;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r)
+          if (r == rows_hi - 1) empty = (vm[r] == 0ull);
+        if (!empty) break;
+        --rows_hi;
+      }
+      return xk;
+    };
+
+    int32_t t = 0;
+    for (;;) {
+      if (t > cap) {
+        status = SCHED_E_STEP_CAP;
+        break;
+      }
+      if (t - t_r >= kRebase) {
+        const int32_t d = t - t_r;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r)
+          if (r < rows_hi) {
+            r_x[r] += d;
+            r_h[r] -= d;
+          }
+        X += N * d;
+        t_r = t;
+      }
+      // ---- 1. arrivals (and last step's cancelled requests become eligible)
+      bool arrived = false;
+      while (arr_ptr < n) {
+        if (arr_ptr >= aw_base + 64) {
+          aw_base = arr_ptr;
+          const int i = aw_base + lane;
+          aw_a = i < n ? (arrival ? arrival[i] : 0) : 0x7FFFFFFF;
+          aw_rank = i < n ? rank_of[i] : 0;
+        }
+        const bool take = (aw_base + lane >= arr_ptr) && aw_a <= t;
+        const uint64_t m = wave::ballot(take);
+        if (m == 0ull) break;
+        if (take) {
+          atomicOr(reinterpret_cast<unsigned long long*>(&L0[aw_rank >> 6]), 1ull << (aw_rank & 63));
+          atomicOr(reinterpret_cast<unsigned long long*>(&L1[aw_rank >> 12]), 1ull << ((aw_rank >> 6) & 63));
+        }
+        arr_ptr += __builtin_popcountll(m);
+        arrived = true;
+        if (arr_ptr < aw_base + 64) break;
+      }
+      if (arrived) f_find();
+      if (ALGO == SCHED_AMIN && nVe != nV) {
+        nVe = nV;
+        v_find();
+      }
+
+      // ---- 2. completions at t; DT = memory they hold at t (s + o each)
+      int32_t DT = 0;
+#pragma unroll
+      for (int r = 0; r < ROWS; ++r)
+        if (r < rows_hi) {
+          const bool v = (vm[r] >> lane) & 1ull;
+          const bool hit = v && r_c[r] == t;
+          uint64_t m = wave::ballot(hit);
+          if (m) {
+            if (hit) completion[r_key[r] & kIdxMask] = t;
+            n_done += __builtin_popcountll(m);
+            while (m) {
+              const int ln = __builtin_ctzll(m);
+              m &= m - 1;
+              const int32_t xk = remove_run(r, ln);
+              DT += xk - t_r + t;
+            }
+          }
+        }
+      // ---- 3. done?
+      if (n_done == n) break;
+
+      // ---- 4. A_min: cancel in ascending (o~, index) while memory at t+1 > M
+      if (ALGO == SCHED_AMIN) {
+        int32_t Pm = X + N * (t + 1 - t_r);
+        while (Pm > M) {
+          uint32_t best = 0xFFFFFFFFu;
+#pragma unroll
+          for (int r = 0; r < ROWS; ++r)
+            if (r < rows_hi) {
+              const bool v = (vm[r] >> lane) & 1ull;
+              if (v && r_key[r] < best) best = r_key[r];
+            }
+          const uint32_t kmin = wave::min_u32(best);
+          int rr = -1, ln = 0;
+          int32_t ek = 0, ck = 0;
+#pragma unroll
+          for (int r = 0; r < ROWS; ++r)
+            if (r < rows_hi && rr < 0) {
+              const bool v = (vm[r] >> lane) & 1ull;
+              const uint64_t m = wave::ballot(v && r_key[r] == kmin);
+              if (m) {
+                rr = r;
+                ln = __builtin_ctzll(m);
+                ek = wave::readlane(r_end[r], ln);
+                ck = wave::readlane(r_c[r], ln);
+              }
+            }
+          if (rr < 0 || nV >= P.cap_v) {  // rr < 0 cannot happen while P > M > 0
+            status = SCHED_E_UNSUPPORTED;
+            break;
+          }
+          const int32_t xk = remove_run(rr, ln);
+          Pm -= xk + t + 1 - t_r;
+          const int32_t oh = static_cast<int32_t>(kmin >> kIdxBits);
+          const uint32_t idx = kmin & kIdxMask;
+          const int32_t pk = ek - oh;
+          const int32_t gen = t - pk;
+          const int32_t nh = gen > oh ? gen : oh;
+          const int32_t sk = xk - t_r + pk;
+          const int32_t ok = ck - pk;
+          if (lane == 0) {
+            vkey[nV] = (static_cast<uint32_t>(nh) << kIdxBits) | idx;
+            vso[nV] = static_cast<uint32_t>(sk) | (static_cast<uint32_t>(ok) << 16);
+            if (evictions) evictions[idx] += 1;
+          }
+          ++nV;
+          ++tot_ev;
+        }
+        if (status != SCHED_OK) break;
+      }
+
+      // ---- 5. admission of the longest feasible prefix in key order
+      for (;;) {
+        const bool hasF = f_rank >= 0;
+        const bool hasV = (ALGO == SCHED_AMIN) && v_pos >= 0;
+        if (!hasF && !hasV) break;
+        const bool fromF = hasF && (!hasV || f_key < v_key);
+        const uint32_t ck = fromF ? f_key : v_key;
+        const uint32_t cso = fromF ? f_so : v_so;
+        const int32_t est = static_cast<int32_t>(ck >> kIdxBits);
+        const int32_t s = static_cast<int32_t>(cso & 0xFFFFu);
+        const int32_t o = static_cast<int32_t>(cso >> 16);
+        const int32_t E = t + est;
+        const int32_t tp1 = t + 1;
+        int32_t hm = INT32_MIN, xs = 0, cnt = 0;
+        bool any_le = false, any_clamp = false;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r)
+          if (r < rows_hi) {
+            const bool v = (vm[r] >> lane) & 1ull;
+            const int32_t e = r_end[r];
+            const bool le = v && e <= E;
+            const bool ge = v && e >= E;  // raw planned ends: the invariant h is kept over
+            hm = (le && r_h[r] > hm) ? r_h[r] : hm;
+            xs += ge ? r_x[r] : 0;
+            cnt += __builtin_popcountll(wave::ballot(ge));
+            any_le |= wave::ballot(le) != 0ull;
+            any_clamp |= wave::ballot(v && e <= tp1) != 0ull;
+          }
+        const int32_t Pm = X + N * (tp1 - t_r);
+        bool ok = DT + X + N * (t - t_r) + s <= M;                  // step t
+        ok = ok && (!any_clamp || Pm + s + 1 <= M);                 // step t+1
+        const int32_t hmax = any_le ? wave::max_i32(hm) : 0;
+        ok = ok && (!any_le || hmax + t_r - t + s <= M);            // planned ends <= E
+        // f(E) over raw planned ends; at E = t+1 every run is present, which is Pm
+        const int32_t f = wave::sum_i32(xs) + cnt * (E - t_r);
+        ok = ok && ((E == tp1 ? Pm : f) + s + est <= M);            // E itself
+        if (!ok) break;
+        // admit: p = t
+        const int32_t xw = s - t + t_r;
+        const int32_t hw = f + (xw + E - t_r) + (E - t_r);
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r)
+          if (r < rows_hi) {
+            const bool v = (vm[r] >> lane) & 1ull;
+            if (v && r_end[r] <= E) r_h[r] += xw + r_end[r] - t_r;
+          }
+        int rr = -1;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r)
+          if (rr < 0 && vm[r] != ~0ull) rr = r;
+        if (rr < 0) {
+          status = SCHED_E_UNSUPPORTED;
+          break;
+        }
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r)
+          if (r == rr) {
+            const int ln = __builtin_ctzll(~vm[r]);
+            if (lane == ln) {
+              r_end[r] = E;
+              r_x[r] = xw;
+              r_c[r] = t + o;
+              r_key[r] = ck;
+              r_h[r] = hw;
+            }
+            vm[r] |= 1ull << ln;
+          }
+        rows_hi = rr + 1 > rows_hi ? rr + 1 : rows_hi;
+        X += xw;
+        N += 1;
+        if (fromF) {
+          f_clear(f_rank);
+          f_find();
+        } else {
+          // remove eligible entry v_pos: last eligible moves in, last pending fills its place
+          if (lane == 0) {
+            const int le = nVe - 1;
+            vkey[v_pos] = vkey[le];
+            vso[v_pos] = vso[le];
+            if (nV > nVe) {
+              vkey[le] = vkey[nV - 1];
+              vso[le] = vso[nV - 1];
+            }
+          }
+          --nVe;
+          --nV;
+          v_find();
+        }
+      }
+      if (status != SCHED_OK) break;
+
+      // ---- 6. this step processes every running request once
+      rsteps += N;
+      if (N == 0 && f_rank < 0 && nV == 0 && arr_ptr < n) {
+        // nothing runs or waits: jump to the next arrival
+        if (arr_ptr >= aw_base + 64) {
+          aw_base = arr_ptr;
+          const int i = aw_base + lane;
+          aw_a = i < n ? (arrival ? arrival[i] : 0) : 0x7FFFFFFF;
+          aw_rank = i < n ? rank_of[i] : 0;
+        }
+        const int32_t na = wave::readlane(aw_a, arr_ptr - aw_base);
+        t = na > t + 1 ? na : t + 1;
+      } else {
+        t += 1;
+      }
+    }
+  }
+
+  // ---- epilogue: totals from the per-request outputs
+  __syncthreads();
+  const bool keep = (status == SCHED_OK || status == SCHED_E_STEP_CAP) && n > 0;
+  int64_t tel = 0, mk = 0;
+  if (keep) {
+    for (int c = 0; c < n; c += 64) {
+      const int i = c + lane;
+      if (i < n) {
+        const int32_t ci = P.completion[b + i];
+        if (ci >= 0) {
+          tel += ci - (P.arrival ? P.arrival[b + i] : 0);
+          mk = ci > mk ? ci : mk;
+        }
+      }
+    }
+  } else if (status != st0 && n > 0) {
+    // a run-time capacity failure: report like an invalid instance
+    for (int c = 0; c < n; c += 64) {
+      const int i = c + lane;
+      if (i < n) {
+        P.completion[b + i] = -1;
+        if (P.evictions) P.evictions[b + i] = 0;
+      }
+    }
+  }
+  tel = wave::sum_i64(tel);
+  mk = wave::max_i64(mk);
+  if (!keep) {
+    rsteps = 0;
+    tot_ev = 0;
+  }
+  if (lane == 0) {
+    P.total_latency[k] = tel;
+    if (P.makespan) P.makespan[k] = static_cast<int32_t>(mk);
+    if (P.request_steps) P.request_steps[k] = rsteps;
+    if (P.total_evictions) P.total_evictions[k] = tot_ev;
+    P.status[k] = status;
+  }
+}
+
+}  // namespace sk
+
+// ---------------------------------------------------------------------------
+// host side: the C ABI
+// ---------------------------------------------------------------------------
+namespace {
+
+template <int ALGO>
+hipError_t launch_sim(int rows, const sk::Params& P, size_t lds, hipStream_t st) {
+  const dim3 grid(P.K), block(64);
+  switch (rows) {
+    case 1: hipLaunchKernelGGL((sk::k_simulate<ALGO, 1>), grid, block, lds, st, P); break;
+    case 2: hipLaunchKernelGGL((sk::k_simulate<ALGO, 2>), grid, block, lds, st, P); break;
+    case 4: hipLaunchKernelGGL((sk::k_simulate<ALGO, 4>), grid, block, lds, st, P); break;
+    case 8: hipLaunchKernelGGL((sk::k_simulate<ALGO, 8>), grid, block, lds, st, P); break;
+    default: hipLaunchKernelGGL((sk::k_simulate<ALGO, 16>), grid, block, lds, st, P); break;
+  }
+  return hipGetLastError();
+}
+
+template <int ALGO>
+hipError_t set_lds_limit(int rows, int bytes) {
+  const void* f;
+  switch (rows) {
+    case 1: f = reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 1>); break;
+    case 2: f = reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 2>); break;
+    case 4: f = reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 4>); break;
+    case 8: f = reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8>); break;
+    default: f = reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16>); break;
+  }
+  return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+}
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+}  // namespace
+
+extern "C" {
+
+int sched_version(void) { return 100; }
+
+const char* sched_strerror(int code) {
+  switch (code) {
+    case SCHED_OK: return "ok";
+    case SCHED_E_INVAL: return "invalid argument";
+    case SCHED_E_INTERVAL: return "invalid request data (o < 1, s < 0, or interval does not contain o)";
+    case SCHED_E_TOO_BIG: return "a request can never fit in M";
+    case SCHED_E_STEP_CAP: return "step cap reached with unfinished requests";
+    case SCHED_E_HIP: return "HIP runtime error";
+    case SCHED_E_UNSUPPORTED: return "beyond kernel capacity";
+    case SCHED_E_ARRIVAL: return "arrivals negative or not non-decreasing";
+    default: return "unknown code";
+  }
+}
+
+int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t M,
+                        const sched_results_t* out, void* stream, const sched_options_t* opts) {
+  if (!in || !out) return SCHED_E_INVAL;
+  if (algo != SCHED_AMAX && algo != SCHED_AMIN && algo != SCHED_HSF) return SCHED_E_INVAL;
+  if (M <= 0 || M >= (int64_t(1) << 30)) return SCHED_E_INVAL;
+  if (in->num_instances < 0 || in->max_requests < 0 || in->total_requests < 0) return SCHED_E_INVAL;
+  if (in->num_instances == 0) return SCHED_OK;
+  if (!in->offsets || !out->total_latency || !out->status) return SCHED_E_INVAL;
+  if (in->total_requests > 0 && (!in->prompt || !in->output || !out->completion)) return SCHED_E_INVAL;
+  if (in->total_requests > 0 && algo == SCHED_AMIN && !in->lower) return SCHED_E_INVAL;
+  if (in->total_requests > 0 && algo == SCHED_AMAX && !in->upper) return SCHED_E_INVAL;
+  if (in->max_requests >= (1 << sk::kIdxBits)) return SCHED_E_UNSUPPORTED;
+  sched_options_t o{};
+  if (opts) o = *opts;
+  if (o.step_cap > sk::kCapLimit) return SCHED_E_INVAL;
+  if (o.running_capacity < 0 || o.evicted_capacity < 0) return SCHED_E_INVAL;
+
+  const int64_t nmax = in->max_requests;
+  int run_cap = o.running_capacity > 0 ? o.running_capacity
+                                       : static_cast<int>(std::min<int64_t>((nmax + 63) / 64 * 64, 1024));
+  if (run_cap > 1024) return SCHED_E_UNSUPPORTED;
+  int rows = (run_cap + 63) / 64;
+  rows = rows <= 1 ? 1 : rows <= 2 ? 2 : rows <= 4 ? 4 : rows <= 8 ? 8 : 16;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return SCHED_E_HIP;
+  int lds_max = 0;
+  if (hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+    return SCHED_E_HIP;
+
+  const int nw = static_cast<int>((nmax + 63) / 64);
+  const int nw1 = (nw + 63) / 64;
+  int cap_v = 0;
+  if (algo == SCHED_AMIN) {
+    const int64_t def = in->num_instances <= 64 ? 16384 : 1024;
+    cap_v = o.evicted_capacity > 0 ? o.evicted_capacity : static_cast<int>(std::min<int64_t>(std::max<int64_t>(nmax, 1), def));
+  }
+  const size_t lds = 8 * static_cast<size_t>(nw + nw1) + 8 * static_cast<size_t>(cap_v);
+  if (lds > static_cast<size_t>(lds_max)) return SCHED_E_UNSUPPORTED;
+
+  const size_t N = static_cast<size_t>(in->total_requests);
+  const size_t K = static_cast<size_t>(in->num_instances);
+  size_t off = 0;
+  const size_t o_sa = off; off = align_up(off + 4 * N, 256);
+  const size_t o_sb = off; off = align_up(off + 4 * N, 256);
+  const size_t o_rec = off; off = align_up(off + 8 * N, 256);
+  const size_t o_rk = off; off = align_up(off + 4 * N, 256);
+  const size_t o_cap = off; off = align_up(off + 4 * K, 256);
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, off, st) != hipSuccess) return SCHED_E_HIP;
+  char* base = static_cast<char*>(ws);
+
+  sk::Params P{};
+  P.K = in->num_instances;
+  P.max_requests = in->max_requests;
+  P.N = in->total_requests;
+  P.offsets = in->offsets;
+  P.arrival = in->arrival;
+  P.prompt = in->prompt;
+  P.output = in->output;
+  P.lower = in->lower;
+  P.upper = in->upper;
+  P.completion = out->completion;
+  P.evictions = out->evictions;
+  P.total_latency = out->total_latency;
+  P.makespan = out->makespan;
+  P.request_steps = out->request_steps;
+  P.total_evictions = out->total_evictions;
+  P.status = out->status;
+  P.M = static_cast<int32_t>(M);
+  P.step_cap = o.step_cap;
+  P.sort_a = reinterpret_cast<uint32_t*>(base + o_sa);
+  P.sort_b = reinterpret_cast<uint32_t*>(base + o_sb);
+  P.rec = reinterpret_cast<uint2*>(base + o_rec);
+  P.rank_of = reinterpret_cast<int32_t*>(base + o_rk);
+  P.cap = reinterpret_cast<int32_t*>(base + o_cap);
+  P.nw_max = nw;
+  P.nw1_max = nw1;
+  P.cap_v = cap_v;
+
+  hipError_t err = hipSuccess;
+  const dim3 grid(P.K), block(64);
+  switch (algo) {
+    case SCHED_AMAX: hipLaunchKernelGGL((sk::k_prepare<SCHED_AMAX>), grid, block, 0, st, P); break;
+    case SCHED_AMIN: hipLaunchKernelGGL((sk::k_prepare<SCHED_AMIN>), grid, block, 0, st, P); break;
+    default: hipLaunchKernelGGL((sk::k_prepare<SCHED_HSF>), grid, block, 0, st, P); break;
+  }
+  err = hipGetLastError();
+  if (err == hipSuccess && lds > 65536) {
+    switch (algo) {
+      case SCHED_AMAX: err = set_lds_limit<SCHED_AMAX>(rows, static_cast<int>(lds)); break;
+      case SCHED_AMIN: err = set_lds_limit<SCHED_AMIN>(rows, static_cast<int>(lds)); break;
+      default: err = set_lds_limit<SCHED_HSF>(rows, static_cast<int>(lds)); break;
+    }
+  }
+  if (err == hipSuccess && o.event_before) err = hipEventRecord(static_cast<hipEvent_t>(o.event_before), st);
+  if (err == hipSuccess) {
+    switch (algo) {
+      case SCHED_AMAX: err = launch_sim<SCHED_AMAX>(rows, P, lds, st); break;
+      case SCHED_AMIN: err = launch_sim<SCHED_AMIN>(rows, P, lds, st); break;
+      default: err = launch_sim<SCHED_HSF>(rows, P, lds, st); break;
+    }
+  }
+  if (err == hipSuccess && o.event_after) err = hipEventRecord(static_cast<hipEvent_t>(o.event_after), st);
+  const hipError_t ferr = hipFreeAsync(ws, st);
+  if (err != hipSuccess || ferr != hipSuccess) return SCHED_E_HIP;
+  return SCHED_OK;
+}
+
+int sched_simulate(const sched_instances_t* in, sched_algo_t algo, int64_t M,
+                   const sched_results_t* out, void* stream) {
+  return sched_simulate_opts(in, algo, M, out, stream, nullptr);
+}
+
+}  // extern "C"

@@ -1,0 +1,248 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Integer outputs must match bit-exactly: per-request completion steps and
+cancellation counts, per-instance total latency, makespan, request-steps,
+total cancellations and status.
+"""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2508_14544_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+ALGOS = {"amax": O.AMAX, "amin": O.AMIN, "hsf": O.HSF}
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def B():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2508_14544_amd import binding
+    binding.load_library()
+    return binding
+
+
+def gpu_run(B, batch, algo, *, pass_upper=True, **opts):
+    import torch
+    _say(f"[gpu] {batch.name} K={batch.num_instances} N={batch.total_requests} algo={algo} opts={opts}")
+    db = B.to_device(batch)
+    out = B.simulate(db, algo, pass_upper=pass_upper, **opts)
+    torch.cuda.synchronize()
+    return {k: (None if v is None else v.cpu().numpy()) for k, v in out.items()}
+
+
+def oracle_run(batch, algo, instances=None, step_cap=0):
+    return O.simulate_batch(batch, algo, instances=instances, step_cap=step_cap)
+
+
+def assert_parity(batch, g, ref, instances=None):
+    ks = list(range(batch.num_instances)) if instances is None else list(instances)
+    assert g["status"][ks].tolist() == ref["status"].tolist()
+    assert g["tel"][ks].tolist() == ref["tel"].tolist()
+    assert g["makespan"][ks].tolist() == ref["makespan"].tolist()
+    assert g["request_steps"][ks].tolist() == ref["request_steps"].tolist()
+    assert g["total_evictions"][ks].tolist() == ref["total_evictions"].tolist()
+    sel = np.concatenate([np.arange(batch.offsets[k], batch.offsets[k + 1]) for k in ks]) if ks else np.zeros(0, int)
+    sel = sel.astype(np.int64)
+    assert np.array_equal(g["completion"][sel], ref["completion"])
+    assert np.array_equal(g["evictions"][sel], ref["evictions"])
+
+
+def _golden():
+    here = os.path.join(os.path.dirname(__file__), "golden")
+    files = [os.path.join(here, f) for f in sorted(os.listdir(here)) if f.endswith(".json")]
+    return [f for f in files if "instance" in json.load(open(f))]
+
+
+@pytest.mark.parametrize("path", _golden(), ids=os.path.basename)
+def test_paper_examples(B, path):
+    g = json.load(open(path))
+    batch = W.from_lists(g["M"], [g["instance"]], name=os.path.basename(path))
+    for name, exp in g["expected"].items():
+        out = gpu_run(B, batch, ALGOS[name])
+        assert int(out["status"][0]) == 0
+        assert out["completion"].tolist() == exp["completion"]
+        assert int(out["tel"][0]) == exp["tel"]
+        for f in ("evictions",):
+            if f in exp:
+                assert out[f].tolist() == exp[f]
+        for f in ("makespan", "request_steps"):
+            if f in exp:
+                assert int(out[f][0]) == exp[f]
+
+
+@pytest.mark.parametrize("algo", ["amax", "amin", "hsf"])
+@pytest.mark.parametrize("seed,arrivals", [(0, True), (1, False), (2, True)])
+def test_random_small(B, algo, seed, arrivals):
+    batch = W.random_small(seed, 300, 12, s_max=6, o_max=10, M=30, arrivals=arrivals)
+    g = gpu_run(B, batch, ALGOS[algo])
+    assert_parity(batch, g, oracle_run(batch, ALGOS[algo]))
+
+
+@pytest.mark.parametrize("algo", ["amax", "amin", "hsf"])
+def test_random_medium_ragged(B, algo):
+    # instances of 0..150 requests (empty ones included), several rows of 64 lanes
+    rng = np.random.default_rng(5)
+    insts = []
+    for k in range(200):
+        n = int(rng.integers(0, 151)) if k % 17 else 0
+        o = rng.integers(1, 40, n)
+        l = np.maximum(1, (o * rng.uniform(0.3, 1.0, n)).astype(int))
+        u = o + rng.integers(0, 30, n)
+        s = rng.integers(0, 20, n)
+        a = np.sort(rng.integers(0, 60, n)) if k % 2 else np.zeros(n, int)
+        insts.append({"arrival": a, "prompt": s, "output": o, "lower": l, "upper": u})
+    batch = W.from_lists(400, insts, name="ragged")
+    g = gpu_run(B, batch, ALGOS[algo])
+    assert_parity(batch, g, oracle_run(batch, ALGOS[algo]))
+
+
+@pytest.mark.parametrize("algo", ["amax", "amin", "hsf"])
+def test_single_n200(B, algo):
+    batch = W.generate("single_n200_m512", 0)
+    g = gpu_run(B, batch, ALGOS[algo])
+    assert_parity(batch, g, oracle_run(batch, ALGOS[algo]))
+
+
+@pytest.mark.parametrize("cap", [384, 512, 1024])
+def test_launch_shape_independence(B, cap):
+    # 8 and 16 register rows per lane give the same bits (the default here is 16 rows)
+    batch = W.generate("batch4096_n1000_m16384", 0, instance_ids=range(0, 4096, 97))
+    ref = gpu_run(B, batch, O.AMIN)
+    g = gpu_run(B, batch, O.AMIN, running_capacity=cap)
+    for f in ("status", "tel", "makespan", "request_steps", "total_evictions", "completion", "evictions"):
+        assert np.array_equal(ref[f], g[f]), f
+
+
+@pytest.mark.parametrize("cap", [150, 192, 512, 1024])
+def test_row_variants_against_oracle(B, cap):
+    # 3 -> 4, 4, 8 and 16 register rows on instances of up to 150 requests
+    rng = np.random.default_rng(11)
+    insts = []
+    for k in range(120):
+        n = int(rng.integers(1, 151))
+        o = rng.integers(1, 30, n)
+        insts.append({"arrival": np.zeros(n, int), "prompt": rng.integers(0, 4, n), "output": o,
+                      "lower": np.maximum(1, o // 2), "upper": o + 5})
+    batch = W.from_lists(600, insts, name="rows")
+    for algo in (O.AMAX, O.AMIN, O.HSF):
+        g = gpu_run(B, batch, algo, running_capacity=cap)
+        assert_parity(batch, g, oracle_run(batch, algo))
+
+
+def test_errors_and_statuses(B):
+    good = {"arrival": [0, 1, 1], "prompt": [1, 2, 1], "output": [3, 2, 4], "lower": [1, 2, 2], "upper": [4, 2, 6]}
+    insts = [
+        good,
+        dict(good, lower=[4, 2, 2]),          # l > o
+        dict(good, lower=[0, 2, 2]),          # l < 1
+        dict(good, output=[0, 2, 4]),         # o < 1
+        dict(good, prompt=[-1, 2, 1]),        # s < 0
+        dict(good, prompt=[1, 2, 9]),         # s + o > M
+        dict(good, arrival=[1, 0, 1]),        # unsorted
+        dict(good, arrival=[-2, 0, 1]),       # negative
+        {"arrival": [], "prompt": [], "output": [], "lower": [], "upper": []},
+        good,
+    ]
+    batch = W.from_lists(10, insts, name="errors")
+    for algo in (O.AMAX, O.AMIN, O.HSF):
+        g = gpu_run(B, batch, algo)
+        assert_parity(batch, g, oracle_run(batch, algo))
+    # A_max-specific: u < o and s + u > M
+    insts2 = [good, dict(good, upper=[2, 2, 6]), dict(good, upper=[4, 2, 10])]
+    b2 = W.from_lists(10, insts2, name="errors_amax")
+    g = gpu_run(B, b2, O.AMAX)
+    assert g["status"].tolist() == [0, O.E_INTERVAL, O.E_TOO_BIG]
+    assert_parity(b2, g, oracle_run(b2, O.AMAX))
+
+
+@pytest.mark.parametrize("cap", [1, 5, 15, 60])
+def test_step_cap(B, cap):
+    batch = W.random_small(3, 100, 10, s_max=6, o_max=10, M=30)
+    for algo in (O.AMAX, O.AMIN, O.HSF):
+        g = gpu_run(B, batch, algo, step_cap=cap)
+        ref = oracle_run(batch, algo, step_cap=cap)
+        if cap <= 5:
+            assert (ref["status"] == O.E_STEP_CAP).any()
+        assert_parity(batch, g, ref)
+
+
+def test_capacity_overflow_reported(B):
+    # 200 requests that all fit at once need more than 64 running slots
+    n = 200
+    batch = W.from_lists(10 ** 6, [{"prompt": [1] * n, "output": [5] * n, "lower": [5] * n, "upper": [5] * n}])
+    g = gpu_run(B, batch, O.HSF, running_capacity=64)
+    assert int(g["status"][0]) == -6 and (g["completion"] == -1).all()
+    g = gpu_run(B, batch, O.HSF, running_capacity=256)
+    assert int(g["status"][0]) == 0 and (g["completion"] == 5).all()
+
+
+def test_determinism_and_chunking(B):
+    batch = W.generate("batch4096_n1000_m16384", 0, instance_ids=range(1000, 1300))
+    a = gpu_run(B, batch, O.AMIN)
+    b = gpu_run(B, batch, O.AMIN)
+    for f in a:
+        if a[f] is not None:
+            assert np.array_equal(a[f], b[f]), f
+    h1 = gpu_run(B, batch.subset(range(0, 150)), O.AMIN)
+    h2 = gpu_run(B, batch.subset(range(150, 300)), O.AMIN)
+    assert np.array_equal(np.concatenate([h1["tel"], h2["tel"]]), a["tel"])
+    assert np.array_equal(np.concatenate([h1["completion"], h2["completion"]]), a["completion"])
+
+
+@pytest.mark.parametrize("algo", ["amin", "amax", "hsf"])
+def test_batch4096_full(B, algo):
+    # the benchmark workload, in the launch configuration the benchmark times
+    batch = W.generate("batch4096_n1000_m16384", 0)
+    g = gpu_run(B, batch, ALGOS[algo])
+    if algo == "amin":
+        ks = None  # every instance
+    else:
+        ks = list(range(0, 4096, 16)) + [1364, 1365, 2729, 2730, 4095]
+    _say(f"[oracle] batch4096 {algo} on {'all' if ks is None else len(ks)} instances")
+    assert_parity(batch, g, oracle_run(batch, ALGOS[algo], instances=ks), instances=ks)
+
+
+@pytest.mark.parametrize("algo", ["amin", "amax"])
+def test_online1024_sampled(B, algo):
+    batch = W.generate("online1024_n10000_m65536", 0)
+    g = gpu_run(B, batch, ALGOS[algo])
+    ks = [0, 1, 511, 1023] + list(range(100, 1024, 128))
+    assert_parity(batch, g, oracle_run(batch, ALGOS[algo], instances=ks), instances=ks)
+
+
+def test_sweep65536_sampled(B):
+    # A_min receives only lower bounds here
+    batch = W.generate("sweep65536_n2000_m32768", 0, with_upper=False)
+    g = gpu_run(B, batch, O.AMIN, pass_upper=False)
+    assert (g["status"] == 0).all()
+    ks = [0, 1, 7280, 7281, 14562, 21843, 29124, 36405, 43686, 50967, 58248, 65535] + list(range(333, 65536, 8192))
+    assert_parity(batch, g, oracle_run(batch, O.AMIN, instances=ks), instances=ks)
+
+
+def test_single_n100000_against_stored_digest(B):
+    path = os.path.join(os.path.dirname(__file__), "golden", "oracle_digests.json")
+    digests = json.load(open(path))["single_n100000_m1048576"]
+    batch = W.generate("single_n100000_m1048576", 0)
+    import hashlib
+    for name, d in digests.items():
+        g = gpu_run(B, batch, ALGOS[name])
+        assert int(g["status"][0]) == d["status"]
+        assert int(g["tel"][0]) == d["tel"]
+        assert int(g["makespan"][0]) == d["makespan"]
+        assert int(g["request_steps"][0]) == d["request_steps"]
+        assert int(g["total_evictions"][0]) == d["total_evictions"]
+        assert hashlib.sha256(g["completion"].astype("<i4").tobytes()).hexdigest() == d["completion_sha256"]
+        assert hashlib.sha256(g["evictions"].astype("<i4").tobytes()).hexdigest() == d["evictions_sha256"]
