@@ -1,0 +1,226 @@
+"""Benchmark: simulated request-steps per second of A_min on 4096 instances x
+n=1000 (M=16384), one MI355X.
+
+A step is one full simulation of the whole batch (every instance from t=0 to
+its last completion) through the C ABI: the per-instance preparation kernel
+and the simulation kernel.  Inputs are resident in HBM before timing starts.
+
+Prints one JSON line.  Also reports the roofline of the simulation kernel
+(int32 VALU lane-operations; see the design doc for the per-request-step figure)
+and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = int32 VALU lane-operations per second
+PEAK_INT32_LANE_OPS = 256 * 4 * 16 * 2.4e9
+# algorithmic int32 lane-operations per simulated request-step ("Roofline")
+OPS_PER_REQUEST_STEP = 6
+METRIC = "simulated request-steps/sec (A_min, 4096×n=1000) + % VALU/LDS roofline"
+SIM_KERNEL = "k_simulate"
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in ("paper_2508_14544_amd/csrc/sched_kernels.hip", "paper_2508_14544_amd/csrc/wave.hpp"):
+        h.update(open(os.path.join(ROOT, p), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload: str, algo: str):
+    """HBM bytes per launch from committed rocprofv3 --pmc counters, if still current."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{SIM_KERNEL}_{algo}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    d = json.load(open(path))
+    if d.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+class HipEvent:
+    """A raw hipEvent_t (timing enabled), recorded by the library on its launch stream."""
+    _hip = None
+
+    def __init__(self):
+        import ctypes
+        if HipEvent._hip is None:
+            lib = ctypes.CDLL("libamdhip64.so")
+            lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+            lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            HipEvent._hip = lib
+        self.h = ctypes.c_void_p()
+        if HipEvent._hip.hipEventCreate(ctypes.byref(self.h)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        self.cuda_event = self.h.value
+
+    def elapsed_ms(self, end: "HipEvent") -> float:
+        import ctypes
+        ms = ctypes.c_float()
+        if HipEvent._hip.hipEventElapsedTime(ctypes.byref(ms), self.h, end.h) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def __del__(self):
+        try:
+            HipEvent._hip.hipEventDestroy(self.h)
+        except Exception:
+            pass
+
+
+def cpu_baseline(batch, algo, g_out, target_s: float, threads: int):
+    """Time the oracle on a bounded sample of instances; check parity on it."""
+    import numpy as np
+    from oracle import oracle as O
+
+    K = batch.num_instances
+    probe = list(range(0, K, max(1, K // threads)))[:threads]
+    t0 = time.perf_counter()
+    O.simulate_batch(batch, algo, instances=probe, threads=threads)
+    per = (time.perf_counter() - t0) / max(1, len(probe))  # wall per instance with `threads` in flight
+    want = int(max(threads, min(K, target_s / max(per, 1e-6))))
+    stride = max(1, K // want)
+    sample = list(range(0, K, stride))[:want]
+    t0 = time.perf_counter()
+    ref = O.simulate_batch(batch, algo, instances=sample, threads=threads)
+    wall = time.perf_counter() - t0
+    rs = int(ref["request_steps"].sum())
+    ok = (g_out["tel"][sample].tolist() == ref["tel"].tolist()
+          and g_out["request_steps"][sample].tolist() == ref["request_steps"].tolist()
+          and g_out["status"][sample].tolist() == ref["status"].tolist())
+    sel = np.concatenate([np.arange(batch.offsets[k], batch.offsets[k + 1]) for k in sample])
+    ok = ok and np.array_equal(g_out["completion"][sel], ref["completion"])
+    ok = ok and np.array_equal(g_out["evictions"][sel], ref["evictions"])
+    return {
+        "value": rs / wall, "unit": "request-steps/s", "cores": threads, "kind": "oracle",
+        "sample": f"{len(sample)} of {K} instances (every {stride}th), {rs} request-steps in {wall:.1f} s",
+    }, bool(ok)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="batch4096_n1000_m16384")
+    ap.add_argument("--algo", default="amin", choices=["amin", "amax", "hsf"])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--running-capacity", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
+    ap.add_argument("--cpu-threads", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after timing, run device copies of this size (for rocprofv3 counter calibration)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only; the instances of a batch are "
+                                   "independent, and sharding them across GPUs is described in DESIGN.md"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2508_14544_amd import binding as B
+    from paper_2508_14544_amd import workloads as W
+
+    B.load_library()
+    algo = B.ALGOS[args.algo]
+    batch = W.generate(args.workload, args.seed)
+    dev = torch.device("cuda:0")
+    db = B.to_device(batch, dev)
+    out = B.alloc_results(db)
+    stream = torch.cuda.current_stream(dev)
+    kw = dict(stream=stream, running_capacity=args.running_capacity)
+
+    for _ in range(args.warmup):
+        B.simulate_into(db, algo, out, **kw)
+    torch.cuda.synchronize()
+
+    ev = [(HipEvent(), HipEvent()) for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(args.steps):
+        B.simulate_into(db, algo, out, event_before=ev[i][0], event_after=ev[i][1], **kw)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    step_ms = t_start.elapsed_time(t_end) / args.steps
+    sim_ms = [a.elapsed_ms(b) for a, b in ev]
+    sim_avg_ms = sum(sim_ms) / len(sim_ms)
+
+    g = {k: (None if v is None else v.cpu().numpy()) for k, v in out.items()}
+    status_ok = bool((g["status"] == 0).all())
+    rs = int(g["request_steps"].sum())
+    value = rs / (step_ms / 1e3)
+
+    if args.calib_copy_mib > 0:
+        nbytes = args.calib_copy_mib << 20
+        src = torch.empty(nbytes // 4, dtype=torch.int32, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    achieved = OPS_PER_REQUEST_STEP * rs / (sim_avg_ms / 1e3)
+    traffic = load_traffic(args.workload, args.algo)
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "request-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload,
+            "algo": {"amin": "A_min", "amax": "A_max", "hsf": "H-SF"}[args.algo],
+            "instances": batch.num_instances,
+            "requests_per_instance": W.WORKLOADS[args.workload].n,
+            "M": batch.M,
+            "seed": args.seed,
+            "request_steps_per_step": rs,
+            "instance_steps_per_step": int(g["makespan"].astype(np.int64).sum()),
+            "all_status_ok": status_ok,
+        },
+        "roofline": {
+            "kernel": SIM_KERNEL,
+            "bound": "alu",
+            "achieved": achieved / 1e12,
+            "peak": PEAK_INT32_LANE_OPS / 1e12,
+            "unit": "TOP/s",
+            "frac": achieved / PEAK_INT32_LANE_OPS,
+            "traffic": traffic,
+            "kernel_ms": sim_avg_ms,
+            "ops_per_request_step": OPS_PER_REQUEST_STEP,
+        },
+        "wall_s_timed_region": wall,
+    }
+    if not args.no_cpu_baseline:
+        threads = args.cpu_threads or min(16, os.cpu_count() or 1)
+        cb, parity = cpu_baseline(batch, algo, g, args.cpu_seconds, threads)
+        result["cpu_baseline"] = cb
+        result["parity_on_cpu_sample"] = parity
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

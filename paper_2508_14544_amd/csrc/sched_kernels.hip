@@ -76,6 +76,7 @@ struct Params {
   int32_t nw_max;        // 64-bit words of the level-0 bitmap
   int32_t nw1_max;       // 64-bit words of the level-1 bitmap
   int32_t cap_v;         // evicted-set capacity
+  int32_t retry_status;  // status for an outgrown running set: retry pass or SCHED_E_UNSUPPORTED
 };
 
 // ---------------------------------------------------------------------------
@@ -216,12 +217,32 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
 // ---------------------------------------------------------------------------
 // k_simulate
 // ---------------------------------------------------------------------------
-template <int ALGO, int ROWS>
+// Internal status of a first pass whose running set outgrew its register rows;
+// the retry pass (more rows) re-runs exactly those instances.
+constexpr int kRetry = -100;
+// r_end of an empty slot of the running set (below every planned end)
+constexpr int32_t kEmpty = INT32_MIN;
+
+__device__ __forceinline__ uint64_t uniform_u64(uint64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ uint32_t uniform_u32(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int32_t>(v)));
+}
+
+template <int ALGO, int ROWS, bool RETRY_PASS>
 __global__ __launch_bounds__(64) void k_simulate(Params P) {
   extern __shared__ uint64_t lds64[];
   const int k = blockIdx.x;
   const int lane = threadIdx.x;
-  const int st0 = P.status[k];
+  int st0 = P.status[k];
+  if (RETRY_PASS) {
+    if (st0 != kRetry) return;
+    st0 = SCHED_OK;
+  }
   const int64_t b = P.offsets[k];
   const int n = (st0 == SCHED_OK) ? static_cast<int>(P.offsets[k + 1] - b) : 0;
   const int32_t M = P.M;
@@ -247,109 +268,134 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
     int32_t* completion = P.completion + b;
     int32_t* evictions = P.evictions ? P.evictions + b : nullptr;
 
-    // running set
+    // running set: register rows; an empty slot has r_end = kEmpty, r_c = -1, r_key = ~0
     int32_t r_end[ROWS], r_x[ROWS], r_c[ROWS], r_h[ROWS];
     uint32_t r_key[ROWS];
-    uint64_t vm[ROWS];
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) {
-      r_end[r] = 0; r_x[r] = 0; r_c[r] = -1; r_h[r] = 0; r_key[r] = 0; vm[r] = 0;
+      r_end[r] = kEmpty; r_x[r] = 0; r_c[r] = -1; r_h[r] = 0; r_key[r] = 0xFFFFFFFFu;
     }
-    int rows_hi = 0;      // rows [0, rows_hi) may hold runs
-    int32_t N = 0;        // number of runs
-    int32_t X = 0;        // sum of x over runs
-    int32_t t_r = 0;      // base step of x and h
+    int rows_hi = 0;              // rows [0, rows_hi) may hold runs
+    int32_t N = 0;                // number of runs
+    int32_t X = 0;                // sum of x over runs
+    int32_t t_r = 0;              // base step of x and h
+    int32_t next_c = 0x7FFFFFFF;  // lower bound on the earliest completion step
 
-    // arrivals window: lane j holds request aw_base + j
-    int32_t aw_base = -64, aw_a = 0, aw_rank = 0;
-    int32_t arr_ptr = 0;
-    // fresh-waiting head and window of ranked records
+    int32_t aw_base = -64, aw_a = 0x7FFFFFFF, aw_rank = 0, arr_ptr = 0;
+    int32_t next_a = 0;           // arrival step of request arr_ptr (0: look at step 0)
     int32_t f_rank = -1, fw_base = -1;
-    uint32_t f_key = 0, f_so = 0, fw_key = 0, fw_so = 0;
-    // evicted-waiting set
+    uint32_t f_key = 0xFFFFFFFFu, f_so = 0, fw_key = 0xFFFFFFFFu, fw_so = 0;
     int32_t nV = 0, nVe = 0, v_pos = -1;
     uint32_t v_key = 0xFFFFFFFFu, v_so = 0;
     int32_t n_done = 0;
+    // cached head of the waiting set (smaller key of the two heads)
+    bool c_any = false, c_fromF = false;
+    uint32_t c_key = 0;
+    int32_t c_est = 0, c_s = 0, c_o = 0;
+    // the head cannot start before retry_at; valid until the next event
+    int32_t retry_at = 0;
 
-    auto f_find = [&]() {
-      const uint64_t w1 = lane < nw1 ? L1[lane] : 0ull;
-      const uint64_t nz = wave::ballot(w1 != 0ull);
-      if (nz == 0ull) {
-        f_rank = -1;
-        return;
-      }
-      const int j1 = __builtin_ctzll(nz);
-      const uint64_t w1v = wave::readlane_u64(w1, j1);
-      const int j0 = j1 * 64 + __builtin_ctzll(w1v);
-      const uint64_t w0 = L0[j0];
-      f_rank = j0 * 64 + __builtin_ctzll(w0);
-      if (fw_base < 0 || f_rank < fw_base || f_rank >= fw_base + 64) {
-        fw_base = f_rank;
-        const int rr = fw_base + lane;
-        const uint2 rv = rr < n ? rec[rr] : make_uint2(0xFFFFFFFFu, 0u);
-        fw_key = rv.x;
-        fw_so = rv.y;
-      }
-      f_key = wave::readlane_u(fw_key, f_rank - fw_base);
-      f_so = wave::readlane_u(fw_so, f_rank - fw_base);
-    };
-    auto f_clear = [&](int r) {
-      const int j0 = r >> 6;
-      if (lane == 0) {
-        const uint64_t w = L0[j0] & ~(1ull << (r & 63));
-        L0[j0] = w;
-        if (w == 0ull) L1[j0 >> 6] &= ~(1ull << (j0 & 63));
-      }
-    };
-    auto v_find = [&]() {
-      uint32_t best = 0xFFFFFFFFu;
-      int32_t bp = -1;
-      for (int j = lane; j < nVe; j += 64) {
-        const uint32_t kv = vkey[j];
-        if (kv < best) {
-          best = kv;
-          bp = j;
-        }
-      }
-      v_key = wave::min_u32(best);
-      if (nVe == 0) {
-        v_pos = -1;
-        return;
-      }
-      const uint64_t who = wave::ballot(best == v_key && bp >= 0);
-      v_pos = wave::readlane(bp, __builtin_ctzll(who));
-      v_so = vso[v_pos];
-    };
-    // remove run at (row rr, lane ln): keep h exact for the others
-    auto remove_run = [&](int rr, int ln) {
-      int32_t xk = 0, ek = 0;
-#pragma unroll
-      for (int r = 0; r < ROWS; ++r)
-        if (r == rr) {
-          xk = wave::readlane(r_x[r], ln);
-          ek = wave::readlane(r_end[r], ln);
-        }
-#pragma unroll
-      for (int r = 0; r < ROWS; ++r)
-        if (r < rows_hi) {
-          const bool v = (vm[r] >> lane) & 1ull;
-          if (v && r_end[r] <= ek) r_h[r] -= xk + r_end[r] - t_r;
-        }
-#pragma unroll
-      for (int r = 0; r < ROWS; ++r)
-        if (r == rr) vm[r] &= ~(1ull << ln);
-      X -= xk;
-      N -= 1;
-      while (rows_hi > 0) {
-        bool empty = false;
-#pragma unroll
-        for (int r = 0; r < ROWS; ++r)
-          if (r == rows_hi - 1) empty = (vm[r] == 0ull);
-        if (!empty) break;
-        --rows_hi;
-      }
-      return xk;
-    };
+#define SK_LOAD_ARRIVALS()                                                           \
+  do {                                                                               \
+    aw_base = arr_ptr;                                                               \
+    const int i_ = aw_base + lane;                                                   \
+    aw_a = 0x7FFFFFFF;                                                               \
+    aw_rank = 0;                                                                     \
+    if (i_ < n) {                                                                    \
+      aw_a = arrival ? arrival[i_] : 0;                                              \
+      aw_rank = rank_of[i_];                                                         \
+    }                                                                                \
+  } while (0)
+    // smallest waiting fresh request: first set bit of the two-level bitmap
+#define SK_F_FIND()                                                                  \
+  do {                                                                               \
+    const uint64_t w1_ = lane < nw1 ? L1[lane] : 0ull;                               \
+    const uint64_t nz_ = wave::ballot(w1_ != 0ull);                                  \
+    if (nz_ == 0ull) {                                                               \
+      f_rank = -1;                                                                   \
+      f_key = 0xFFFFFFFFu;                                                           \
+    } else {                                                                         \
+      const int j1_ = __builtin_ctzll(nz_);                                          \
+      const uint64_t w1v_ = wave::readlane_u64(w1_, j1_);                            \
+      const int j0_ = j1_ * 64 + __builtin_ctzll(w1v_);                              \
+      const uint64_t w0_ = uniform_u64(L0[j0_]);                                     \
+      f_rank = j0_ * 64 + __builtin_ctzll(w0_);                                      \
+      if (fw_base < 0 || f_rank < fw_base || f_rank >= fw_base + 64) {               \
+        fw_base = f_rank;                                                            \
+        const int rr_ = fw_base + lane;                                              \
+        fw_key = 0xFFFFFFFFu;                                                        \
+        fw_so = 0u;                                                                  \
+        if (rr_ < n) {                                                               \
+          const uint2 rv_ = rec[rr_];                                                \
+          fw_key = rv_.x;                                                            \
+          fw_so = rv_.y;                                                             \
+        }                                                                            \
+      }                                                                              \
+      f_key = wave::readlane_u(fw_key, f_rank - fw_base);                            \
+      f_so = wave::readlane_u(fw_so, f_rank - fw_base);                              \
+    }                                                                                \
+  } while (0)
+    // smallest eligible cancelled request
+#define SK_V_FIND()                                                                  \
+  do {                                                                               \
+    uint32_t best_ = 0xFFFFFFFFu;                                                    \
+    int32_t bp_ = -1;                                                                \
+    for (int j_ = lane; j_ < nVe; j_ += 64) {                                        \
+      const uint32_t kv_ = vkey[j_];                                                 \
+      if (kv_ < best_) {                                                             \
+        best_ = kv_;                                                                 \
+        bp_ = j_;                                                                    \
+      }                                                                              \
+    }                                                                                \
+    v_key = wave::min_u32(best_);                                                    \
+    if (nVe == 0) {                                                                  \
+      v_pos = -1;                                                                    \
+      v_key = 0xFFFFFFFFu;                                                           \
+    } else {                                                                         \
+      const uint64_t who_ = wave::ballot(best_ == v_key && bp_ >= 0);                \
+      v_pos = wave::readlane(bp_, __builtin_ctzll(who_));                            \
+      v_so = uniform_u32(vso[v_pos]);                                                \
+    }                                                                                \
+  } while (0)
+    // the head of the waiting set: smaller key of the fresh and cancelled heads
+#define SK_PICK()                                                                    \
+  do {                                                                               \
+    c_any = f_rank >= 0 || v_pos >= 0;                                               \
+    c_fromF = f_rank >= 0 && f_key < v_key;                                          \
+    c_key = c_fromF ? f_key : v_key;                                                 \
+    const uint32_t so_ = c_fromF ? f_so : v_so;                                      \
+    c_est = static_cast<int32_t>(c_key >> kIdxBits);                                 \
+    c_s = static_cast<int32_t>(so_ & 0xFFFFu);                                       \
+    c_o = static_cast<int32_t>(so_ >> 16);                                           \
+  } while (0)
+#define SK_SHRINK_ROWS()                                                             \
+  do {                                                                               \
+    while (rows_hi > 0) {                                                            \
+      bool empty_ = false;                                                           \
+      _Pragma("unroll") for (int r_ = 0; r_ < ROWS; ++r_) {                          \
+        if (r_ == rows_hi - 1) empty_ = wave::ballot(r_end[r_] != kEmpty) == 0ull;   \
+      }                                                                              \
+      if (!empty_) break;                                                            \
+      --rows_hi;                                                                     \
+    }                                                                                \
+  } while (0)
+    // A run with raw planned end ek and x = xk leaves: every run with
+    // t+1 < Rend <= ek loses its share of f at its own planned end.
+#define SK_DROP_SHARE(T_, XK_, EK_)                                                  \
+  do {                                                                               \
+    const int32_t tt_ = (T_), xk_ = (XK_), ek_ = (EK_);                              \
+    if (ek_ > tt_ + 1) {                                                             \
+      const uint32_t lo_ = static_cast<uint32_t>(tt_) + 2u;                          \
+      const uint32_t span_ = static_cast<uint32_t>(ek_) - lo_;                       \
+      _Pragma("unroll") for (int r_ = 0; r_ < ROWS; ++r_) {                          \
+        if (r_ < rows_hi) {                                                          \
+          const int32_t e_ = r_end[r_];                                              \
+          const bool in_ = static_cast<uint32_t>(e_) - lo_ <= span_;                 \
+          r_h[r_] -= in_ ? xk_ + e_ - t_r : 0;                                       \
+        }                                                                            \
+      }                                                                              \
+    }                                                                                \
+  } while (0)
 
     int32_t t = 0;
     for (;;) {
@@ -360,187 +406,274 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
       if (t - t_r >= kRebase) {
         const int32_t d = t - t_r;
 #pragma unroll
-        for (int r = 0; r < ROWS; ++r)
+        for (int r = 0; r < ROWS; ++r) {
           if (r < rows_hi) {
             r_x[r] += d;
             r_h[r] -= d;
           }
+        }
         X += N * d;
         t_r = t;
       }
-      // ---- 1. arrivals (and last step's cancelled requests become eligible)
-      bool arrived = false;
-      while (arr_ptr < n) {
-        if (arr_ptr >= aw_base + 64) {
-          aw_base = arr_ptr;
-          const int i = aw_base + lane;
-          aw_a = i < n ? (arrival ? arrival[i] : 0) : 0x7FFFFFFF;
-          aw_rank = i < n ? rank_of[i] : 0;
+      bool heads_changed = false;
+      bool event = false;
+      // ---- 1. arrivals; requests cancelled at the previous step become eligible
+      if (t >= next_a) {
+        while (arr_ptr < n) {
+          if (arr_ptr >= aw_base + 64) SK_LOAD_ARRIVALS();
+          const bool take = (aw_base + lane >= arr_ptr) && aw_a <= t;
+          const uint64_t m = wave::ballot(take);
+          if (m == 0ull) break;
+          if (take) {
+            atomicOr(reinterpret_cast<unsigned long long*>(&L0[aw_rank >> 6]), 1ull << (aw_rank & 63));
+            atomicOr(reinterpret_cast<unsigned long long*>(&L1[aw_rank >> 12]), 1ull << ((aw_rank >> 6) & 63));
+          }
+          arr_ptr += __builtin_popcountll(m);
+          if (arr_ptr < aw_base + 64) break;
         }
-        const bool take = (aw_base + lane >= arr_ptr) && aw_a <= t;
-        const uint64_t m = wave::ballot(take);
-        if (m == 0ull) break;
-        if (take) {
-          atomicOr(reinterpret_cast<unsigned long long*>(&L0[aw_rank >> 6]), 1ull << (aw_rank & 63));
-          atomicOr(reinterpret_cast<unsigned long long*>(&L1[aw_rank >> 12]), 1ull << ((aw_rank >> 6) & 63));
+        if (arr_ptr < n) {
+          if (arr_ptr >= aw_base + 64) SK_LOAD_ARRIVALS();
+          next_a = wave::readlane(aw_a, arr_ptr - aw_base);
+        } else {
+          next_a = 0x7FFFFFFF;
         }
-        arr_ptr += __builtin_popcountll(m);
-        arrived = true;
-        if (arr_ptr < aw_base + 64) break;
+        SK_F_FIND();
+        heads_changed = true;
       }
-      if (arrived) f_find();
       if (ALGO == SCHED_AMIN && nVe != nV) {
         nVe = nV;
-        v_find();
+        SK_V_FIND();
+        heads_changed = true;
+      }
+      if (heads_changed) {
+        SK_PICK();
+        event = true;
       }
 
-      // ---- 2. completions at t; DT = memory they hold at t (s + o each)
+      // ---- 2. completions at t; DT = memory they still hold at t (s + o each)
       int32_t DT = 0;
+      if (t >= next_c) {
+        int32_t sx = 0, cmin = 0x7FFFFFFF;
+        int ndone = 0;
 #pragma unroll
-      for (int r = 0; r < ROWS; ++r)
-        if (r < rows_hi) {
-          const bool v = (vm[r] >> lane) & 1ull;
-          const bool hit = v && r_c[r] == t;
-          uint64_t m = wave::ballot(hit);
-          if (m) {
-            if (hit) completion[r_key[r] & kIdxMask] = t;
-            n_done += __builtin_popcountll(m);
-            while (m) {
-              const int ln = __builtin_ctzll(m);
-              m &= m - 1;
-              const int32_t xk = remove_run(r, ln);
-              DT += xk - t_r + t;
+        for (int r = 0; r < ROWS; ++r) {
+          if (r < rows_hi) {
+            const bool hit = r_c[r] == t;
+            const uint64_t m = wave::ballot(hit);
+            if (m) {
+              ndone += __builtin_popcountll(m);
+              if (ALGO == SCHED_AMAX) {
+                // planned with u >= o: the run may end before its planned end
+                uint64_t mm = m;
+                while (mm) {
+                  const int ln = __builtin_ctzll(mm);
+                  mm &= mm - 1;
+                  SK_DROP_SHARE(t, wave::readlane(r_x[r], ln), wave::readlane(r_end[r], ln));
+                }
+              }
+              if (hit) {
+                completion[r_key[r] & kIdxMask] = t;
+                sx += r_x[r];
+                r_end[r] = kEmpty;
+                r_c[r] = -1;
+                r_key[r] = 0xFFFFFFFFu;
+              }
             }
+            if (!hit && r_c[r] >= 0) cmin = r_c[r] < cmin ? r_c[r] : cmin;
           }
         }
-      // ---- 3. done?
-      if (n_done == n) break;
+        if (ndone) {
+          event = true;
+          const int32_t sxw = wave::sum_i32(sx);
+          X -= sxw;
+          N -= ndone;
+          DT = sxw + ndone * (t - t_r);
+          n_done += ndone;
+          SK_SHRINK_ROWS();
+        }
+        next_c = static_cast<int32_t>(wave::min_u32(static_cast<uint32_t>(cmin)));  // all >= 0
+        // ---- 3. done?
+        if (n_done == n) break;
+      }
 
       // ---- 4. A_min: cancel in ascending (o~, index) while memory at t+1 > M
       if (ALGO == SCHED_AMIN) {
         int32_t Pm = X + N * (t + 1 - t_r);
-        while (Pm > M) {
-          uint32_t best = 0xFFFFFFFFu;
+        if (Pm > M) {
+          while (Pm > M) {
+            uint32_t best = 0xFFFFFFFFu;
 #pragma unroll
-          for (int r = 0; r < ROWS; ++r)
-            if (r < rows_hi) {
-              const bool v = (vm[r] >> lane) & 1ull;
-              if (v && r_key[r] < best) best = r_key[r];
+            for (int r = 0; r < ROWS; ++r) {
+              if (r < rows_hi) best = r_key[r] < best ? r_key[r] : best;
             }
-          const uint32_t kmin = wave::min_u32(best);
-          int rr = -1, ln = 0;
-          int32_t ek = 0, ck = 0;
+            const uint32_t kmin = wave::min_u32(best);
+            int rr = -1, ln = 0;
+            int32_t ek = 0, xk = 0, ck = 0;
 #pragma unroll
-          for (int r = 0; r < ROWS; ++r)
-            if (r < rows_hi && rr < 0) {
-              const bool v = (vm[r] >> lane) & 1ull;
-              const uint64_t m = wave::ballot(v && r_key[r] == kmin);
-              if (m) {
-                rr = r;
-                ln = __builtin_ctzll(m);
-                ek = wave::readlane(r_end[r], ln);
-                ck = wave::readlane(r_c[r], ln);
+            for (int r = 0; r < ROWS; ++r) {
+              if (r < rows_hi && rr < 0) {
+                const uint64_t m = wave::ballot(r_key[r] == kmin);
+                if (m) {
+                  rr = r;
+                  ln = __builtin_ctzll(m);
+                  ek = wave::readlane(r_end[r], ln);
+                  xk = wave::readlane(r_x[r], ln);
+                  ck = wave::readlane(r_c[r], ln);
+                }
               }
             }
-          if (rr < 0 || nV >= P.cap_v) {  // rr < 0 cannot happen while P > M > 0
-            status = SCHED_E_UNSUPPORTED;
-            break;
+            if (rr < 0 || nV >= P.cap_v) {  // rr < 0 cannot happen while P > M > 0
+              status = SCHED_E_UNSUPPORTED;
+              break;
+            }
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+              if (r == rr && lane == ln) {
+                r_end[r] = kEmpty;
+                r_c[r] = -1;
+                r_key[r] = 0xFFFFFFFFu;
+              }
+            }
+            SK_DROP_SHARE(t, xk, ek);
+            X -= xk;
+            N -= 1;
+            Pm -= xk + t + 1 - t_r;
+            const int32_t oh = static_cast<int32_t>(kmin >> kIdxBits);
+            const uint32_t idx = kmin & kIdxMask;
+            const int32_t pk = ek - oh;
+            const int32_t gen = t - pk;
+            const int32_t nh = gen > oh ? gen : oh;
+            const int32_t sk = xk - t_r + pk;
+            const int32_t okk = ck - pk;
+            if (lane == 0) {
+              vkey[nV] = (static_cast<uint32_t>(nh) << kIdxBits) | idx;
+              vso[nV] = static_cast<uint32_t>(sk) | (static_cast<uint32_t>(okk) << 16);
+              if (evictions) atomicAdd(&evictions[idx], 1);
+            }
+            ++nV;
+            ++tot_ev;
           }
-          const int32_t xk = remove_run(rr, ln);
-          Pm -= xk + t + 1 - t_r;
-          const int32_t oh = static_cast<int32_t>(kmin >> kIdxBits);
-          const uint32_t idx = kmin & kIdxMask;
-          const int32_t pk = ek - oh;
-          const int32_t gen = t - pk;
-          const int32_t nh = gen > oh ? gen : oh;
-          const int32_t sk = xk - t_r + pk;
-          const int32_t ok = ck - pk;
-          if (lane == 0) {
-            vkey[nV] = (static_cast<uint32_t>(nh) << kIdxBits) | idx;
-            vso[nV] = static_cast<uint32_t>(sk) | (static_cast<uint32_t>(ok) << 16);
-            if (evictions) evictions[idx] += 1;
-          }
-          ++nV;
-          ++tot_ev;
+          if (status != SCHED_OK) break;
+          SK_SHRINK_ROWS();
+          event = true;
         }
-        if (status != SCHED_OK) break;
       }
+      if (event) retry_at = 0;
 
       // ---- 5. admission of the longest feasible prefix in key order
-      for (;;) {
-        const bool hasF = f_rank >= 0;
-        const bool hasV = (ALGO == SCHED_AMIN) && v_pos >= 0;
-        if (!hasF && !hasV) break;
-        const bool fromF = hasF && (!hasV || f_key < v_key);
-        const uint32_t ck = fromF ? f_key : v_key;
-        const uint32_t cso = fromF ? f_so : v_so;
-        const int32_t est = static_cast<int32_t>(ck >> kIdxBits);
-        const int32_t s = static_cast<int32_t>(cso & 0xFFFFu);
-        const int32_t o = static_cast<int32_t>(cso >> 16);
+      bool stuck = true;          // the head cannot start before the next event
+      int32_t wait_until = t + 1; // otherwise: not before this step
+      while (c_any) {
+        const int32_t s = c_s, est = c_est;
         const int32_t E = t + est;
         const int32_t tp1 = t + 1;
-        int32_t hm = INT32_MIN, xs = 0, cnt = 0;
-        bool any_le = false, any_clamp = false;
-#pragma unroll
-        for (int r = 0; r < ROWS; ++r)
-          if (r < rows_hi) {
-            const bool v = (vm[r] >> lane) & 1ull;
-            const int32_t e = r_end[r];
-            const bool le = v && e <= E;
-            const bool ge = v && e >= E;  // raw planned ends: the invariant h is kept over
-            hm = (le && r_h[r] > hm) ? r_h[r] : hm;
-            xs += ge ? r_x[r] : 0;
-            cnt += __builtin_popcountll(wave::ballot(ge));
-            any_le |= wave::ballot(le) != 0ull;
-            any_clamp |= wave::ballot(v && e <= tp1) != 0ull;
-          }
+        // step t+1: every running request is present; exact when a planned end
+        // falls there and implied by the first planned end after it otherwise
         const int32_t Pm = X + N * (tp1 - t_r);
-        bool ok = DT + X + N * (t - t_r) + s <= M;                  // step t
-        ok = ok && (!any_clamp || Pm + s + 1 <= M);                 // step t+1
-        const int32_t hmax = any_le ? wave::max_i32(hm) : 0;
-        ok = ok && (!any_le || hmax + t_r - t + s <= M);            // planned ends <= E
-        // f(E) over raw planned ends; at E = t+1 every run is present, which is Pm
-        const int32_t f = wave::sum_i32(xs) + cnt * (E - t_r);
-        ok = ok && ((E == tp1 ? Pm : f) + s + est <= M);            // E itself
-        if (!ok) break;
-        // admit: p = t
-        const int32_t xw = s - t + t_r;
-        const int32_t hw = f + (xw + E - t_r) + (E - t_r);
+        if (Pm + s + 1 > M) break;
+        stuck = false;
+        if (t < retry_at) {
+          wait_until = retry_at;
+          break;
+        }
+        // step t (runs completing at t hold s+o); implied by step t+1 when DT = 0
+        if (DT > 0 && DT + X + N * (t - t_r) + s > M) break;
+        // planned ends c in (t+1, E] need h + t_r - t + s <= M (h + t_r = f(c) + c);
+        // the candidate's own end E needs f(E) + s + est <= M, f(E) = sum of x + E - t_r
+        const uint32_t lo2 = static_cast<uint32_t>(t) + 2u;
+        const bool win = E > tp1;
+        const uint32_t span = win ? static_cast<uint32_t>(E) - lo2 : 0u;
+        const int32_t cE = E - t_r;
+        const int32_t lim = M + t - t_r - s;   // h above this violates
+        int32_t fl = 0;
+        bool badl = false;
 #pragma unroll
-        for (int r = 0; r < ROWS; ++r)
+        for (int r = 0; r < ROWS; ++r) {
           if (r < rows_hi) {
-            const bool v = (vm[r] >> lane) & 1ull;
-            if (v && r_end[r] <= E) r_h[r] += xw + r_end[r] - t_r;
+            const int32_t e = r_end[r];
+            const bool le = win && static_cast<uint32_t>(e) - lo2 <= span;
+            badl = badl || (le && r_h[r] > lim);
+            fl += e >= E ? r_x[r] + cE : 0;
           }
-        int rr = -1;
+        }
+        if (wave::ballot(badl)) {
+          // each violating end improves by one per step, or leaves the window
+          int32_t fix = 0;
 #pragma unroll
-        for (int r = 0; r < ROWS; ++r)
-          if (rr < 0 && vm[r] != ~0ull) rr = r;
+          for (int r = 0; r < ROWS; ++r) {
+            if (r < rows_hi) {
+              const int32_t e = r_end[r];
+              const bool le = static_cast<uint32_t>(e) - lo2 <= span;
+              if (le && r_h[r] > lim) {
+                const int32_t a = r_h[r] - lim, bb = e - 1 - t;
+                const int32_t m = a < bb ? a : bb;
+                fix = m > fix ? m : fix;
+              }
+            }
+          }
+          retry_at = t + wave::max_i32(fix);
+          wait_until = retry_at;
+          break;
+        }
+        const int32_t f = wave::sum_i32(fl);
+        if (win && f + s + est > M) {
+          // f at the sliding end only grows until it passes the next planned end
+          int32_t emin = 0x7FFFFFFF;
+#pragma unroll
+          for (int r = 0; r < ROWS; ++r) {
+            if (r < rows_hi) {
+              const int32_t e = r_end[r];
+              emin = (e >= E && e < emin) ? e : emin;
+            }
+          }
+          retry_at = static_cast<int32_t>(wave::min_u32(static_cast<uint32_t>(emin))) - est + 1;
+          wait_until = retry_at;
+          break;
+        }
+        // admit: start at p = t
+        const int32_t xw = s - t + t_r;
+        const int32_t hw = f + (xw + cE) + cE;
+        int rr = -1, ln = 0;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+          const int32_t e = r_end[r];
+          if (r < rows_hi) r_h[r] += (e != kEmpty && e <= E) ? xw + e - t_r : 0;
+          if (rr < 0) {
+            const uint64_t fr = wave::ballot(e == kEmpty);
+            if (fr) {
+              rr = r;
+              ln = __builtin_ctzll(fr);
+            }
+          }
+        }
         if (rr < 0) {
-          status = SCHED_E_UNSUPPORTED;
+          status = RETRY_PASS ? SCHED_E_UNSUPPORTED : P.retry_status;
           break;
         }
 #pragma unroll
-        for (int r = 0; r < ROWS; ++r)
-          if (r == rr) {
-            const int ln = __builtin_ctzll(~vm[r]);
-            if (lane == ln) {
-              r_end[r] = E;
-              r_x[r] = xw;
-              r_c[r] = t + o;
-              r_key[r] = ck;
-              r_h[r] = hw;
-            }
-            vm[r] |= 1ull << ln;
+        for (int r = 0; r < ROWS; ++r) {
+          if (r == rr && lane == ln) {
+            r_end[r] = E;
+            r_x[r] = xw;
+            r_c[r] = t + c_o;
+            r_key[r] = c_key;
+            r_h[r] = hw;
           }
+        }
         rows_hi = rr + 1 > rows_hi ? rr + 1 : rows_hi;
+        next_c = t + c_o < next_c ? t + c_o : next_c;
         X += xw;
         N += 1;
-        if (fromF) {
-          f_clear(f_rank);
-          f_find();
+        if (c_fromF) {
+          const int j0 = f_rank >> 6;
+          if (lane == 0) {
+            const uint64_t w = L0[j0] & ~(1ull << (f_rank & 63));
+            L0[j0] = w;
+            if (w == 0ull) L1[j0 >> 6] &= ~(1ull << (j0 & 63));
+          }
+          SK_F_FIND();
         } else {
-          // remove eligible entry v_pos: last eligible moves in, last pending fills its place
+          // the last eligible entry moves into the hole; the last pending one fills its place
           if (lane == 0) {
             const int le = nVe - 1;
             vkey[v_pos] = vkey[le];
@@ -552,26 +685,42 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
           }
           --nVe;
           --nV;
-          v_find();
+          SK_V_FIND();
         }
+        SK_PICK();
+        stuck = true;
+        wait_until = t + 1;
+        retry_at = 0;
       }
       if (status != SCHED_OK) break;
 
       // ---- 6. this step processes every running request once
       rsteps += N;
-      if (N == 0 && f_rank < 0 && nV == 0 && arr_ptr < n) {
-        // nothing runs or waits: jump to the next arrival
-        if (arr_ptr >= aw_base + 64) {
-          aw_base = arr_ptr;
-          const int i = aw_base + lane;
-          aw_a = i < n ? (arrival ? arrival[i] : 0) : 0x7FFFFFFF;
-          aw_rank = i < n ? rank_of[i] : 0;
+      int32_t tn = t + 1;
+      if (nV == nVe) {
+        // Nothing changes before the next completion, arrival or (A_min)
+        // overflow; until then the head cannot start before wait_until (or at
+        // all when stuck: the memory at t+1 only grows).
+        int32_t jump = stuck ? 0x7FFFFFFF : wait_until;
+        jump = next_c < jump ? next_c : jump;
+        jump = next_a < jump ? next_a : jump;
+        if (ALGO == SCHED_AMIN && N > 0) {
+          const int32_t Pm = X + N * (t + 1 - t_r);  // <= M here
+          // first step whose projection exceeds M, if it comes before the jump
+          if (static_cast<int64_t>(Pm) + static_cast<int64_t>(N) * (jump - 1 - t) > M) {
+            const int32_t tev = t + (M - Pm) / N + 1;
+            jump = tev < jump ? tev : jump;
+          }
         }
-        const int32_t na = wave::readlane(aw_a, arr_ptr - aw_base);
-        t = na > t + 1 ? na : t + 1;
-      } else {
-        t += 1;
+        const int32_t lim = t_r + kRebase;
+        jump = lim < jump ? lim : jump;
+        jump = cap + 1 < jump ? cap + 1 : jump;
+        if (jump > tn) {
+          rsteps += static_cast<int64_t>(N) * (jump - tn);
+          tn = jump;
+        }
       }
+      t = tn;
     }
   }
 
@@ -591,7 +740,7 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
       }
     }
   } else if (status != st0 && n > 0) {
-    // a run-time capacity failure: report like an invalid instance
+    // capacity outgrown at run time: report like an invalid instance (or hand it to the retry pass)
     for (int c = 0; c < n; c += 64) {
       const int i = c + lane;
       if (i < n) {
@@ -614,6 +763,12 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
     P.status[k] = status;
   }
 }
+#undef SK_LOAD_ARRIVALS
+#undef SK_PICK
+#undef SK_F_FIND
+#undef SK_V_FIND
+#undef SK_SHRINK_ROWS
+#undef SK_DROP_SHARE
 
 }  // namespace sk
 
@@ -623,29 +778,37 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
 namespace {
 
 template <int ALGO>
-hipError_t launch_sim(int rows, const sk::Params& P, size_t lds, hipStream_t st) {
-  const dim3 grid(P.K), block(64);
+const void* sim_kernel(int rows, bool retry) {
+  if (retry) return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true>);
   switch (rows) {
-    case 1: hipLaunchKernelGGL((sk::k_simulate<ALGO, 1>), grid, block, lds, st, P); break;
-    case 2: hipLaunchKernelGGL((sk::k_simulate<ALGO, 2>), grid, block, lds, st, P); break;
-    case 4: hipLaunchKernelGGL((sk::k_simulate<ALGO, 4>), grid, block, lds, st, P); break;
-    case 8: hipLaunchKernelGGL((sk::k_simulate<ALGO, 8>), grid, block, lds, st, P); break;
-    default: hipLaunchKernelGGL((sk::k_simulate<ALGO, 16>), grid, block, lds, st, P); break;
+    case 1: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 1, false>);
+    case 2: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 2, false>);
+    case 4: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 4, false>);
+    case 8: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, false>);
+    default: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, false>);
+  }
+}
+
+template <int ALGO>
+hipError_t launch_sim(int rows, bool retry, const sk::Params& P, size_t lds, hipStream_t st) {
+  const dim3 grid(P.K), block(64);
+  if (retry) {
+    hipLaunchKernelGGL((sk::k_simulate<ALGO, 16, true>), grid, block, lds, st, P);
+    return hipGetLastError();
+  }
+  switch (rows) {
+    case 1: hipLaunchKernelGGL((sk::k_simulate<ALGO, 1, false>), grid, block, lds, st, P); break;
+    case 2: hipLaunchKernelGGL((sk::k_simulate<ALGO, 2, false>), grid, block, lds, st, P); break;
+    case 4: hipLaunchKernelGGL((sk::k_simulate<ALGO, 4, false>), grid, block, lds, st, P); break;
+    case 8: hipLaunchKernelGGL((sk::k_simulate<ALGO, 8, false>), grid, block, lds, st, P); break;
+    default: hipLaunchKernelGGL((sk::k_simulate<ALGO, 16, false>), grid, block, lds, st, P); break;
   }
   return hipGetLastError();
 }
 
 template <int ALGO>
-hipError_t set_lds_limit(int rows, int bytes) {
-  const void* f;
-  switch (rows) {
-    case 1: f = reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 1>); break;
-    case 2: f = reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 2>); break;
-    case 4: f = reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 4>); break;
-    case 8: f = reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8>); break;
-    default: f = reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16>); break;
-  }
-  return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+hipError_t set_lds_limit(int rows, bool retry, int bytes) {
+  return hipFuncSetAttribute(sim_kernel<ALGO>(rows, retry), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
 }
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -688,11 +851,14 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   if (o.running_capacity < 0 || o.evicted_capacity < 0) return SCHED_E_INVAL;
 
   const int64_t nmax = in->max_requests;
-  int run_cap = o.running_capacity > 0 ? o.running_capacity
-                                       : static_cast<int>(std::min<int64_t>((nmax + 63) / 64 * 64, 1024));
-  if (run_cap > 1024) return SCHED_E_UNSUPPORTED;
-  int rows = (run_cap + 63) / 64;
+  // Register rows of the running set.  By default a first pass holds up to 512
+  // runs and a second pass with 1024 re-runs only the instances that outgrew it.
+  if (o.running_capacity > 1024) return SCHED_E_UNSUPPORTED;
+  const bool forced = o.running_capacity > 0;
+  const int64_t want = forced ? o.running_capacity : std::min<int64_t>(std::max<int64_t>(nmax, 1), 512);
+  int rows = static_cast<int>((want + 63) / 64);
   rows = rows <= 1 ? 1 : rows <= 2 ? 2 : rows <= 4 ? 4 : rows <= 8 ? 8 : 16;
+  const bool two_pass = !forced && nmax > 512;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   int dev = 0;
@@ -750,6 +916,7 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   P.nw_max = nw;
   P.nw1_max = nw1;
   P.cap_v = cap_v;
+  P.retry_status = two_pass ? sk::kRetry : SCHED_E_UNSUPPORTED;
 
   hipError_t err = hipSuccess;
   const dim3 grid(P.K), block(64);
@@ -759,19 +926,22 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
     default: hipLaunchKernelGGL((sk::k_prepare<SCHED_HSF>), grid, block, 0, st, P); break;
   }
   err = hipGetLastError();
-  if (err == hipSuccess && lds > 65536) {
-    switch (algo) {
-      case SCHED_AMAX: err = set_lds_limit<SCHED_AMAX>(rows, static_cast<int>(lds)); break;
-      case SCHED_AMIN: err = set_lds_limit<SCHED_AMIN>(rows, static_cast<int>(lds)); break;
-      default: err = set_lds_limit<SCHED_HSF>(rows, static_cast<int>(lds)); break;
+  for (int pass = 0; pass < (two_pass ? 2 : 1) && err == hipSuccess; ++pass) {
+    const bool retry = pass == 1;
+    if (lds > 65536) {
+      switch (algo) {
+        case SCHED_AMAX: err = set_lds_limit<SCHED_AMAX>(rows, retry, static_cast<int>(lds)); break;
+        case SCHED_AMIN: err = set_lds_limit<SCHED_AMIN>(rows, retry, static_cast<int>(lds)); break;
+        default: err = set_lds_limit<SCHED_HSF>(rows, retry, static_cast<int>(lds)); break;
+      }
     }
   }
   if (err == hipSuccess && o.event_before) err = hipEventRecord(static_cast<hipEvent_t>(o.event_before), st);
-  if (err == hipSuccess) {
+  for (int pass = 0; pass < (two_pass ? 2 : 1) && err == hipSuccess; ++pass) {
     switch (algo) {
-      case SCHED_AMAX: err = launch_sim<SCHED_AMAX>(rows, P, lds, st); break;
-      case SCHED_AMIN: err = launch_sim<SCHED_AMIN>(rows, P, lds, st); break;
-      default: err = launch_sim<SCHED_HSF>(rows, P, lds, st); break;
+      case SCHED_AMAX: err = launch_sim<SCHED_AMAX>(rows, pass == 1, P, lds, st); break;
+      case SCHED_AMIN: err = launch_sim<SCHED_AMIN>(rows, pass == 1, P, lds, st); break;
+      default: err = launch_sim<SCHED_HSF>(rows, pass == 1, P, lds, st); break;
     }
   }
   if (err == hipSuccess && o.event_after) err = hipEventRecord(static_cast<hipEvent_t>(o.event_after), st);
