@@ -37,11 +37,16 @@ def kernel_source_hash() -> str:
 
 
 def load_traffic(workload: str, algo: str):
-    """HBM bytes per launch from committed rocprofv3 --pmc counters, if still current."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{SIM_KERNEL}_{algo}_{workload}.json")
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary, if it is
+    still current (same kernel source); otherwise None."""
+    path = os.path.join(ROOT, "profiles", f"{SIM_KERNEL}_{algo}_{workload}.md")
     if not os.path.exists(path):
         return None
-    d = json.load(open(path))
+    text = open(path).read()
+    if "```json" not in text:
+        return None
+    block = text.split("```json", 1)[1].split("```", 1)[0]
+    d = json.loads(block)
     if d.get("kernel_source_hash") != kernel_source_hash():
         return None
     return d.get("hbm_bytes_per_launch")
