@@ -222,6 +222,8 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
 constexpr int kRetry = -100;
 // r_end of an empty slot of the running set (below every planned end)
 constexpr int32_t kEmpty = INT32_MIN;
+// r_c of an empty slot (after every step)
+constexpr int32_t kNever = 0x7FFFFFFF;
 
 __device__ __forceinline__ uint64_t uniform_u64(uint64_t v) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
@@ -253,8 +255,9 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
   if (st0 == SCHED_OK && n > 0) {
     uint64_t* L0 = lds64;
     uint64_t* L1 = lds64 + P.nw_max;
-    uint32_t* vkey = reinterpret_cast<uint32_t*>(L1 + P.nw1_max);
-    uint32_t* vso = vkey + P.cap_v;
+    // cancelled requests, one 64-bit entry each: key | (s | o << 16) << 32;
+    // slots [0, nVe) may start now, [nVe, nV) were cancelled at this step
+    uint64_t* vent = L1 + P.nw1_max;
     const int nw = (n + 63) >> 6;
     const int nw1 = (nw + 63) >> 6;
     for (int w = lane; w < nw; w += 64) L0[w] = 0;
@@ -268,18 +271,20 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
     int32_t* completion = P.completion + b;
     int32_t* evictions = P.evictions ? P.evictions + b : nullptr;
 
-    // running set: register rows; an empty slot has r_end = kEmpty, r_c = -1, r_key = ~0
+    // running set: register rows; an empty slot has r_end = kEmpty, r_c = kNever,
+    // r_key = ~0, which every scan below treats as neutral, so scans cover all rows
     int32_t r_end[ROWS], r_x[ROWS], r_c[ROWS], r_h[ROWS];
     uint32_t r_key[ROWS];
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) {
-      r_end[r] = kEmpty; r_x[r] = 0; r_c[r] = -1; r_h[r] = 0; r_key[r] = 0xFFFFFFFFu;
+      r_end[r] = kEmpty; r_x[r] = 0; r_c[r] = kNever; r_h[r] = 0; r_key[r] = 0xFFFFFFFFu;
     }
-    int rows_hi = 0;              // rows [0, rows_hi) may hold runs
+    int fr_row = 0;               // row that receives new runs ...
+    uint64_t fr_mask = ~0ull;     // ... and its free lanes
     int32_t N = 0;                // number of runs
     int32_t X = 0;                // sum of x over runs
     int32_t t_r = 0;              // base step of x and h
-    int32_t next_c = 0x7FFFFFFF;  // lower bound on the earliest completion step
+    int32_t next_c = kNever;      // lower bound on the earliest completion step
 
     int32_t aw_base = -64, aw_a = 0x7FFFFFFF, aw_rank = 0, arr_ptr = 0;
     int32_t next_a = 0;           // arrival step of request arr_ptr (0: look at step 0)
@@ -335,27 +340,44 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
       f_so = wave::readlane_u(fw_so, f_rank - fw_base);                              \
     }                                                                                \
   } while (0)
-    // smallest eligible cancelled request
+    // per-lane smallest cancelled entry over slots [FROM_, TO_): vb_k, vb_p, vb_s
+#define SK_V_SCAN(FROM_, TO_)                                                        \
+  uint32_t vb_k = 0xFFFFFFFFu, vb_s = 0u;                                            \
+  int32_t vb_p = -1;                                                                 \
+  _Pragma("unroll 4") for (int j_ = (FROM_) + lane; j_ < (TO_); j_ += 64) {         \
+    const uint64_t ev_ = vent[j_];                                                   \
+    const uint32_t kk_ = static_cast<uint32_t>(ev_);                                 \
+    const bool lt_ = kk_ < vb_k;                                                     \
+    vb_k = lt_ ? kk_ : vb_k;                                                         \
+    vb_p = lt_ ? j_ : vb_p;                                                          \
+    vb_s = lt_ ? static_cast<uint32_t>(ev_ >> 32) : vb_s;                            \
+  }
+    // smallest cancelled request that may start now (slots [0, nVe))
 #define SK_V_FIND()                                                                  \
   do {                                                                               \
-    uint32_t best_ = 0xFFFFFFFFu;                                                    \
-    int32_t bp_ = -1;                                                                \
-    for (int j_ = lane; j_ < nVe; j_ += 64) {                                        \
-      const uint32_t kv_ = vkey[j_];                                                 \
-      if (kv_ < best_) {                                                             \
-        best_ = kv_;                                                                 \
-        bp_ = j_;                                                                    \
-      }                                                                              \
+    SK_V_SCAN(0, nVe)                                                                \
+    const uint32_t km_ = wave::min_u32(vb_k);                                        \
+    v_key = km_;                                                                     \
+    v_pos = -1;                                                                      \
+    if (km_ != 0xFFFFFFFFu) {                                                        \
+      const int ln_ = __builtin_ctzll(wave::ballot(vb_k == km_));                    \
+      v_pos = wave::readlane(vb_p, ln_);                                             \
+      v_so = wave::readlane_u(vb_s, ln_);                                            \
     }                                                                                \
-    v_key = wave::min_u32(best_);                                                    \
-    if (nVe == 0) {                                                                  \
-      v_pos = -1;                                                                    \
-      v_key = 0xFFFFFFFFu;                                                           \
-    } else {                                                                         \
-      const uint64_t who_ = wave::ballot(best_ == v_key && bp_ >= 0);                \
-      v_pos = wave::readlane(bp_, __builtin_ctzll(who_));                            \
-      v_so = uniform_u32(vso[v_pos]);                                                \
+  } while (0)
+    // the requests cancelled at the previous step may start now: merge them
+    // into the cached head instead of rescanning every slot
+#define SK_V_MERGE()                                                                 \
+  do {                                                                               \
+    SK_V_SCAN(nVe, nV)                                                               \
+    const uint32_t km_ = wave::min_u32(vb_k);                                        \
+    if (km_ < v_key) {                                                               \
+      const int ln_ = __builtin_ctzll(wave::ballot(vb_k == km_));                    \
+      v_key = km_;                                                                   \
+      v_pos = wave::readlane(vb_p, ln_);                                             \
+      v_so = wave::readlane_u(vb_s, ln_);                                            \
     }                                                                                \
+    nVe = nV;                                                                        \
   } while (0)
     // the head of the waiting set: smaller key of the fresh and cancelled heads
 #define SK_PICK()                                                                    \
@@ -368,31 +390,35 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
     c_s = static_cast<int32_t>(so_ & 0xFFFFu);                                       \
     c_o = static_cast<int32_t>(so_ >> 16);                                           \
   } while (0)
-#define SK_SHRINK_ROWS()                                                             \
-  do {                                                                               \
-    while (rows_hi > 0) {                                                            \
-      bool empty_ = false;                                                           \
-      _Pragma("unroll") for (int r_ = 0; r_ < ROWS; ++r_) {                          \
-        if (r_ == rows_hi - 1) empty_ = wave::ballot(r_end[r_] != kEmpty) == 0ull;   \
-      }                                                                              \
-      if (!empty_) break;                                                            \
-      --rows_hi;                                                                     \
+    // BODY with the compile-time row index r equal to the uniform row RR_
+#define SK_CASE(R_, BODY)                                                            \
+  case R_:                                                                           \
+    if constexpr ((R_) < ROWS) {                                                     \
+      constexpr int r = (R_);                                                        \
+      BODY                                                                           \
     }                                                                                \
-  } while (0)
+    break;
+#define SK_AT_ROW(RR_, BODY)                                                         \
+  switch (RR_) {                                                                     \
+    SK_CASE(0, BODY) SK_CASE(1, BODY) SK_CASE(2, BODY) SK_CASE(3, BODY)              \
+    SK_CASE(4, BODY) SK_CASE(5, BODY) SK_CASE(6, BODY) SK_CASE(7, BODY)              \
+    SK_CASE(8, BODY) SK_CASE(9, BODY) SK_CASE(10, BODY) SK_CASE(11, BODY)            \
+    SK_CASE(12, BODY) SK_CASE(13, BODY) SK_CASE(14, BODY) SK_CASE(15, BODY)          \
+    default: break;                                                                  \
+  }
     // A run with raw planned end ek and x = xk leaves: every run with
     // t+1 < Rend <= ek loses its share of f at its own planned end.
 #define SK_DROP_SHARE(T_, XK_, EK_)                                                  \
   do {                                                                               \
-    const int32_t tt_ = (T_), xk_ = (XK_), ek_ = (EK_);                              \
+    const int32_t tt_ = (T_), ek_ = (EK_);                                           \
     if (ek_ > tt_ + 1) {                                                             \
       const uint32_t lo_ = static_cast<uint32_t>(tt_) + 2u;                          \
       const uint32_t span_ = static_cast<uint32_t>(ek_) - lo_;                       \
+      const uint32_t dx_ = static_cast<uint32_t>(XK_) - static_cast<uint32_t>(t_r);  \
       _Pragma("unroll") for (int r_ = 0; r_ < ROWS; ++r_) {                          \
-        if (r_ < rows_hi) {                                                          \
-          const int32_t e_ = r_end[r_];                                              \
-          const bool in_ = static_cast<uint32_t>(e_) - lo_ <= span_;                 \
-          r_h[r_] -= in_ ? xk_ + e_ - t_r : 0;                                       \
-        }                                                                            \
+        const uint32_t e_ = static_cast<uint32_t>(r_end[r_]);                        \
+        const bool in_ = e_ - lo_ <= span_;                                          \
+        r_h[r_] = static_cast<int32_t>(static_cast<uint32_t>(r_h[r_]) - (in_ ? dx_ + e_ : 0u)); \
       }                                                                              \
     }                                                                                \
   } while (0)
@@ -404,15 +430,13 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
         break;
       }
       if (t - t_r >= kRebase) {
-        const int32_t d = t - t_r;
+        const uint32_t d = static_cast<uint32_t>(t - t_r);
 #pragma unroll
         for (int r = 0; r < ROWS; ++r) {
-          if (r < rows_hi) {
-            r_x[r] += d;
-            r_h[r] -= d;
-          }
+          r_x[r] = static_cast<int32_t>(static_cast<uint32_t>(r_x[r]) + d);
+          r_h[r] = static_cast<int32_t>(static_cast<uint32_t>(r_h[r]) - d);
         }
-        X += N * d;
+        X += N * static_cast<int32_t>(d);
         t_r = t;
       }
       bool heads_changed = false;
@@ -441,8 +465,7 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
         heads_changed = true;
       }
       if (ALGO == SCHED_AMIN && nVe != nV) {
-        nVe = nV;
-        SK_V_FIND();
+        SK_V_MERGE();
         heads_changed = true;
       }
       if (heads_changed) {
@@ -453,35 +476,34 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
       // ---- 2. completions at t; DT = memory they still hold at t (s + o each)
       int32_t DT = 0;
       if (t >= next_c) {
-        int32_t sx = 0, cmin = 0x7FFFFFFF;
+        int32_t sx = 0;
         int ndone = 0;
 #pragma unroll
         for (int r = 0; r < ROWS; ++r) {
-          if (r < rows_hi) {
-            const bool hit = r_c[r] == t;
-            const uint64_t m = wave::ballot(hit);
-            if (m) {
-              ndone += __builtin_popcountll(m);
-              if (ALGO == SCHED_AMAX) {
-                // planned with u >= o: the run may end before its planned end
-                uint64_t mm = m;
-                while (mm) {
-                  const int ln = __builtin_ctzll(mm);
-                  mm &= mm - 1;
-                  SK_DROP_SHARE(t, wave::readlane(r_x[r], ln), wave::readlane(r_end[r], ln));
-                }
-              }
-              if (hit) {
-                completion[r_key[r] & kIdxMask] = t;
-                sx += r_x[r];
-                r_end[r] = kEmpty;
-                r_c[r] = -1;
-                r_key[r] = 0xFFFFFFFFu;
+          const bool hit = r_c[r] == t;
+          const uint64_t m = wave::ballot(hit);
+          if (m) {
+            ndone += __builtin_popcountll(m);
+            if (ALGO == SCHED_AMAX) {
+              // planned with u >= o: the run may end before its planned end
+              uint64_t mm = m;
+              while (mm) {
+                const int ln = __builtin_ctzll(mm);
+                mm &= mm - 1;
+                SK_DROP_SHARE(t, wave::readlane(r_x[r], ln), wave::readlane(r_end[r], ln));
               }
             }
-            if (!hit && r_c[r] >= 0) cmin = r_c[r] < cmin ? r_c[r] : cmin;
+            if (hit) completion[r_key[r] & kIdxMask] = t;
+            sx += hit ? r_x[r] : 0;
+            r_end[r] = hit ? kEmpty : r_end[r];
+            r_c[r] = hit ? kNever : r_c[r];
+            r_key[r] = hit ? 0xFFFFFFFFu : r_key[r];
+            if (r == fr_row) fr_mask |= m;
           }
         }
+        int32_t cmin = r_c[0];
+#pragma unroll
+        for (int r = 1; r < ROWS; ++r) cmin = r_c[r] < cmin ? r_c[r] : cmin;
         if (ndone) {
           event = true;
           const int32_t sxw = wave::sum_i32(sx);
@@ -489,7 +511,6 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
           N -= ndone;
           DT = sxw + ndone * (t - t_r);
           n_done += ndone;
-          SK_SHRINK_ROWS();
         }
         next_c = static_cast<int32_t>(wave::min_u32(static_cast<uint32_t>(cmin)));  // all >= 0
         // ---- 3. done?
@@ -501,39 +522,27 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
         int32_t Pm = X + N * (t + 1 - t_r);
         if (Pm > M) {
           while (Pm > M) {
-            uint32_t best = 0xFFFFFFFFu;
+            uint32_t best = r_key[0];
+            int32_t brow = 0;
 #pragma unroll
-            for (int r = 0; r < ROWS; ++r) {
-              if (r < rows_hi) best = r_key[r] < best ? r_key[r] : best;
+            for (int r = 1; r < ROWS; ++r) {
+              const bool lt = r_key[r] < best;
+              best = lt ? r_key[r] : best;
+              brow = lt ? r : brow;
             }
             const uint32_t kmin = wave::min_u32(best);
-            int rr = -1, ln = 0;
-            int32_t ek = 0, xk = 0, ck = 0;
-#pragma unroll
-            for (int r = 0; r < ROWS; ++r) {
-              if (r < rows_hi && rr < 0) {
-                const uint64_t m = wave::ballot(r_key[r] == kmin);
-                if (m) {
-                  rr = r;
-                  ln = __builtin_ctzll(m);
-                  ek = wave::readlane(r_end[r], ln);
-                  xk = wave::readlane(r_x[r], ln);
-                  ck = wave::readlane(r_c[r], ln);
-                }
-              }
-            }
-            if (rr < 0 || nV >= P.cap_v) {  // rr < 0 cannot happen while P > M > 0
+            if (kmin == 0xFFFFFFFFu || nV >= P.cap_v) {  // no run: impossible while P > M > 0
               status = SCHED_E_UNSUPPORTED;
               break;
             }
-#pragma unroll
-            for (int r = 0; r < ROWS; ++r) {
-              if (r == rr && lane == ln) {
-                r_end[r] = kEmpty;
-                r_c[r] = -1;
-                r_key[r] = 0xFFFFFFFFu;
-              }
-            }
+            const int ln = __builtin_ctzll(wave::ballot(best == kmin));
+            const int rr = wave::readlane(brow, ln);
+            int32_t ek = 0, xk = 0, ck = 0;
+            SK_AT_ROW(rr, ek = wave::readlane(r_end[r], ln); xk = wave::readlane(r_x[r], ln);
+                      ck = wave::readlane(r_c[r], ln); r_end[r] = wave::writelane(r_end[r], kEmpty, ln);
+                      r_c[r] = wave::writelane(r_c[r], kNever, ln);
+                      r_key[r] = wave::writelane_u(r_key[r], 0xFFFFFFFFu, ln);)
+            if (rr == fr_row) fr_mask |= 1ull << ln;
             SK_DROP_SHARE(t, xk, ek);
             X -= xk;
             N -= 1;
@@ -546,15 +555,14 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
             const int32_t sk = xk - t_r + pk;
             const int32_t okk = ck - pk;
             if (lane == 0) {
-              vkey[nV] = (static_cast<uint32_t>(nh) << kIdxBits) | idx;
-              vso[nV] = static_cast<uint32_t>(sk) | (static_cast<uint32_t>(okk) << 16);
+              const uint32_t so = static_cast<uint32_t>(sk) | (static_cast<uint32_t>(okk) << 16);
+              vent[nV] = (static_cast<uint64_t>(so) << 32) | ((static_cast<uint32_t>(nh) << kIdxBits) | idx);
               if (evictions) atomicAdd(&evictions[idx], 1);
             }
             ++nV;
             ++tot_ev;
           }
           if (status != SCHED_OK) break;
-          SK_SHRINK_ROWS();
           event = true;
         }
       }
@@ -584,32 +592,25 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
         const bool win = E > tp1;
         const uint32_t span = win ? static_cast<uint32_t>(E) - lo2 : 0u;
         const int32_t cE = E - t_r;
-        const int32_t lim = M + t - t_r - s;   // h above this violates
-        int32_t fl = 0;
-        bool badl = false;
+        const int32_t lim = win ? M + t - t_r - s : 0x7FFFFFFF;  // h above this violates
+        int32_t fl = 0, hmx = INT32_MIN;
+        bool inw[ROWS];
 #pragma unroll
         for (int r = 0; r < ROWS; ++r) {
-          if (r < rows_hi) {
-            const int32_t e = r_end[r];
-            const bool le = win && static_cast<uint32_t>(e) - lo2 <= span;
-            badl = badl || (le && r_h[r] > lim);
-            fl += e >= E ? r_x[r] + cE : 0;
-          }
+          const int32_t e = r_end[r];
+          inw[r] = static_cast<uint32_t>(e) - lo2 <= span;
+          const int32_t hv = inw[r] ? r_h[r] : INT32_MIN;
+          hmx = hv > hmx ? hv : hmx;
+          fl += e >= E ? r_x[r] + cE : 0;
         }
-        if (wave::ballot(badl)) {
+        if (wave::ballot(hmx > lim)) {
           // each violating end improves by one per step, or leaves the window
           int32_t fix = 0;
 #pragma unroll
           for (int r = 0; r < ROWS; ++r) {
-            if (r < rows_hi) {
-              const int32_t e = r_end[r];
-              const bool le = static_cast<uint32_t>(e) - lo2 <= span;
-              if (le && r_h[r] > lim) {
-                const int32_t a = r_h[r] - lim, bb = e - 1 - t;
-                const int32_t m = a < bb ? a : bb;
-                fix = m > fix ? m : fix;
-              }
-            }
+            const int32_t a = r_h[r] - lim, bb = r_end[r] - 1 - t;
+            const int32_t m = a < bb ? a : bb;
+            fix = (inw[r] && r_h[r] > lim && m > fix) ? m : fix;
           }
           retry_at = t + wave::max_i32(fix);
           wait_until = retry_at;
@@ -618,50 +619,52 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
         const int32_t f = wave::sum_i32(fl);
         if (win && f + s + est > M) {
           // f at the sliding end only grows until it passes the next planned end
-          int32_t emin = 0x7FFFFFFF;
+          int32_t emin = kNever;
 #pragma unroll
           for (int r = 0; r < ROWS; ++r) {
-            if (r < rows_hi) {
-              const int32_t e = r_end[r];
-              emin = (e >= E && e < emin) ? e : emin;
-            }
+            const int32_t e = r_end[r];
+            emin = (e >= E && e < emin) ? e : emin;
           }
           retry_at = static_cast<int32_t>(wave::min_u32(static_cast<uint32_t>(emin))) - est + 1;
           wait_until = retry_at;
           break;
         }
-        // admit: start at p = t
+        // admit: start at p = t; runs whose planned end is in (t+1, E] gain its share
         const int32_t xw = s - t + t_r;
         const int32_t hw = f + (xw + cE) + cE;
-        int rr = -1, ln = 0;
+        if (win) {
+          const uint32_t dh = static_cast<uint32_t>(xw) - static_cast<uint32_t>(t_r);
 #pragma unroll
-        for (int r = 0; r < ROWS; ++r) {
-          const int32_t e = r_end[r];
-          if (r < rows_hi) r_h[r] += (e != kEmpty && e <= E) ? xw + e - t_r : 0;
+          for (int r = 0; r < ROWS; ++r)
+            r_h[r] = static_cast<int32_t>(static_cast<uint32_t>(r_h[r]) +
+                                          (inw[r] ? static_cast<uint32_t>(r_end[r]) + dh : 0u));
+        }
+        if (fr_mask == 0ull) {
+          int rr = -1;
+          uint64_t mm = 0ull;
+#pragma unroll
+          for (int r = ROWS - 1; r >= 0; --r) {
+            const uint64_t m = wave::ballot(r_end[r] == kEmpty);
+            rr = m ? r : rr;
+            mm = m ? m : mm;
+          }
           if (rr < 0) {
-            const uint64_t fr = wave::ballot(e == kEmpty);
-            if (fr) {
-              rr = r;
-              ln = __builtin_ctzll(fr);
-            }
+            status = RETRY_PASS ? SCHED_E_UNSUPPORTED : P.retry_status;
+            break;
           }
+          fr_row = rr;
+          fr_mask = mm;
         }
-        if (rr < 0) {
-          status = RETRY_PASS ? SCHED_E_UNSUPPORTED : P.retry_status;
-          break;
+        {
+          const int ln = __builtin_ctzll(fr_mask);
+          fr_mask &= fr_mask - 1;
+          const int32_t cw = t + c_o;
+          const uint32_t kw = c_key;
+          SK_AT_ROW(fr_row, r_end[r] = wave::writelane(r_end[r], E, ln); r_x[r] = wave::writelane(r_x[r], xw, ln);
+                    r_c[r] = wave::writelane(r_c[r], cw, ln); r_key[r] = wave::writelane_u(r_key[r], kw, ln);
+                    r_h[r] = wave::writelane(r_h[r], hw, ln);)
+          next_c = cw < next_c ? cw : next_c;
         }
-#pragma unroll
-        for (int r = 0; r < ROWS; ++r) {
-          if (r == rr && lane == ln) {
-            r_end[r] = E;
-            r_x[r] = xw;
-            r_c[r] = t + c_o;
-            r_key[r] = c_key;
-            r_h[r] = hw;
-          }
-        }
-        rows_hi = rr + 1 > rows_hi ? rr + 1 : rows_hi;
-        next_c = t + c_o < next_c ? t + c_o : next_c;
         X += xw;
         N += 1;
         if (c_fromF) {
@@ -676,12 +679,8 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
           // the last eligible entry moves into the hole; the last pending one fills its place
           if (lane == 0) {
             const int le = nVe - 1;
-            vkey[v_pos] = vkey[le];
-            vso[v_pos] = vso[le];
-            if (nV > nVe) {
-              vkey[le] = vkey[nV - 1];
-              vso[le] = vso[nV - 1];
-            }
+            vent[v_pos] = vent[le];
+            if (nV > nVe) vent[le] = vent[nV - 1];
           }
           --nVe;
           --nV;
@@ -767,7 +766,10 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
 #undef SK_PICK
 #undef SK_F_FIND
 #undef SK_V_FIND
-#undef SK_SHRINK_ROWS
+#undef SK_V_SCAN
+#undef SK_V_MERGE
+#undef SK_CASE
+#undef SK_AT_ROW
 #undef SK_DROP_SHARE
 
 }  // namespace sk
@@ -784,6 +786,7 @@ const void* sim_kernel(int rows, bool retry) {
     case 1: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 1, false>);
     case 2: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 2, false>);
     case 4: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 4, false>);
+    case 6: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 6, false>);
     case 8: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, false>);
     default: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, false>);
   }
@@ -791,19 +794,9 @@ const void* sim_kernel(int rows, bool retry) {
 
 template <int ALGO>
 hipError_t launch_sim(int rows, bool retry, const sk::Params& P, size_t lds, hipStream_t st) {
-  const dim3 grid(P.K), block(64);
-  if (retry) {
-    hipLaunchKernelGGL((sk::k_simulate<ALGO, 16, true>), grid, block, lds, st, P);
-    return hipGetLastError();
-  }
-  switch (rows) {
-    case 1: hipLaunchKernelGGL((sk::k_simulate<ALGO, 1, false>), grid, block, lds, st, P); break;
-    case 2: hipLaunchKernelGGL((sk::k_simulate<ALGO, 2, false>), grid, block, lds, st, P); break;
-    case 4: hipLaunchKernelGGL((sk::k_simulate<ALGO, 4, false>), grid, block, lds, st, P); break;
-    case 8: hipLaunchKernelGGL((sk::k_simulate<ALGO, 8, false>), grid, block, lds, st, P); break;
-    default: hipLaunchKernelGGL((sk::k_simulate<ALGO, 16, false>), grid, block, lds, st, P); break;
-  }
-  return hipGetLastError();
+  sk::Params p = P;
+  void* args[] = {&p};
+  return hipLaunchKernel(sim_kernel<ALGO>(rows, retry), dim3(P.K), dim3(64), args, lds, st);
 }
 
 template <int ALGO>
@@ -857,7 +850,7 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   const bool forced = o.running_capacity > 0;
   const int64_t want = forced ? o.running_capacity : std::min<int64_t>(std::max<int64_t>(nmax, 1), 512);
   int rows = static_cast<int>((want + 63) / 64);
-  rows = rows <= 1 ? 1 : rows <= 2 ? 2 : rows <= 4 ? 4 : rows <= 8 ? 8 : 16;
+  rows = rows <= 1 ? 1 : rows <= 2 ? 2 : rows <= 4 ? 4 : rows <= 6 ? 6 : rows <= 8 ? 8 : 16;
   const bool two_pass = !forced && nmax > 512;
 
   hipStream_t st = static_cast<hipStream_t>(stream);

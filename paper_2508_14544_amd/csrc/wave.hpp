@@ -32,6 +32,20 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
+// v with lane `lane` replaced by the uniform value s (the other lanes keep v).
+// `lane` must come from scalar arithmetic (not straight from a VALU-written
+// SGPR such as v_readlane's result), which needs no wait states.
+__device__ __forceinline__ int32_t writelane(int32_t v, int32_t s, int lane) {
+  const int32_t su = __builtin_amdgcn_readfirstlane(s);
+  const int32_t lu = __builtin_amdgcn_readfirstlane(lane);
+  asm("v_writelane_b32 %0, %1, %2" : "+v"(v) : "s"(su), "{m0}"(lu));
+  return v;
+}
+
+__device__ __forceinline__ uint32_t writelane_u(uint32_t v, uint32_t s, int lane) {
+  return static_cast<uint32_t>(writelane(static_cast<int32_t>(v), static_cast<int32_t>(s), lane));
+}
+
 __device__ __forceinline__ int32_t uniform(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
 template <int CTRL>
