@@ -76,7 +76,7 @@ struct Params {
   int32_t nw_max;        // 64-bit words of the level-0 bitmap
   int32_t nw1_max;       // 64-bit words of the level-1 bitmap
   int32_t cap_v;         // evicted-set capacity
-  int32_t retry_status;  // status for an outgrown running set: retry pass or SCHED_E_UNSUPPORTED
+  int32_t retry_status;  // status for an outgrown running set: next pass (kRetry) or SCHED_E_UNSUPPORTED
 };
 
 // ---------------------------------------------------------------------------
@@ -649,7 +649,7 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
             mm = m ? m : mm;
           }
           if (rr < 0) {
-            status = RETRY_PASS ? SCHED_E_UNSUPPORTED : P.retry_status;
+            status = P.retry_status;
             break;
           }
           fr_row = rr;
@@ -779,9 +779,14 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
 // ---------------------------------------------------------------------------
 namespace {
 
+// Row counts of the register running set: a first pass, then retry passes
+// (RETRY_PASS kernels) for the instances whose running set outgrew it.
 template <int ALGO>
 const void* sim_kernel(int rows, bool retry) {
-  if (retry) return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true>);
+  if (retry) {
+    return rows <= 8 ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, true>)
+                     : reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true>);
+  }
   switch (rows) {
     case 1: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 1, false>);
     case 2: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 2, false>);
@@ -790,6 +795,12 @@ const void* sim_kernel(int rows, bool retry) {
     case 8: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, false>);
     default: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, false>);
   }
+}
+
+// register rows that hold `want` runs
+int rows_for(int64_t want) {
+  const int64_t r = (want + 63) / 64;
+  return r <= 1 ? 1 : r <= 2 ? 2 : r <= 4 ? 4 : r <= 6 ? 6 : r <= 8 ? 8 : 16;
 }
 
 template <int ALGO>
@@ -848,10 +859,17 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   // runs and a second pass with 1024 re-runs only the instances that outgrew it.
   if (o.running_capacity > 1024) return SCHED_E_UNSUPPORTED;
   const bool forced = o.running_capacity > 0;
-  const int64_t want = forced ? o.running_capacity : std::min<int64_t>(std::max<int64_t>(nmax, 1), 512);
-  int rows = static_cast<int>((want + 63) / 64);
-  rows = rows <= 1 ? 1 : rows <= 2 ? 2 : rows <= 4 ? 4 : rows <= 6 ? 6 : rows <= 8 ? 8 : 16;
-  const bool two_pass = !forced && nmax > 512;
+  // passes: the first covers up to 384 runs (every run of most instances);
+  // instances whose running set outgrows it are simulated again with 8, then 16 rows
+  int tiers[3] = {0, 0, 0};
+  int n_tiers = 1;
+  if (forced) {
+    tiers[0] = rows_for(o.running_capacity);
+  } else {
+    tiers[0] = rows_for(std::min<int64_t>(std::max<int64_t>(nmax, 1), 384));
+    if (nmax > 384) tiers[n_tiers++] = 8;
+    if (nmax > 512) tiers[n_tiers++] = 16;
+  }
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   int dev = 0;
@@ -909,7 +927,6 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   P.nw_max = nw;
   P.nw1_max = nw1;
   P.cap_v = cap_v;
-  P.retry_status = two_pass ? sk::kRetry : SCHED_E_UNSUPPORTED;
 
   hipError_t err = hipSuccess;
   const dim3 grid(P.K), block(64);
@@ -919,22 +936,22 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
     default: hipLaunchKernelGGL((sk::k_prepare<SCHED_HSF>), grid, block, 0, st, P); break;
   }
   err = hipGetLastError();
-  for (int pass = 0; pass < (two_pass ? 2 : 1) && err == hipSuccess; ++pass) {
-    const bool retry = pass == 1;
+  for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass) {
     if (lds > 65536) {
       switch (algo) {
-        case SCHED_AMAX: err = set_lds_limit<SCHED_AMAX>(rows, retry, static_cast<int>(lds)); break;
-        case SCHED_AMIN: err = set_lds_limit<SCHED_AMIN>(rows, retry, static_cast<int>(lds)); break;
-        default: err = set_lds_limit<SCHED_HSF>(rows, retry, static_cast<int>(lds)); break;
+        case SCHED_AMAX: err = set_lds_limit<SCHED_AMAX>(tiers[pass], pass > 0, static_cast<int>(lds)); break;
+        case SCHED_AMIN: err = set_lds_limit<SCHED_AMIN>(tiers[pass], pass > 0, static_cast<int>(lds)); break;
+        default: err = set_lds_limit<SCHED_HSF>(tiers[pass], pass > 0, static_cast<int>(lds)); break;
       }
     }
   }
   if (err == hipSuccess && o.event_before) err = hipEventRecord(static_cast<hipEvent_t>(o.event_before), st);
-  for (int pass = 0; pass < (two_pass ? 2 : 1) && err == hipSuccess; ++pass) {
+  for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass) {
+    P.retry_status = pass + 1 < n_tiers ? sk::kRetry : SCHED_E_UNSUPPORTED;
     switch (algo) {
-      case SCHED_AMAX: err = launch_sim<SCHED_AMAX>(rows, pass == 1, P, lds, st); break;
-      case SCHED_AMIN: err = launch_sim<SCHED_AMIN>(rows, pass == 1, P, lds, st); break;
-      default: err = launch_sim<SCHED_HSF>(rows, pass == 1, P, lds, st); break;
+      case SCHED_AMAX: err = launch_sim<SCHED_AMAX>(tiers[pass], pass > 0, P, lds, st); break;
+      case SCHED_AMIN: err = launch_sim<SCHED_AMIN>(tiers[pass], pass > 0, P, lds, st); break;
+      default: err = launch_sim<SCHED_HSF>(tiers[pass], pass > 0, P, lds, st); break;
     }
   }
   if (err == hipSuccess && o.event_after) err = hipEventRecord(static_cast<hipEvent_t>(o.event_after), st);
