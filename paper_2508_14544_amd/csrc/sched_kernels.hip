@@ -391,20 +391,11 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
     c_o = static_cast<int32_t>(so_ >> 16);                                           \
   } while (0)
     // BODY with the compile-time row index r equal to the uniform row RR_
-#define SK_CASE(R_, BODY)                                                            \
-  case R_:                                                                           \
-    if constexpr ((R_) < ROWS) {                                                     \
-      constexpr int r = (R_);                                                        \
+#define SK_AT_ROW(RR_, BODY)                                                         \
+  _Pragma("unroll") for (int r = 0; r < ROWS; ++r) {                                 \
+    if (r == (RR_)) {                                                                \
       BODY                                                                           \
     }                                                                                \
-    break;
-#define SK_AT_ROW(RR_, BODY)                                                         \
-  switch (RR_) {                                                                     \
-    SK_CASE(0, BODY) SK_CASE(1, BODY) SK_CASE(2, BODY) SK_CASE(3, BODY)              \
-    SK_CASE(4, BODY) SK_CASE(5, BODY) SK_CASE(6, BODY) SK_CASE(7, BODY)              \
-    SK_CASE(8, BODY) SK_CASE(9, BODY) SK_CASE(10, BODY) SK_CASE(11, BODY)            \
-    SK_CASE(12, BODY) SK_CASE(13, BODY) SK_CASE(14, BODY) SK_CASE(15, BODY)          \
-    default: break;                                                                  \
   }
     // A run with raw planned end ek and x = xk leaves: every run with
     // t+1 < Rend <= ek loses its share of f at its own planned end.
@@ -594,12 +585,11 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
         const int32_t cE = E - t_r;
         const int32_t lim = win ? M + t - t_r - s : 0x7FFFFFFF;  // h above this violates
         int32_t fl = 0, hmx = INT32_MIN;
-        bool inw[ROWS];
 #pragma unroll
         for (int r = 0; r < ROWS; ++r) {
           const int32_t e = r_end[r];
-          inw[r] = static_cast<uint32_t>(e) - lo2 <= span;
-          const int32_t hv = inw[r] ? r_h[r] : INT32_MIN;
+          const bool in = static_cast<uint32_t>(e) - lo2 <= span;
+          const int32_t hv = in ? r_h[r] : INT32_MIN;
           hmx = hv > hmx ? hv : hmx;
           fl += e >= E ? r_x[r] + cE : 0;
         }
@@ -610,7 +600,8 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
           for (int r = 0; r < ROWS; ++r) {
             const int32_t a = r_h[r] - lim, bb = r_end[r] - 1 - t;
             const int32_t m = a < bb ? a : bb;
-            fix = (inw[r] && r_h[r] > lim && m > fix) ? m : fix;
+            const bool in = static_cast<uint32_t>(r_end[r]) - lo2 <= span;
+            fix = (in && r_h[r] > lim && m > fix) ? m : fix;
           }
           retry_at = t + wave::max_i32(fix);
           wait_until = retry_at;
@@ -635,9 +626,10 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
         if (win) {
           const uint32_t dh = static_cast<uint32_t>(xw) - static_cast<uint32_t>(t_r);
 #pragma unroll
-          for (int r = 0; r < ROWS; ++r)
-            r_h[r] = static_cast<int32_t>(static_cast<uint32_t>(r_h[r]) +
-                                          (inw[r] ? static_cast<uint32_t>(r_end[r]) + dh : 0u));
+          for (int r = 0; r < ROWS; ++r) {
+            const uint32_t e = static_cast<uint32_t>(r_end[r]);
+            r_h[r] = static_cast<int32_t>(static_cast<uint32_t>(r_h[r]) + (e - lo2 <= span ? e + dh : 0u));
+          }
         }
         if (fr_mask == 0ull) {
           int rr = -1;
@@ -768,7 +760,6 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
 #undef SK_V_FIND
 #undef SK_V_SCAN
 #undef SK_V_MERGE
-#undef SK_CASE
 #undef SK_AT_ROW
 #undef SK_DROP_SHARE
 

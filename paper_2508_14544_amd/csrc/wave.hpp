@@ -1,9 +1,10 @@
 // wave.hpp -- wave64 primitives for gfx950 (CDNA4).
 //
-// Reductions run a DPP butterfly inside each row of 16 lanes (quad_perm
-// 1,0,3,2 / 2,3,0,1, then row_half_mirror and row_mirror), after which every
-// lane of a row holds the row result; the four row results are combined in
-// scalar registers via v_readlane.  The result is wave-uniform.
+// 32-bit reductions first fold the four 16-lane rows onto each other with the
+// gfx950 lane swaps (v_permlane32_swap, v_permlane16_swap), then run a DPP
+// butterfly inside each row (quad_perm 1,0,3,2 / 2,3,0,1, row_half_mirror,
+// row_mirror); every lane then holds the result, read once with
+// v_readfirstlane.  The result is wave-uniform.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -32,14 +33,14 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
-// v with lane `lane` replaced by the uniform value s (the other lanes keep v).
-// `lane` must come from scalar arithmetic (not straight from a VALU-written
-// SGPR such as v_readlane's result), which needs no wait states.
+// v_writelane_b32 through its LLVM intrinsic (this compiler has no clang builtin
+// for it): the compiler knows its semantics and inserts the wait states.
+extern "C" __device__ int32_t sk_llvm_writelane(int32_t src, int32_t lane, int32_t old)
+    __asm("llvm.amdgcn.writelane");
+
+// v with lane `lane` replaced by the uniform value s (the other lanes keep v)
 __device__ __forceinline__ int32_t writelane(int32_t v, int32_t s, int lane) {
-  const int32_t su = __builtin_amdgcn_readfirstlane(s);
-  const int32_t lu = __builtin_amdgcn_readfirstlane(lane);
-  asm("v_writelane_b32 %0, %1, %2" : "+v"(v) : "s"(su), "{m0}"(lu));
-  return v;
+  return sk_llvm_writelane(s, lane, v);
 }
 
 __device__ __forceinline__ uint32_t writelane_u(uint32_t v, uint32_t s, int lane) {
@@ -53,31 +54,51 @@ __device__ __forceinline__ int32_t dpp(int32_t v) {
   return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
 }
 
+// Cross-row folds (gfx950): after fold_rows every lane holds OP over the four
+// lanes {l mod 16 + 16 k}; v_permlane32_swap exchanges the two 32-lane halves
+// and v_permlane16_swap the odd and even 16-lane rows.
+template <typename F>
+__device__ __forceinline__ uint32_t fold_rows(uint32_t v, F op) {
+  const auto h = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  v = op(static_cast<uint32_t>(h[0]), static_cast<uint32_t>(h[1]));
+  const auto q = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return op(static_cast<uint32_t>(q[0]), static_cast<uint32_t>(q[1]));
+}
+
+template <typename F>
+__device__ __forceinline__ uint32_t fold_in_row(uint32_t v, F op) {
+  v = op(v, static_cast<uint32_t>(dpp<kDppQuadXor1>(static_cast<int32_t>(v))));
+  v = op(v, static_cast<uint32_t>(dpp<kDppQuadXor2>(static_cast<int32_t>(v))));
+  v = op(v, static_cast<uint32_t>(dpp<kDppRowHalfMirror>(static_cast<int32_t>(v))));
+  v = op(v, static_cast<uint32_t>(dpp<kDppRowMirror>(static_cast<int32_t>(v))));
+  return v;
+}
+
+struct OpMaxI32 {
+  __device__ uint32_t operator()(uint32_t a, uint32_t b) const {
+    return static_cast<int32_t>(a) > static_cast<int32_t>(b) ? a : b;
+  }
+};
+struct OpAddU32 {
+  __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a + b; }
+};
+struct OpMinU32 {
+  __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a < b ? a : b; }
+};
+
 __device__ __forceinline__ int32_t max_i32(int32_t v) {
-  v = max(v, dpp<kDppQuadXor1>(v));
-  v = max(v, dpp<kDppQuadXor2>(v));
-  v = max(v, dpp<kDppRowHalfMirror>(v));
-  v = max(v, dpp<kDppRowMirror>(v));
-  int32_t a = readlane(v, 0), b = readlane(v, 16), c = readlane(v, 32), d = readlane(v, 48);
-  return max(max(a, b), max(c, d));
+  const uint32_t r = fold_in_row(fold_rows(static_cast<uint32_t>(v), OpMaxI32{}), OpMaxI32{});
+  return uniform(static_cast<int32_t>(r));
 }
 
 __device__ __forceinline__ int32_t sum_i32(int32_t v) {
-  v += dpp<kDppQuadXor1>(v);
-  v += dpp<kDppQuadXor2>(v);
-  v += dpp<kDppRowHalfMirror>(v);
-  v += dpp<kDppRowMirror>(v);
-  return readlane(v, 0) + readlane(v, 16) + readlane(v, 32) + readlane(v, 48);
+  const uint32_t r = fold_in_row(fold_rows(static_cast<uint32_t>(v), OpAddU32{}), OpAddU32{});
+  return uniform(static_cast<int32_t>(r));
 }
 
 __device__ __forceinline__ uint32_t min_u32(uint32_t v) {
-  auto m = [](uint32_t x, uint32_t y) { return x < y ? x : y; };
-  v = m(v, static_cast<uint32_t>(dpp<kDppQuadXor1>(static_cast<int32_t>(v))));
-  v = m(v, static_cast<uint32_t>(dpp<kDppQuadXor2>(static_cast<int32_t>(v))));
-  v = m(v, static_cast<uint32_t>(dpp<kDppRowHalfMirror>(static_cast<int32_t>(v))));
-  v = m(v, static_cast<uint32_t>(dpp<kDppRowMirror>(static_cast<int32_t>(v))));
-  uint32_t a = readlane_u(v, 0), b = readlane_u(v, 16), c = readlane_u(v, 32), d = readlane_u(v, 48);
-  return m(m(a, b), m(c, d));
+  const uint32_t r = fold_in_row(fold_rows(v, OpMinU32{}), OpMinU32{});
+  return static_cast<uint32_t>(uniform(static_cast<int32_t>(r)));
 }
 
 // 64-bit sums for the epilogue (not on the hot path).
