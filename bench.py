@@ -106,10 +106,15 @@ def cpu_baseline(batch, algo, g_out, target_s: float, threads: int):
     sel = np.concatenate([np.arange(batch.offsets[k], batch.offsets[k + 1]) for k in sample])
     ok = ok and np.array_equal(g_out["completion"][sel], ref["completion"])
     ok = ok and np.array_equal(g_out["evictions"][sel], ref["evictions"])
+    # algorithmic work count (untimed pass with the oracle's counters) on part of the sample
+    sub = sample[::3]
+    st = O.simulate_batch(batch, algo, instances=sub, threads=threads, stats=True)
+    work = sum(x["work"] for x in st["stats"])
+    w_ratio = work / max(1, int(st["request_steps"].sum()))
     return {
         "value": rs / wall, "unit": "request-steps/s", "cores": threads, "kind": "oracle",
         "sample": f"{len(sample)} of {K} instances (every {stride}th), {rs} request-steps in {wall:.1f} s",
-    }, bool(ok)
+    }, bool(ok), (w_ratio, len(sub))
 
 
 def main():
@@ -124,6 +129,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--instances", default="",
+                    help="comma-separated instance ids: simulate only these (critical-path profiling)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, run device copies of this size (for rocprofv3 counter calibration)")
     args = ap.parse_args()
@@ -142,8 +149,17 @@ def main():
     B.load_library()
     algo = B.ALGOS[args.algo]
     batch = W.generate(args.workload, args.seed)
+    subset = [int(x) for x in args.instances.split(",") if x.strip()]
+    if subset:
+        batch = batch.subset(subset)
     dev = torch.device("cuda:0")
+    torch.cuda.synchronize()
+    h0 = time.perf_counter()
     db = B.to_device(batch, dev)
+    torch.cuda.synchronize()
+    h2d_ms = (time.perf_counter() - h0) * 1e3
+    h2d_bytes = sum(int(t.numel()) * t.element_size() for t in
+                    (db.offsets, db.arrival, db.prompt, db.output, db.lower, db.upper) if t is not None)
     out = B.alloc_results(db)
     stream = torch.cuda.current_stream(dev)
     kw = dict(stream=stream, running_capacity=args.running_capacity)
@@ -167,7 +183,10 @@ def main():
     sim_ms = [a.elapsed_ms(b) for a, b in ev]
     sim_avg_ms = sum(sim_ms) / len(sim_ms)
 
+    d0 = time.perf_counter()
     g = {k: (None if v is None else v.cpu().numpy()) for k, v in out.items()}
+    d2h_ms = (time.perf_counter() - d0) * 1e3
+    d2h_bytes = sum(int(v.numel()) * v.element_size() for v in out.values() if v is not None)
     status_ok = bool((g["status"] == 0).all())
     rs = int(g["request_steps"].sum())
     value = rs / (step_ms / 1e3)
@@ -204,6 +223,8 @@ def main():
             "seed": args.seed,
             "request_steps_per_step": rs,
             "instance_steps_per_step": int(g["makespan"].astype(np.int64).sum()),
+            "requests_x_makespan_per_step": int((np.diff(batch.offsets) * g["makespan"].astype(np.int64)).sum()),
+            "instances_subset": subset or None,
             "all_status_ok": status_ok,
         },
         "roofline": {
@@ -215,15 +236,23 @@ def main():
             "frac": achieved / PEAK_INT32_LANE_OPS,
             "traffic": traffic,
             "kernel_ms": sim_avg_ms,
+            "kernel_ms_median": float(np.median(sim_ms)),
             "ops_per_request_step": OPS_PER_REQUEST_STEP,
+        },
+        "transfers": {
+            "note": "torch copies from/to pageable host memory, including allocation",
+            "h2d_ms": h2d_ms, "h2d_bytes": h2d_bytes, "d2h_ms": d2h_ms, "d2h_bytes": d2h_bytes,
+            "pcie_inclusive_request_steps_per_s": rs / ((step_ms + h2d_ms + d2h_ms) / 1e3),
         },
         "wall_s_timed_region": wall,
     }
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, os.cpu_count() or 1)
-        cb, parity = cpu_baseline(batch, algo, g, args.cpu_seconds, threads)
+        cb, parity, (w_ratio, w_n) = cpu_baseline(batch, algo, g, args.cpu_seconds, threads)
         result["cpu_baseline"] = cb
         result["parity_on_cpu_sample"] = parity
+        result["w_alg"] = {"per_request_step": w_ratio, "per_s": value * w_ratio,
+                           "sample": f"oracle work counters on {w_n} sampled instances"}
     print(json.dumps(result), flush=True)
 
 

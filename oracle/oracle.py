@@ -28,7 +28,7 @@ AMAX, AMIN, HSF = 0, 1, 2
 ALGOS = {"amax": AMAX, "amin": AMIN, "hsf": HSF}
 OK, E_INVAL, E_INTERVAL, E_TOO_BIG, E_STEP_CAP, E_ARRIVAL = 0, -1, -2, -3, -4, -7
 EV_START, EV_EVICT, EV_COMPLETE = 0, 1, 2
-STAT_NAMES = ["max_running", "max_evicted_waiting", "max_waiting", "steps", "tests", "evict_events"]
+STAT_NAMES = ["max_running", "max_evicted_waiting", "max_waiting", "steps", "tests", "evict_events", "work"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SO = os.path.join(_HERE, "liboracle.so")

@@ -244,6 +244,11 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
           ek[k].key_est = est[running[k]];
         }
         qsort(ek, n_running, sizeof(evict_key_t), cmp_evict);
+        if (stats) {
+          int64_t lg = 0;
+          while ((INT64_C(1) << lg) < n_running) lg++;
+          stats[ORC_STAT_WORK] += (int64_t)n_running * lg;
+        }
         int32_t n_removed = 0;
         for (int32_t k = 0; k < n_running && P > M; k++) {
           int32_t i = ek[k].i;
@@ -293,7 +298,10 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
       qp[nq] = t;
       qs[nq] = s[w];
       qe[nq] = t + est[w];
-      if (stats) stats[ORC_STAT_TESTS]++;
+      if (stats) {
+        stats[ORC_STAT_TESTS]++;
+        stats[ORC_STAT_WORK] += nq + 1;
+      }
       if (!feasible(nq + 1, qp, qs, qe, M)) break;
       nq++;
       heap_pop(&waiting);
@@ -307,6 +315,7 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
     /* 6. this step processes every running request once */
     *request_steps += n_running;
     if (stats) {
+      stats[ORC_STAT_WORK] += (int64_t)n_running * (algo == ORC_AMIN ? 2 : 1);
       if (n_running > stats[ORC_STAT_MAX_RUNNING]) stats[ORC_STAT_MAX_RUNNING] = n_running;
       if (n_evicted_waiting > stats[ORC_STAT_MAX_EVICTED_WAIT])
         stats[ORC_STAT_MAX_EVICTED_WAIT] = n_evicted_waiting;

@@ -44,6 +44,9 @@ enum {
   ORC_STAT_STEPS = 3,           /* number of steps simulated                   */
   ORC_STAT_TESTS = 4,           /* feasibility tests evaluated                 */
   ORC_STAT_EVICT_EVENTS = 5,    /* steps at which at least one eviction happened */
+  ORC_STAT_WORK = 6,            /* algorithmic work count: per step |S_t| (twice for A_min:
+                                   projection), per feasibility test |Q| (planned set with the
+                                   candidate), per eviction event |S_t| ceil(log2 |S_t|) (a sort) */
   ORC_STAT_COUNT = 8
 };
 

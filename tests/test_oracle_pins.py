@@ -222,3 +222,31 @@ def test_theorem31_upper_bound_soft(l, u):
         M = 40 * (1 + u)
         ratio = O.simulate(inst, O.AMAX, M)["tel"] / O.simulate(inst, O.HSF, M)["tel"]
         assert ratio <= bound
+
+
+def test_work_counter_definition():
+    """The reported algorithmic work count W_alg: per step |S_t| (twice for A_min,
+    whose projection reads the running set again), per feasibility test |Q|
+    including the candidate, per eviction event |S_t| ceil(log2 |S_t|).  A single
+    request (s=1, o=3, ample M) is tested once with |Q| = 1 and runs in steps
+    0, 1, 2 (it completes at step 3), so W = 1 + 3 = 4, and 1 + 2*3 = 7 for A_min."""
+    inst = {"arrival": np.zeros(1, np.int32), "prompt": np.array([1], np.int32),
+            "output": np.array([3], np.int32), "lower": np.array([1], np.int32),
+            "upper": np.array([3], np.int32)}
+    for algo, want in ((O.AMAX, 4), (O.HSF, 4), (O.AMIN, 7)):
+        r = O.simulate(inst, algo, 100, stats=True)
+        assert r["stats"]["work"] == want
+        assert r["request_steps"] == 3
+    # two requests that cannot run together (M = 4, s + o = 4 each), H-SF: the
+    # second is refused at steps 0, 1, 2 (|Q| = 2 with the running one) and at
+    # step 3, where the run completing at 3 still holds s + o = 4 (|Q| = 2); it is
+    # admitted at step 4 (|Q| = 1) and completes at 7.  Tests: 1 + 2+2+2+2 + 1 = 10;
+    # request-steps: 1 at steps 0..2, 0 at step 3, 1 at steps 4..6.
+    inst2 = {"arrival": np.zeros(2, np.int32), "prompt": np.array([1, 1], np.int32),
+             "output": np.array([3, 3], np.int32), "lower": np.array([3, 3], np.int32),
+             "upper": np.array([3, 3], np.int32)}
+    r = O.simulate(inst2, O.HSF, 4, stats=True)
+    assert r["completion"].tolist() == [3, 7]
+    assert r["stats"]["tests"] == 6
+    assert r["request_steps"] == 6
+    assert r["stats"]["work"] == 10 + 6
