@@ -24,8 +24,8 @@ from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
-AMAX, AMIN, HSF = 0, 1, 2
-ALGOS = {"amax": AMAX, "amin": AMIN, "hsf": HSF}
+AMAX, AMIN, HSF, AELL, ADAPTIVE = 0, 1, 2, 3, 4
+ALGOS = {"amax": AMAX, "amin": AMIN, "hsf": HSF, "aell": AELL, "adaptive": ADAPTIVE}
 OK, E_INVAL, E_INTERVAL, E_TOO_BIG, E_STEP_CAP, E_ARRIVAL = 0, -1, -2, -3, -4, -7
 EV_START, EV_EVICT, EV_COMPLETE = 0, 1, 2
 STAT_NAMES = ["max_running", "max_evicted_waiting", "max_waiting", "steps", "tests", "evict_events", "work"]
@@ -65,6 +65,8 @@ def _load():
                                          P64, P64, ctypes.POINTER(_Event), ctypes.c_int64, P64]
             lib.orc_default_step_cap.restype = ctypes.c_int64
             lib.orc_default_step_cap.argtypes = [ctypes.c_int32, P32, P32]
+            lib.orc_adaptive_choice.restype = ctypes.c_int32
+            lib.orc_adaptive_choice.argtypes = [ctypes.c_int32, P32, P32]
             _lib = lib
     return _lib
 
@@ -121,6 +123,13 @@ def simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap: int = 
     return out
 
 
+def adaptive_choice(inst: Dict[str, Sequence[int]]) -> int:
+    """AELL or AMIN: the algorithm ADAPTIVE simulates for this instance."""
+    lib = _load()
+    lo, up = _c32(inst["lower"]), _c32(inst["upper"])
+    return int(lib.orc_adaptive_choice(int(lo.shape[0]), _p32(lo), _p32(up)))
+
+
 def default_step_cap(inst: Dict[str, Sequence[int]]) -> int:
     lib = _load()
     o = _c32(inst["output"])
@@ -167,9 +176,16 @@ def literal_simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap
     Each step: arrivals join the waiting list; runs reaching p + o complete;
     for A_min the running set's memory at t+1 is projected and runs are removed
     in ascending (o~, index) while it exceeds M, each removed request's o~
-    rising to the tokens it had generated; then waiting requests are taken in
-    (planning length, index) order while equation (2) keeps holding.
+    rising to the tokens it had generated; for A_l a run that has generated l
+    tokens without finishing is removed, plans with u from then on and goes to
+    the back of the queue (fresh requests first, promoted ones in promotion
+    order, same step by index) and may restart at once; then waiting requests
+    are taken in (planning length, index) order (A_l: queue order) while
+    equation (2) keeps holding.  ADAPTIVE runs the algorithm adaptive_choice
+    picks.
     """
+    if algo == ADAPTIVE:
+        algo = adaptive_choice(inst)
     o = [int(x) for x in inst["output"]]
     n = len(o)
     s = [int(x) for x in inst["prompt"]]
@@ -180,7 +196,10 @@ def literal_simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap
         plan = list(o)
     else:
         plan = [int(x) for x in inst["lower"]]
+    upper = [int(x) for x in inst["upper"]] if inst.get("upper") is not None else None
     cap = step_cap if step_cap > 0 else default_step_cap(inst)
+    queue_pos = list(range(n))   # A_l order: fresh by index, then promotion order
+    promotions = 0
 
     start = {}                  # request -> current start step (running only)
     waiting: List[int] = []
@@ -216,11 +235,21 @@ def literal_simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap
                 del start[i]
                 waiting.append(i)
                 eligible_from[i] = t + 1
+        if algo == AELL:
+            for i in sorted(r for r in start if start[r] + plan[r] == t):
+                plan[i] = upper[i]
+                queue_pos[i] = n + promotions
+                promotions += 1
+                evict_count[i] += 1
+                del start[i]
+                waiting.append(i)
+                eligible_from[i] = t
 
         # in-progress runs: (start, prompt, planned length from its start)
         in_progress = [(start[i], s[i], max(plan[i], t + 1 - start[i])) for i in start]
         in_progress += [(t - o[i], s[i], o[i]) for i in finished_now]
-        order = sorted((w for w in waiting if eligible_from[w] <= t), key=lambda r: (plan[r], r))
+        order_key = (lambda r: (queue_pos[r], r)) if algo == AELL else (lambda r: (plan[r], r))
+        order = sorted((w for w in waiting if eligible_from[w] <= t), key=order_key)
         chosen: List[int] = []
         for w in order:
             trial = chosen + [w]
@@ -334,6 +363,8 @@ def audit(inst: Dict[str, Sequence[int]], algo: int, M: int, result: Dict[str, o
     n = len(o)
     s = [int(x) for x in inst["prompt"]]
     arr = [int(x) for x in inst["arrival"]] if inst.get("arrival") is not None else [0] * n
+    if algo == ADAPTIVE:
+        algo = adaptive_choice(inst)
     events = result["events"]
     assert result["status"] == OK
     runs = []                # (request, start, end, evicted?)
@@ -345,7 +376,8 @@ def audit(inst: Dict[str, Sequence[int]], algo: int, M: int, result: Dict[str, o
         if kind == EV_START:
             assert i not in open_run, "request started twice"
             assert t >= arr[i], "started before arrival"
-            assert t > last_evict[i], "restarted in the step it was evicted"
+            if algo == AMIN:
+                assert t > last_evict[i], "restarted in the step it was evicted"
             open_run[i] = t
             final_start[i] = t
         elif kind == EV_EVICT:
@@ -372,8 +404,15 @@ def audit(inst: Dict[str, Sequence[int]], algo: int, M: int, result: Dict[str, o
         pre = sum(s[i] + tau - p for (i, p, e, ev) in runs if p < tau <= e)
         post = sum(s[i] + tau - p for (i, p, e, ev) in runs if p <= tau <= e and not (ev and e == tau))
         assert pre <= M and post <= M, f"memory {pre}/{post} > {M} at step {tau}"
+    if algo == AELL:
+        # promotions: exactly l tokens after the start, only for o > l, once per request
+        lo = [int(x) for x in inst["lower"]]
+        for (i, p, e, ev) in runs:
+            if ev:
+                assert e - p == lo[i] and o[i] > lo[i], "promotion not at l tokens"
+        assert all(c <= 1 for c in n_evict), "a request was promoted twice"
     # evictions happen only when the projection at tau+1 overflows, and stop once it fits
-    ev_steps = sorted({e for (i, p, e, ev) in runs if ev})
+    ev_steps = sorted({e for (i, p, e, ev) in runs if ev}) if algo == AMIN else []
     for tau in ev_steps:
         # the running set at the eviction point: started before tau, not completing at tau
         before = sum(s[i] + tau + 1 - p for (i, p, e, ev) in runs

@@ -15,6 +15,12 @@
  *     the running lower bound o~, evict in ascending o~ on projected overflow
  *     at t+1 and raise o~ to the tokens already generated.
  *   - Algorithm 3 (H-SF): plan with the true output o, shortest first.
+ *   - Algorithm 5 (A_l, the promote-l policy of Section 5.1): plan a new run
+ *     with o~ = l; a run that reaches l generated tokens unfinished is removed,
+ *     its o~ becomes u, and it rejoins the queue behind every fresh request
+ *     (promoted requests keep their promotion order); it may restart at once.
+ *   - The adaptive switch of Section 5.1 between A_min and A_l at
+ *     alpha* = (3 - sqrt 5)/2, from Theorems 5.1 and 5.2.
  *   - Equation (3) (total end-to-end latency).
  * Readings where the paper is silent (each listed in the design notes):
  *   memory of a run counts at both its start and its completion step; a
@@ -32,18 +38,19 @@
 enum { NOT_ARRIVED = 0, WAITING = 1, RUNNING = 2, DONE = 3 };
 
 /* ---------------------------------------------------------------------------
- * Waiting set: binary min-heap of request indices ordered by (est, index).
+ * Waiting set: binary min-heap of request indices ordered by (key, index), where
+ * key is the planning length (A_max, A_min, H-SF) or the queue position (A_l).
  * Only "peek the smallest" and "remove the smallest" are needed, because the
  * admission walk stops at the first request that does not fit.
  * ------------------------------------------------------------------------- */
 typedef struct {
   int32_t* idx;
   int64_t size;
-  const int64_t* est;
+  const int64_t* key;
 } heap_t;
 
 static int key_less(const heap_t* h, int32_t x, int32_t y) {
-  if (h->est[x] != h->est[y]) return h->est[x] < h->est[y];
+  if (h->key[x] != h->key[y]) return h->key[x] < h->key[y];
   return x < y;
 }
 
@@ -107,6 +114,11 @@ static int cmp_evict(const void* x, const void* y) {
   return a->i < b->i ? -1 : (a->i > b->i);
 }
 
+static int cmp_index(const void* x, const void* y) {
+  const int32_t a = *(const int32_t*)x, b = *(const int32_t*)y;
+  return a < b ? -1 : (a > b);
+}
+
 int64_t orc_default_step_cap(int32_t n, const int32_t* a, const int32_t* o) {
   int64_t max_a = 0, sum = 0;
   for (int32_t i = 0; i < n; i++) {
@@ -136,16 +148,31 @@ static int validate(int32_t n, const int32_t* a, const int32_t* s, const int32_t
     if (ai < 0) return ORC_E_ARRIVAL;
     if (i > 0 && a && a[i] < a[i - 1]) return ORC_E_ARRIVAL;
   }
+  const int need_l = algo == ORC_AMIN || algo == ORC_AELL;
+  const int need_u = algo == ORC_AMAX || algo == ORC_AELL;
   for (int32_t i = 0; i < n; i++) {
     if (o[i] < 1 || s[i] < 0) return ORC_E_INTERVAL;
-    if (algo == ORC_AMIN && (l[i] < 1 || l[i] > o[i])) return ORC_E_INTERVAL;
-    if (algo == ORC_AMAX && u[i] < o[i]) return ORC_E_INTERVAL;
+    if (need_l && (l[i] < 1 || l[i] > o[i])) return ORC_E_INTERVAL;
+    if (need_u && u[i] < o[i]) return ORC_E_INTERVAL;
   }
   for (int32_t i = 0; i < n; i++) {
     if ((int64_t)s[i] + o[i] > M) return ORC_E_TOO_BIG;
-    if (algo == ORC_AMAX && (int64_t)s[i] + u[i] > M) return ORC_E_TOO_BIG;
+    if (need_u && (int64_t)s[i] + u[i] > M) return ORC_E_TOO_BIG;
   }
   return ORC_OK;
+}
+
+int32_t orc_adaptive_choice(int32_t n, const int32_t* l, const int32_t* u) {
+  int64_t L = 0, U = 0;
+  for (int32_t i = 0; i < n; i++) {
+    L += l[i];
+    U += u[i];
+  }
+  /* alpha = L/U < (3 - sqrt 5)/2  <=>  sqrt(5) U < 3U - 2L  <=>  5 U^2 < (3U - 2L)^2 */
+  if (n == 0 || 3 * U - 2 * L <= 0) return ORC_AMIN;
+  const unsigned __int128 d = (unsigned __int128)(3 * U - 2 * L);
+  const unsigned __int128 uu = (unsigned __int128)U;
+  return d * d > 5 * uu * uu ? ORC_AELL : ORC_AMIN;
 }
 
 int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o,
@@ -162,9 +189,10 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
   *total_evictions = 0;
   if (n_events) *n_events = 0;
   if (n < 0 || M <= 0 || (n > 0 && (!s || !o || !completion))) return ORC_E_INVAL;
-  if (algo != ORC_AMAX && algo != ORC_AMIN && algo != ORC_HSF) return ORC_E_INVAL;
-  if (n > 0 && algo == ORC_AMIN && !l) return ORC_E_INVAL;
-  if (n > 0 && algo == ORC_AMAX && !u) return ORC_E_INVAL;
+  if (algo < ORC_AMAX || algo > ORC_ADAPTIVE) return ORC_E_INVAL;
+  if (n > 0 && (algo == ORC_AMIN || algo == ORC_AELL || algo == ORC_ADAPTIVE) && !l) return ORC_E_INVAL;
+  if (n > 0 && (algo == ORC_AMAX || algo == ORC_AELL || algo == ORC_ADAPTIVE) && !u) return ORC_E_INVAL;
+  if (algo == ORC_ADAPTIVE) algo = orc_adaptive_choice(n, l, u);
   for (int32_t i = 0; i < n; i++) {
     completion[i] = -1;
     if (evictions) evictions[i] = 0;
@@ -185,12 +213,19 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
   int64_t* qe = (int64_t*)malloc(sizeof(int64_t) * (n + 1));
   evict_key_t* ek = (evict_key_t*)malloc(sizeof(evict_key_t) * n);
   int32_t* evc = (int32_t*)calloc(n, sizeof(int32_t));
-  heap_t waiting = {heap_mem, 0, est};
+  /* queue position (A_l): fresh requests by index, promoted ones after every
+   * fresh one, in promotion order */
+  int64_t* qpos = (int64_t*)malloc(sizeof(int64_t) * n);
+  int32_t* promoted = (int32_t*)malloc(sizeof(int32_t) * n);
+  int64_t n_promotions = 0;
+  heap_t waiting = {heap_mem, 0, algo == ORC_AELL ? qpos : est};
 
   /* Planning length: u (A_max, Alg. 1), o (H-SF, Alg. 3), o~ initialised to l
-   * (A_min, Alg. 2 and Alg. 4). */
-  for (int32_t i = 0; i < n; i++)
+   * (A_min, Alg. 2 and Alg. 4; A_l, Alg. 5). */
+  for (int32_t i = 0; i < n; i++) {
     est[i] = (algo == ORC_AMAX) ? u[i] : (algo == ORC_HSF) ? o[i] : l[i];
+    qpos[i] = i;
+  }
 
   int32_t n_running = 0, n_deferred = 0, n_done = 0, next_arrival = 0;
   int32_t n_evicted_waiting = 0;
@@ -271,6 +306,38 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
       }
     }
 
+    /* 4'. A_l: a run that has generated o~ = l tokens without finishing has
+     *     o > l; it leaves the running set, plans with u from now on and joins
+     *     the back of the queue (same-step promotions in index order), where it
+     *     may be admitted again at this step (Alg. 5). */
+    if (algo == ORC_AELL) {
+      int32_t n_prom = 0;
+      kept = 0;
+      for (int32_t k = 0; k < n_running; k++) {
+        int32_t i = running[k];
+        if (p[i] + est[i] == t) promoted[n_prom++] = i;
+        else running[kept++] = i;
+      }
+      if (n_prom > 0) {
+        if (stats) {
+          stats[ORC_STAT_EVICT_EVENTS]++;
+          stats[ORC_STAT_WORK] += n_running;
+        }
+        n_running = kept;
+        qsort(promoted, n_prom, sizeof(int32_t), cmp_index);
+        for (int32_t x = 0; x < n_prom; x++) {
+          int32_t i = promoted[x];
+          est[i] = u[i];
+          qpos[i] = (int64_t)n + n_promotions++;
+          evc[i]++;
+          state[i] = WAITING;
+          n_evicted_waiting++;
+          heap_push(&waiting, i);
+          log_event(events, events_cap, &nev, t, ORC_EV_EVICT, i);
+        }
+      }
+    }
+
     /* 5. admission: the planned set holds the runs completing now (present
      *    only at c = t) and the running ones (planned end p + est, but at least
      *    t+1 since they are known to be present then).  Walk the eligible
@@ -348,5 +415,7 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
   free(qe);
   free(ek);
   free(evc);
+  free(qpos);
+  free(promoted);
   return st;
 }

@@ -16,7 +16,11 @@
 extern "C" {
 #endif
 
-enum { ORC_AMAX = 0, ORC_AMIN = 1, ORC_HSF = 2 };
+/* ORC_AELL: the promote-l policy A_l (Section 5.1, Algorithm 5);
+ * ORC_ADAPTIVE: per instance, A_l when the ratio alpha = (sum l)/(sum u) is
+ * below alpha* = (3 - sqrt 5)/2 (where Theorem 5.2's bound for A_l is below
+ * Theorem 5.1's for A_min, Section 5.1), A_min otherwise. */
+enum { ORC_AMAX = 0, ORC_AMIN = 1, ORC_HSF = 2, ORC_AELL = 3, ORC_ADAPTIVE = 4 };
 
 enum {
   ORC_OK = 0,
@@ -53,9 +57,11 @@ enum {
 /*
  * Simulate one instance of n requests.
  *   a, s, o : arrival step, prompt size, true output length (length n).
- *   l, u    : predicted interval bounds; l is needed for A_min, u for A_max
- *             (either may be NULL when the algorithm does not read it).
- *   algo    : ORC_AMAX, ORC_AMIN or ORC_HSF.
+ *   l, u    : predicted interval bounds; l is needed for A_min, u for A_max,
+ *             both for A_l and the adaptive choice (either may be NULL when the
+ *             algorithm does not read it).
+ *   algo    : ORC_AMAX, ORC_AMIN, ORC_HSF, ORC_AELL or ORC_ADAPTIVE (which
+ *             simulates orc_adaptive_choice's algorithm).
  *   M       : KV-cache budget in tokens (> 0).
  *   step_cap: last step index that may be simulated; <= 0 selects the default
  *             min(2^30, 4*(max a + sum(o+1)) + 64).
@@ -72,6 +78,11 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
                  int64_t* tel, int64_t* makespan, int64_t* request_steps,
                  int64_t* total_evictions, int64_t* stats, orc_event_t* events,
                  int64_t events_cap, int64_t* n_events);
+
+/* The adaptive choice for one instance: ORC_AELL iff (sum l)/(sum u) <
+ * (3 - sqrt 5)/2, decided exactly as (3U - 2L)^2 > 5U^2; ORC_AMIN otherwise
+ * (also for n = 0). */
+int32_t orc_adaptive_choice(int32_t n, const int32_t* l, const int32_t* u);
 
 /* The default step cap for an instance (same formula as above). */
 int64_t orc_default_step_cap(int32_t n, const int32_t* a, const int32_t* o);

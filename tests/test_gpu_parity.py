@@ -71,6 +71,8 @@ def test_paper_examples(B, path):
     g = json.load(open(path))
     batch = W.from_lists(g["M"], [g["instance"]], name=os.path.basename(path))
     for name, exp in g["expected"].items():
+        if name not in ALGOS:
+            continue
         out = gpu_run(B, batch, ALGOS[name])
         assert int(out["status"][0]) == 0
         assert out["completion"].tolist() == exp["completion"]

@@ -250,3 +250,109 @@ def test_work_counter_definition():
     assert r["stats"]["tests"] == 6
     assert r["request_steps"] == 6
     assert r["stats"]["work"] == 10 + 6
+
+
+def _two_point(l, u, a, b, seed, s=0):
+    rng = np.random.default_rng(seed)
+    o = np.array([l] * (a * u) + [u] * (b * l))
+    rng.shuffle(o)
+    n = len(o)
+    return {"prompt": np.full(n, s), "output": o, "lower": np.full(n, l), "upper": np.full(n, u)}, o
+
+
+@pytest.mark.parametrize("l,u,a,b,seed", [(2, 8, 3, 5, 0), (3, 12, 4, 6, 1), (4, 9, 10, 10, 2), (5, 20, 6, 4, 3)])
+def test_aell_closed_form_theorem52_instance(l, u, a, b, seed):
+    # The construction of Theorem 5.2's proof: two-point outputs {l, u}, s = 0,
+    # M = l*u, a*u short and b*l long requests in random index order.  A_l plans
+    # every fresh request with l: batch j takes requests [j*u, (j+1)*u) at step
+    # j*l (they hold l each at their planned end); shorts complete at (j+1)*l,
+    # longs are promoted then.  After the B1 = n/u fresh batches the longs run in
+    # promotion order, l at a time (u each at the end): batch m completes at
+    # B1*l + (m+1)*u.  Runs never overlap a refused step because s = 0.
+    inst, o = _two_point(l, u, a, b, seed)
+    n = len(o)
+    r = O.simulate(inst, O.AELL, l * u)
+    b1 = n // u
+    tel = sum((i // u + 1) * l for i in range(n) if o[i] == l)
+    tel += sum(b1 * l + (q // l + 1) * u for q in range(b * l))
+    assert r["tel"] == tel
+    assert r["total_evictions"] == b * l
+    assert r["request_steps"] == n * l + b * l * u
+
+
+def test_aell_ratio_approaches_theorem52():
+    # Theorem 5.2 (proof, eq. (3)): TEL(A_l)/TEL(H-SF) = 1 + (a^2 t + 2 a^2)/(a^2 t^2
+    # + 2 a^2 t + 1) + O(1/M) with a = l/u and t = (#short)/(#long).  The exact
+    # H-SF total on the construction is Theorem 3.2's (u*l*(1+..+A) + B*l*A*l +
+    # u*l*(1+..+B)); the discrete ratio approaches the limit from below.
+    l, u, a, b = 10, 40, 20, 20
+    inst, o = _two_point(l, u, a, b, 4)
+    M = l * u
+    ra = O.simulate(inst, O.AELL, M)["tel"]
+    rh = O.simulate(inst, O.HSF, M)["tel"]
+    assert rh == u * l * a * (a + 1) // 2 + b * l * a * l + u * l * b * (b + 1) // 2
+    al, t = l / u, (a * u) / (b * l)
+    limit = 1 + (al ** 2 * t + 2 * al ** 2) / (al ** 2 * t ** 2 + 2 * al ** 2 * t + 1)
+    assert limit - 0.01 <= ra / rh <= limit
+
+
+def test_amin_two_point_theorem51_soft():
+    # Theorem 5.1: under two-point outputs CR(A_min) <= (3 - alpha)/2 + O(1/M).
+    # Checked (soft, in the limit sense) at M = 4000 on 4000 shuffled requests.
+    l, u = 10, 40
+    rng = np.random.default_rng(0)
+    o = np.array([l] * 2000 + [u] * 2000)
+    rng.shuffle(o)
+    n = len(o)
+    inst = {"prompt": np.ones(n, int), "output": o, "lower": np.full(n, l), "upper": np.full(n, u)}
+    ratio = O.simulate(inst, O.AMIN, 4000)["tel"] / O.simulate(inst, O.HSF, 4000)["tel"]
+    assert ratio <= (3 - l / u) / 2
+
+
+def test_aell_reduction_exact_lower_bounds_sorted():
+    # With l = o (the lower bound is exact) nothing is ever promoted; if o is
+    # non-decreasing in the index, A_l's queue order is H-SF's (o, index) order,
+    # so the two schedules coincide.
+    b = W.random_small(11, 40, 9, s_max=5, o_max=9, M=25)
+    for k in range(b.num_instances):
+        inst = dict(b.instance(k))
+        order = np.argsort(inst["output"], kind="stable")
+        inst = {f: (None if v is None else np.asarray(v)[order]) for f, v in inst.items()}
+        inst["arrival"] = np.zeros(len(order), np.int32)
+        inst["lower"] = inst["output"].copy()
+        inst["upper"] = np.maximum(inst["upper"], inst["output"])
+        ra = O.simulate(inst, O.AELL, b.M)
+        rh = O.simulate(inst, O.HSF, b.M)
+        assert ra["total_evictions"] == 0
+        assert same(ra, rh)
+
+
+@pytest.mark.parametrize("l,u,want", [(1, 3, "aell"), (2, 5, "amin"), (19, 50, "aell"), (191, 500, "amin"),
+                                      (1, 1, "amin"), (38, 100, "aell"), (382, 1000, "amin")])
+def test_adaptive_switch_threshold(l, u, want):
+    # Section 5.1: A_l when alpha = l/u < alpha* = (3 - sqrt 5)/2 = 0.381966...,
+    # A_min otherwise; 0.38 < alpha* < 0.382.  ADAPTIVE reproduces the choice.
+    rng = np.random.default_rng(l + u)
+    n = 30
+    o = rng.choice([l, u], n)
+    inst = {"prompt": np.ones(n, int), "output": o, "lower": np.full(n, l), "upper": np.full(n, u)}
+    assert O.adaptive_choice(inst) == O.ALGOS[want]
+    M = 4 * (1 + u)
+    assert same(O.simulate(inst, O.ADAPTIVE, M), O.simulate(inst, O.ALGOS[want], M))
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_aell_c_oracle_equals_literal_and_audit(seed):
+    # the C loop against the pure-Python loop with dense equation (2), and the
+    # event-log audit (memory before/after each step, promotions at exactly l
+    # tokens and only for o > l, once per request)
+    b = W.random_small(seed + 20, 60, 8, s_max=5, o_max=9, M=24, arrivals=(seed % 2 == 1), alpha=1.0)
+    n_prom = 0
+    for k in range(b.num_instances):
+        inst = b.instance(k)
+        for algo in (O.AELL, O.ADAPTIVE):
+            r = O.simulate(inst, algo, b.M, events=True)
+            assert same(r, O.literal_simulate(inst, algo, b.M))
+            O.audit(inst, algo, b.M, r)
+            n_prom += r["total_evictions"]
+    assert n_prom > 0
