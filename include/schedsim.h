@@ -1,6 +1,6 @@
 /*
  * schedsim.h -- C ABI of the MI355X (gfx950) simulator of the memory-constrained
- * LLM-inference schedulers A_max, A_min and H-SF (arXiv 2508.14544).
+ * LLM-inference schedulers A_max, A_min, H-SF and A_l (arXiv 2508.14544).
  *
  * Problem (Section 2): one worker with a KV cache of M tokens serves n
  * requests; request i has prompt size s_i, true output length o_i (revealed
@@ -19,10 +19,22 @@
  *               cancel runs in ascending (o~_i, i) until it fits and raise each
  *               cancelled request's o~_i to the tokens it had generated.
  *   SCHED_HSF   Algorithm 3 (hindsight shortest-first): plan with the true o_i.
+ *   SCHED_AELL  Algorithm 5, the promote-l policy A_l of Section 5.1: plan a
+ *               new run with l_i; a run that has generated l_i tokens without
+ *               finishing (so o_i > l_i) is cancelled, plans with u_i from then
+ *               on, and waits behind every fresh request (cancelled requests in
+ *               the order they were cancelled, same step by index); it may
+ *               restart in the step it was cancelled.
+ *   SCHED_ADAPTIVE  The switch of Section 5.1: per instance, SCHED_AELL when
+ *               (sum l_i)/(sum u_i) < (3 - sqrt 5)/2 (below this ratio the
+ *               competitive-ratio bound of Theorem 5.2 for A_l is the smaller
+ *               one; Theorem 5.1 bounds A_min), SCHED_AMIN otherwise.  The
+ *               comparison is exact: (3U - 2L)^2 > 5U^2.
  * Each step, waiting requests are tried in ascending (planning length, index)
- * order and the longest prefix that keeps equation (2) is started.  Ties break
- * by ascending request index.  Requests arriving at step a_i join the waiting
- * set at that step (the paper has every a_i = 0).
+ * order (A_l: the queue order above) and the longest prefix that keeps
+ * equation (2) is started.  Ties break by ascending request index.  Requests
+ * arriving at step a_i join the waiting set at that step (the paper has every
+ * a_i = 0).
  *
  * All pointers in sched_instances_t and sched_results_t are DEVICE pointers
  * (e.g. torch tensors on the GPU), allocated and owned by the caller; the
@@ -39,7 +51,13 @@
 extern "C" {
 #endif
 
-typedef enum { SCHED_AMAX = 0, SCHED_AMIN = 1, SCHED_HSF = 2 } sched_algo_t;
+typedef enum {
+  SCHED_AMAX = 0,
+  SCHED_AMIN = 1,
+  SCHED_HSF = 2,
+  SCHED_AELL = 3,
+  SCHED_ADAPTIVE = 4
+} sched_algo_t;
 
 /* Return codes of the calls (synchronous) and per-instance status values
  * (written to results.status, valid once the stream has reached the call). */
@@ -47,8 +65,10 @@ enum {
   SCHED_OK = 0,
   SCHED_E_INVAL = -1,       /* call: NULL/inconsistent arguments, M <= 0 or M >= 2^30.
                                status: offsets out of range or n_k > max_requests */
-  SCHED_E_INTERVAL = -2,    /* status: o < 1, s < 0, or (A_min) l < 1 or l > o, or (A_max) u < o */
-  SCHED_E_TOO_BIG = -3,     /* status: s + o > M, or (A_max) s + u > M: can never run           */
+  SCHED_E_INTERVAL = -2,    /* status: o < 1, s < 0, or l < 1 or l > o (A_min, A_l, adaptive),
+                               or u < o (A_max, A_l, adaptive)                                   */
+  SCHED_E_TOO_BIG = -3,     /* status: s + o > M, or s + u > M (A_max, and A_l also when the
+                               adaptive policy picks it): can never run                         */
   SCHED_E_STEP_CAP = -4,    /* status: unfinished requests when the step cap was passed        */
   SCHED_E_HIP = -5,         /* call: a HIP runtime call failed                                  */
   SCHED_E_UNSUPPORTED = -6, /* call: capacity request beyond what the kernels hold.
@@ -67,16 +87,18 @@ typedef struct {
   const int32_t* arrival;   /* [N] arrival step a_i, non-decreasing per instance; NULL = all 0 */
   const int32_t* prompt;    /* [N] prompt size s_i                                      */
   const int32_t* output;    /* [N] true output length o_i (the simulated world)         */
-  const int32_t* lower;     /* [N] l_i; required for SCHED_AMIN, unused otherwise       */
-  const int32_t* upper;     /* [N] u_i; required for SCHED_AMAX, unused otherwise       */
+  const int32_t* lower;     /* [N] l_i; required for SCHED_AMIN, SCHED_AELL, SCHED_ADAPTIVE */
+  const int32_t* upper;     /* [N] u_i; required for SCHED_AMAX, SCHED_AELL, SCHED_ADAPTIVE */
 } sched_instances_t;
 
 /* Outputs.  Per request: completion step C_i (-1 if it never completed) and
  * the number of times it was cancelled.  Per instance: total latency
  * sum(C_i - a_i) over completed requests (equation (3)), makespan max C_i,
  * request-steps (sum over steps of the number of running requests, wasted
- * work included), total cancellations and status.  Instances whose status is
- * not SCHED_OK and not SCHED_E_STEP_CAP report C_i = -1 and zero counters. */
+ * work included), total cancellations (A_l: promotions) and status, and the
+ * policy the instance was simulated with (the requested one, or SCHED_AMIN /
+ * SCHED_AELL under SCHED_ADAPTIVE).  Instances whose status is not SCHED_OK
+ * and not SCHED_E_STEP_CAP report C_i = -1 and zero counters. */
 typedef struct {
   int32_t* completion;      /* [N] required     */
   int32_t* evictions;       /* [N] or NULL      */
@@ -85,6 +107,7 @@ typedef struct {
   int64_t* request_steps;   /* [K] or NULL      */
   int64_t* total_evictions; /* [K] or NULL      */
   int32_t* status;          /* [K] required     */
+  int32_t* algo_used;       /* [K] or NULL      */
 } sched_results_t;
 
 typedef struct {
@@ -92,7 +115,7 @@ typedef struct {
                                min(2^30, 4*(max a + sum(o+1)) + 64)                       */
   int32_t running_capacity; /* max concurrently running requests per instance, <= 1024;
                                0: min(max_requests rounded up to 64, 1024)                */
-  int32_t evicted_capacity; /* max cancelled requests waiting at once (A_min); 0: default */
+  int32_t evicted_capacity; /* max cancelled requests waiting at once (A_min, A_l); 0: default */
   void* event_before;       /* hipEvent_t recorded just before the simulation kernel, or NULL */
   void* event_after;        /* hipEvent_t recorded just after it, or NULL                  */
 } sched_options_t;

@@ -15,8 +15,8 @@ from typing import Dict, Optional
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libschedsim.so")
 
-AMAX, AMIN, HSF = 0, 1, 2
-ALGOS = {"amax": AMAX, "amin": AMIN, "hsf": HSF}
+AMAX, AMIN, HSF, AELL, ADAPTIVE = 0, 1, 2, 3, 4
+ALGOS = {"amax": AMAX, "amin": AMIN, "hsf": HSF, "aell": AELL, "adaptive": ADAPTIVE}
 OK, E_INVAL, E_INTERVAL, E_TOO_BIG, E_STEP_CAP, E_HIP, E_UNSUPPORTED, E_ARRIVAL = 0, -1, -2, -3, -4, -5, -6, -7
 
 # every symbol include/schedsim.h declares
@@ -46,6 +46,7 @@ class SchedResults(ctypes.Structure):
         ("request_steps", ctypes.c_void_p),
         ("total_evictions", ctypes.c_void_p),
         ("status", ctypes.c_void_p),
+        ("algo_used", ctypes.c_void_p),
     ]
 
 
@@ -143,6 +144,7 @@ def alloc_results(db: DeviceBatch, evictions: bool = True):
         "request_steps": torch.empty(K, dtype=torch.int64, device=dev),
         "total_evictions": torch.empty(K, dtype=torch.int64, device=dev),
         "status": torch.empty(K, dtype=torch.int32, device=dev),
+        "algo_used": torch.empty(K, dtype=torch.int32, device=dev),
     }
 
 
@@ -159,7 +161,7 @@ def simulate_into(db: DeviceBatch, algo: int, out: Dict[str, object], *, M: Opti
                           _ptr(db.upper) if pass_upper else None)
     res = SchedResults(_ptr(out["completion"]), _ptr(out.get("evictions")), _ptr(out["tel"]),
                        _ptr(out.get("makespan")), _ptr(out.get("request_steps")), _ptr(out.get("total_evictions")),
-                       _ptr(out["status"]))
+                       _ptr(out["status"]), _ptr(out.get("algo_used")))
     opts = SchedOptions(int(step_cap), int(running_capacity), int(evicted_capacity),
                         None if event_before is None else int(event_before.cuda_event),
                         None if event_after is None else int(event_after.cuda_event))

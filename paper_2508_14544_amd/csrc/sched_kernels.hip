@@ -64,6 +64,7 @@ struct Params {
   int64_t* request_steps;
   int64_t* total_evictions;
   int32_t* status;
+  int32_t* algo_used;    // optional output: the policy each instance ran
   int32_t M;
   int64_t step_cap;      // > 0: user cap for every instance
   // workspace
@@ -72,6 +73,7 @@ struct Params {
   uint2* rec;
   int32_t* rank_of;
   int32_t* cap;
+  int32_t* algo_of;      // adaptive runs: the policy each instance runs (else NULL)
   // LDS layout of k_simulate
   int32_t nw_max;        // 64-bit words of the level-0 bitmap
   int32_t nw1_max;       // 64-bit words of the level-1 bitmap
@@ -93,8 +95,13 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
   if (b < 0 || e < b || e > P.N || e - b > P.max_requests) status = SCHED_E_INVAL;
   const int n = (status == SCHED_OK) ? static_cast<int>(e - b) : 0;
 
+  // l is read by A_min and A_l, u by A_max and A_l; the adaptive policy reads
+  // both (their sums pick the policy) and validates with the one it picks
+  constexpr bool kReadL = ALGO == SCHED_AMIN || ALGO == SCHED_AELL || ALGO == SCHED_ADAPTIVE;
+  constexpr bool kReadU = ALGO == SCHED_AMAX || ALGO == SCHED_AELL || ALGO == SCHED_ADAPTIVE;
   bool arr_bad = false, int_bad = false, big_bad = false, unsup = (n >= (1 << kIdxBits));
-  int64_t max_a = 0, sum_o = 0;
+  bool bad_l = false, unsup_l = false, bad_u = false, big_u = false, unsup_u = false;
+  int64_t max_a = 0, sum_o = 0, sum_l = 0, sum_u = 0;
   int32_t prev_last = 0;
   for (int c = 0; c < n; c += 64) {
     const int i = c + lane;
@@ -104,8 +111,8 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
       a = P.arrival ? P.arrival[b + i] : 0;
       s = P.prompt[b + i];
       o = P.output[b + i];
-      if (ALGO == SCHED_AMIN) lo = P.lower[b + i];
-      if (ALGO == SCHED_AMAX) up = P.upper[b + i];
+      if (kReadL) lo = P.lower[b + i];
+      if (kReadU) up = P.upper[b + i];
     }
     int32_t ap = __shfl_up(a, 1, 64);
     if (lane == 0) ap = prev_last;
@@ -113,15 +120,37 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
     if (act) {
       if (a < 0 || (i > 0 && a < ap)) arr_bad = true;
       if (o < 1 || s < 0) int_bad = true;
-      if (ALGO == SCHED_AMIN && (lo < 1 || lo > o)) int_bad = true;
-      if (ALGO == SCHED_AMAX && up < o) int_bad = true;
+      if (lo < 1 || lo > o) bad_l = true;
+      if (up < o) bad_u = true;
       if (static_cast<int64_t>(s) + o > P.M) big_bad = true;
-      if (ALGO == SCHED_AMAX && static_cast<int64_t>(s) + up > P.M) big_bad = true;
-      if (o >= kEstLimit || s >= kPromptLimit || (ALGO == SCHED_AMAX && up >= kEstLimit)) unsup = true;
+      if (static_cast<int64_t>(s) + up > P.M) big_u = true;
+      if (o >= kEstLimit || s >= kPromptLimit) unsup = true;
+      if (lo >= kEstLimit) unsup_l = true;
+      if (up >= kEstLimit) unsup_u = true;
       max_a = a > max_a ? a : max_a;
       sum_o += static_cast<int64_t>(o) + 1;
+      sum_l += lo;
+      sum_u += up;
     }
   }
+  // the policy this instance runs; the adaptive one takes A_l when
+  // L/U < (3 - sqrt 5)/2, i.e. sqrt(5) U < 3U - 2L, i.e. 5U^2 < (3U - 2L)^2
+  int algo = ALGO;
+  if (ALGO == SCHED_ADAPTIVE) {
+    const int64_t L = wave::sum_i64(sum_l), U = wave::sum_i64(sum_u);
+    const int64_t d = 3 * U - 2 * L;
+    algo = SCHED_AMIN;
+    if (n > 0 && d > 0) {
+      const unsigned __int128 dd = static_cast<unsigned __int128>(d) * static_cast<unsigned __int128>(d);
+      const unsigned __int128 uu = static_cast<unsigned __int128>(U) * static_cast<unsigned __int128>(U);
+      if (dd > 5 * uu) algo = SCHED_AELL;
+    }
+  }
+  const bool use_l = algo == SCHED_AMIN || algo == SCHED_AELL;
+  const bool use_u = algo == SCHED_AMAX || algo == SCHED_AELL;
+  int_bad = int_bad || (use_l && bad_l) || (use_u && bad_u);
+  big_bad = big_bad || (use_u && big_u);
+  unsup = unsup || (use_l && unsup_l) || (use_u && unsup_u);
   if (status == SCHED_OK) {
     if (wave::ballot(arr_bad)) status = SCHED_E_ARRIVAL;
     else if (wave::ballot(int_bad)) status = SCHED_E_INTERVAL;
@@ -144,20 +173,23 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
   if (lane == 0) {
     P.status[k] = status;
     P.cap[k] = static_cast<int32_t>(cap);
+    if (P.algo_of) P.algo_of[k] = algo;
+    if (P.algo_used) P.algo_used[k] = algo;
   }
   if (status != SCHED_OK || n == 0) return;
 
-  // ---- keys (est0 << 17 | index), est0 = u (A_max), l (A_min), o (H-SF)
+  // ---- keys (est0 << 17 | index), est0 = u (A_max), l (A_min, A_l), o (H-SF)
   for (int c = 0; c < n; c += 64) {
     const int i = c + lane;
     if (i < n) {
-      int32_t est = (ALGO == SCHED_AMAX) ? P.upper[b + i] : (ALGO == SCHED_AMIN) ? P.lower[b + i] : P.output[b + i];
+      int32_t est = (algo == SCHED_AMAX) ? P.upper[b + i] : (algo == SCHED_HSF) ? P.output[b + i] : P.lower[b + i];
       P.sort_a[b + i] = (static_cast<uint32_t>(est) << kIdxBits) | static_cast<uint32_t>(i);
     }
   }
-  // ---- stable LSD radix sort on bits 17..24 then 25..31
+  // ---- stable LSD radix sort on bits 17..24 then 25..31 (A_l's queue is in
+  // index order: its ranks are the indices, no sort)
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int pass = 0; pass < 2; ++pass) {
+  for (int pass = 0; pass < (algo == SCHED_AELL ? 0 : 2); ++pass) {
     const uint32_t* src = pass == 0 ? P.sort_a : P.sort_b;
     uint32_t* dst = pass == 0 ? P.sort_b : P.sort_a;
     const int shift = kIdxBits + 8 * pass;
@@ -240,6 +272,7 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
   extern __shared__ uint64_t lds64[];
   const int k = blockIdx.x;
   const int lane = threadIdx.x;
+  if (P.algo_of && P.algo_of[k] != ALGO) return;  // adaptive run: the other policy's instance
   int st0 = P.status[k];
   if (RETRY_PASS) {
     if (st0 != kRetry) return;
@@ -255,8 +288,9 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
   if (st0 == SCHED_OK && n > 0) {
     uint64_t* L0 = lds64;
     uint64_t* L1 = lds64 + P.nw_max;
-    // cancelled requests, one 64-bit entry each: key | (s | o << 16) << 32;
-    // slots [0, nVe) may start now, [nVe, nV) were cancelled at this step
+    // cancelled requests, one 64-bit entry each.  A_min: key | (s | o << 16) << 32,
+    // slots [0, nVe) may start now, [nVe, nV) were cancelled at this step.
+    // A_l: a FIFO ring of index | s << 17 | o << 33 | u << 48 from slot v_head.
     uint64_t* vent = L1 + P.nw1_max;
     const int nw = (n + 63) >> 6;
     const int nw1 = (nw + 63) >> 6;
@@ -268,16 +302,18 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
     const uint2* rec = P.rec + b;
     const int32_t* arrival = P.arrival ? P.arrival + b : nullptr;
     const int32_t* rank_of = P.rank_of + b;
+    const int32_t* upper_k = ALGO == SCHED_AELL ? P.upper + b : nullptr;
     int32_t* completion = P.completion + b;
     int32_t* evictions = P.evictions ? P.evictions + b : nullptr;
 
     // running set: register rows; an empty slot has r_end = kEmpty, r_c = kNever,
     // r_key = ~0, which every scan below treats as neutral, so scans cover all rows
-    int32_t r_end[ROWS], r_x[ROWS], r_c[ROWS], r_h[ROWS];
+    // (A_l also keeps each run's u, its planning length after a promotion)
+    int32_t r_end[ROWS], r_x[ROWS], r_c[ROWS], r_h[ROWS], r_u[ROWS];
     uint32_t r_key[ROWS];
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) {
-      r_end[r] = kEmpty; r_x[r] = 0; r_c[r] = kNever; r_h[r] = 0; r_key[r] = 0xFFFFFFFFu;
+      r_end[r] = kEmpty; r_x[r] = 0; r_c[r] = kNever; r_h[r] = 0; r_key[r] = 0xFFFFFFFFu; r_u[r] = 0;
     }
     int fr_row = 0;               // row that receives new runs ...
     uint64_t fr_mask = ~0ull;     // ... and its free lanes
@@ -290,13 +326,15 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
     int32_t next_a = 0;           // arrival step of request arr_ptr (0: look at step 0)
     int32_t f_rank = -1, fw_base = -1;
     uint32_t f_key = 0xFFFFFFFFu, f_so = 0, fw_key = 0xFFFFFFFFu, fw_so = 0;
-    int32_t nV = 0, nVe = 0, v_pos = -1;
+    int32_t f_u = 0, fw_u = 0;
+    int32_t nV = 0, nVe = 0, v_pos = -1, v_head = 0;
     uint32_t v_key = 0xFFFFFFFFu, v_so = 0;
+    int32_t v_u = 0;
     int32_t n_done = 0;
     // cached head of the waiting set (smaller key of the two heads)
     bool c_any = false, c_fromF = false;
     uint32_t c_key = 0;
-    int32_t c_est = 0, c_s = 0, c_o = 0;
+    int32_t c_est = 0, c_s = 0, c_o = 0, c_u = 0;
     // the head cannot start before retry_at; valid until the next event
     int32_t retry_at = 0;
 
@@ -334,10 +372,12 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
           const uint2 rv_ = rec[rr_];                                                \
           fw_key = rv_.x;                                                            \
           fw_so = rv_.y;                                                             \
+          if (ALGO == SCHED_AELL) fw_u = upper_k[rr_];                               \
         }                                                                            \
       }                                                                              \
       f_key = wave::readlane_u(fw_key, f_rank - fw_base);                            \
       f_so = wave::readlane_u(fw_so, f_rank - fw_base);                              \
+      if (ALGO == SCHED_AELL) f_u = wave::readlane(fw_u, f_rank - fw_base);          \
     }                                                                                \
   } while (0)
     // per-lane smallest cancelled entry over slots [FROM_, TO_): vb_k, vb_p, vb_s
@@ -379,16 +419,34 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
     }                                                                                \
     nVe = nV;                                                                        \
   } while (0)
+    // A_l: the oldest promoted request (head of the ring), planned with u
+#define SK_V_HEAD()                                                                  \
+  do {                                                                               \
+    v_pos = -1;                                                                      \
+    v_key = 0xFFFFFFFFu;                                                             \
+    if (nV > 0) {                                                                    \
+      const uint64_t e_ = uniform_u64(vent[v_head]);                                 \
+      const uint32_t ix_ = static_cast<uint32_t>(e_) & kIdxMask;                     \
+      const uint32_t s_ = static_cast<uint32_t>(e_ >> 17) & 0xFFFFu;                 \
+      const uint32_t o_ = static_cast<uint32_t>(e_ >> 33) & 0x7FFFu;                 \
+      v_u = static_cast<int32_t>((e_ >> 48) & 0x7FFFu);                              \
+      v_pos = v_head;                                                                \
+      v_key = (static_cast<uint32_t>(v_u) << kIdxBits) | ix_;                        \
+      v_so = s_ | (o_ << 16);                                                        \
+    }                                                                                \
+  } while (0)
     // the head of the waiting set: smaller key of the fresh and cancelled heads
+    // (A_l: every fresh request comes before the promoted ones)
 #define SK_PICK()                                                                    \
   do {                                                                               \
     c_any = f_rank >= 0 || v_pos >= 0;                                               \
-    c_fromF = f_rank >= 0 && f_key < v_key;                                          \
+    c_fromF = f_rank >= 0 && (ALGO == SCHED_AELL || f_key < v_key);                  \
     c_key = c_fromF ? f_key : v_key;                                                 \
     const uint32_t so_ = c_fromF ? f_so : v_so;                                      \
     c_est = static_cast<int32_t>(c_key >> kIdxBits);                                 \
     c_s = static_cast<int32_t>(so_ & 0xFFFFu);                                       \
     c_o = static_cast<int32_t>(so_ >> 16);                                           \
+    c_u = c_fromF ? f_u : v_u;                                                       \
   } while (0)
     // BODY with the compile-time row index r equal to the uniform row RR_
 #define SK_AT_ROW(RR_, BODY)                                                         \
@@ -475,7 +533,7 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
           const uint64_t m = wave::ballot(hit);
           if (m) {
             ndone += __builtin_popcountll(m);
-            if (ALGO == SCHED_AMAX) {
+            if (ALGO == SCHED_AMAX || ALGO == SCHED_AELL) {
               // planned with u >= o: the run may end before its planned end
               uint64_t mm = m;
               while (mm) {
@@ -492,9 +550,6 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
             if (r == fr_row) fr_mask |= m;
           }
         }
-        int32_t cmin = r_c[0];
-#pragma unroll
-        for (int r = 1; r < ROWS; ++r) cmin = r_c[r] < cmin ? r_c[r] : cmin;
         if (ndone) {
           event = true;
           const int32_t sxw = wave::sum_i32(sx);
@@ -503,9 +558,77 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
           DT = sxw + ndone * (t - t_r);
           n_done += ndone;
         }
-        next_c = static_cast<int32_t>(wave::min_u32(static_cast<uint32_t>(cmin)));  // all >= 0
         // ---- 3. done?
         if (n_done == n) break;
+        // ---- 3'. A_l: a run still present at its planned end t (planned with
+        // l, so o > l) is promoted: it leaves, plans with u and joins the back of
+        // the queue, lowest index first among this step's promotions
+        if (ALGO == SCHED_AELL) {
+          bool promoted = false;
+          for (;;) {
+            uint32_t best = 0xFFFFFFFFu;
+            int32_t brow = 0;
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+              const uint32_t kk = r_end[r] == t ? (r_key[r] & kIdxMask) : 0xFFFFFFFFu;
+              const bool lt = kk < best;
+              best = lt ? kk : best;
+              brow = lt ? r : brow;
+            }
+            const uint32_t imin = wave::min_u32(best);
+            if (imin == 0xFFFFFFFFu) break;
+            if (nV >= P.cap_v) {
+              status = SCHED_E_UNSUPPORTED;
+              break;
+            }
+            const int ln = __builtin_ctzll(wave::ballot(best == imin));
+            const int rr = wave::readlane(brow, ln);
+            int32_t xk = 0, ck = 0, uk = 0;
+            uint32_t kk = 0;
+            SK_AT_ROW(rr, xk = wave::readlane(r_x[r], ln); ck = wave::readlane(r_c[r], ln);
+                      uk = wave::readlane(r_u[r], ln); kk = wave::readlane_u(r_key[r], ln);
+                      r_end[r] = wave::writelane(r_end[r], kEmpty, ln);
+                      r_c[r] = wave::writelane(r_c[r], kNever, ln);
+                      r_key[r] = wave::writelane_u(r_key[r], 0xFFFFFFFFu, ln);)
+            if (rr == fr_row) fr_mask |= 1ull << ln;
+            // its planned end is t itself: no later planned end loses a share
+            X -= xk;
+            N -= 1;
+            const int32_t pk = t - static_cast<int32_t>(kk >> kIdxBits);
+            const uint64_t sk = static_cast<uint32_t>(xk - t_r + pk);
+            const uint64_t okk = static_cast<uint32_t>(ck - pk);
+            if (lane == 0) {
+              int slot = v_head + nV;
+              slot = slot >= P.cap_v ? slot - P.cap_v : slot;
+              vent[slot] = imin | (sk << 17) | (okk << 33) | (static_cast<uint64_t>(uk) << 48);
+              if (evictions) atomicAdd(&evictions[imin], 1);
+            }
+            ++nV;
+            ++tot_ev;
+            promoted = true;
+          }
+          if (status != SCHED_OK) break;
+          if (promoted) {
+            event = true;
+            if (v_pos < 0) {
+              SK_V_HEAD();
+              SK_PICK();
+            }
+          }
+        }
+        // next event: a completion (A_l: or a planned end, where a run is promoted);
+        // empty slots read as unsigned are above every step
+        uint32_t cmin = 0xFFFFFFFFu;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+          uint32_t ev = static_cast<uint32_t>(r_c[r]);
+          if (ALGO == SCHED_AELL) {
+            const uint32_t pe = static_cast<uint32_t>(r_end[r]);
+            ev = pe < ev ? pe : ev;
+          }
+          cmin = ev < cmin ? ev : cmin;
+        }
+        next_c = static_cast<int32_t>(wave::min_u32(cmin));  // kNever when nothing runs
       }
 
       // ---- 4. A_min: cancel in ascending (o~, index) while memory at t+1 > M
@@ -652,10 +775,13 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
           fr_mask &= fr_mask - 1;
           const int32_t cw = t + c_o;
           const uint32_t kw = c_key;
+          const int32_t uw = c_u;
           SK_AT_ROW(fr_row, r_end[r] = wave::writelane(r_end[r], E, ln); r_x[r] = wave::writelane(r_x[r], xw, ln);
                     r_c[r] = wave::writelane(r_c[r], cw, ln); r_key[r] = wave::writelane_u(r_key[r], kw, ln);
-                    r_h[r] = wave::writelane(r_h[r], hw, ln);)
-          next_c = cw < next_c ? cw : next_c;
+                    r_h[r] = wave::writelane(r_h[r], hw, ln);
+                    if (ALGO == SCHED_AELL) r_u[r] = wave::writelane(r_u[r], uw, ln);)
+          const int32_t ew = ALGO == SCHED_AELL && E < cw ? E : cw;  // A_l: promotion at E
+          next_c = ew < next_c ? ew : next_c;
         }
         X += xw;
         N += 1;
@@ -667,6 +793,10 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
             if (w == 0ull) L1[j0 >> 6] &= ~(1ull << (j0 & 63));
           }
           SK_F_FIND();
+        } else if (ALGO == SCHED_AELL) {
+          v_head = v_head + 1 == P.cap_v ? 0 : v_head + 1;
+          --nV;
+          SK_V_HEAD();
         } else {
           // the last eligible entry moves into the hole; the last pending one fills its place
           if (lane == 0) {
@@ -688,7 +818,7 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
       // ---- 6. this step processes every running request once
       rsteps += N;
       int32_t tn = t + 1;
-      if (nV == nVe) {
+      if (ALGO != SCHED_AMIN || nV == nVe) {
         // Nothing changes before the next completion, arrival or (A_min)
         // overflow; until then the head cannot start before wait_until (or at
         // all when stuck: the memory at t+1 only grows).
@@ -760,6 +890,7 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
 #undef SK_V_FIND
 #undef SK_V_SCAN
 #undef SK_V_MERGE
+#undef SK_V_HEAD
 #undef SK_AT_ROW
 #undef SK_DROP_SHARE
 
@@ -806,13 +937,31 @@ hipError_t set_lds_limit(int rows, bool retry, int bytes) {
   return hipFuncSetAttribute(sim_kernel<ALGO>(rows, retry), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
 }
 
+hipError_t set_lds_limit_any(int algo, int rows, bool retry, int bytes) {
+  switch (algo) {
+    case SCHED_AMAX: return set_lds_limit<SCHED_AMAX>(rows, retry, bytes);
+    case SCHED_AMIN: return set_lds_limit<SCHED_AMIN>(rows, retry, bytes);
+    case SCHED_HSF: return set_lds_limit<SCHED_HSF>(rows, retry, bytes);
+    default: return set_lds_limit<SCHED_AELL>(rows, retry, bytes);
+  }
+}
+
+hipError_t launch_sim_any(int algo, int rows, bool retry, const sk::Params& P, size_t lds, hipStream_t st) {
+  switch (algo) {
+    case SCHED_AMAX: return launch_sim<SCHED_AMAX>(rows, retry, P, lds, st);
+    case SCHED_AMIN: return launch_sim<SCHED_AMIN>(rows, retry, P, lds, st);
+    case SCHED_HSF: return launch_sim<SCHED_HSF>(rows, retry, P, lds, st);
+    default: return launch_sim<SCHED_AELL>(rows, retry, P, lds, st);
+  }
+}
+
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 }  // namespace
 
 extern "C" {
 
-int sched_version(void) { return 100; }
+int sched_version(void) { return 110; }
 
 const char* sched_strerror(int code) {
   switch (code) {
@@ -831,14 +980,16 @@ const char* sched_strerror(int code) {
 int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t M,
                         const sched_results_t* out, void* stream, const sched_options_t* opts) {
   if (!in || !out) return SCHED_E_INVAL;
-  if (algo != SCHED_AMAX && algo != SCHED_AMIN && algo != SCHED_HSF) return SCHED_E_INVAL;
+  if (algo < SCHED_AMAX || algo > SCHED_ADAPTIVE) return SCHED_E_INVAL;
+  const bool need_l = algo == SCHED_AMIN || algo == SCHED_AELL || algo == SCHED_ADAPTIVE;
+  const bool need_u = algo == SCHED_AMAX || algo == SCHED_AELL || algo == SCHED_ADAPTIVE;
   if (M <= 0 || M >= (int64_t(1) << 30)) return SCHED_E_INVAL;
   if (in->num_instances < 0 || in->max_requests < 0 || in->total_requests < 0) return SCHED_E_INVAL;
   if (in->num_instances == 0) return SCHED_OK;
   if (!in->offsets || !out->total_latency || !out->status) return SCHED_E_INVAL;
   if (in->total_requests > 0 && (!in->prompt || !in->output || !out->completion)) return SCHED_E_INVAL;
-  if (in->total_requests > 0 && algo == SCHED_AMIN && !in->lower) return SCHED_E_INVAL;
-  if (in->total_requests > 0 && algo == SCHED_AMAX && !in->upper) return SCHED_E_INVAL;
+  if (in->total_requests > 0 && need_l && !in->lower) return SCHED_E_INVAL;
+  if (in->total_requests > 0 && need_u && !in->upper) return SCHED_E_INVAL;
   if (in->max_requests >= (1 << sk::kIdxBits)) return SCHED_E_UNSUPPORTED;
   sched_options_t o{};
   if (opts) o = *opts;
@@ -846,8 +997,6 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   if (o.running_capacity < 0 || o.evicted_capacity < 0) return SCHED_E_INVAL;
 
   const int64_t nmax = in->max_requests;
-  // Register rows of the running set.  By default a first pass holds up to 512
-  // runs and a second pass with 1024 re-runs only the instances that outgrew it.
   if (o.running_capacity > 1024) return SCHED_E_UNSUPPORTED;
   const bool forced = o.running_capacity > 0;
   // passes: the first covers up to 384 runs (every run of most instances);
@@ -871,13 +1020,30 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
 
   const int nw = static_cast<int>((nmax + 63) / 64);
   const int nw1 = (nw + 63) / 64;
-  int cap_v = 0;
-  if (algo == SCHED_AMIN) {
-    const int64_t def = in->num_instances <= 64 ? 16384 : 1024;
-    cap_v = o.evicted_capacity > 0 ? o.evicted_capacity : static_cast<int>(std::min<int64_t>(std::max<int64_t>(nmax, 1), def));
-  }
-  const size_t lds = 8 * static_cast<size_t>(nw + nw1) + 8 * static_cast<size_t>(cap_v);
-  if (lds > static_cast<size_t>(lds_max)) return SCHED_E_UNSUPPORTED;
+  // evicted-set slots (8 bytes of LDS each).  A_min scans its set per admission,
+  // so it is kept small where many instances share a CU; A_l's is a FIFO in
+  // which every request appears at most once, so n slots never overflow
+  const size_t lds_bitmaps = 8 * static_cast<size_t>(nw + nw1);
+  auto cap_v_for = [&](int a) -> int {
+    if (o.evicted_capacity > 0 && (a == SCHED_AMIN || a == SCHED_AELL)) return o.evicted_capacity;
+    if (a == SCHED_AMIN) {
+      const int64_t def = in->num_instances <= 64 ? 16384 : 1024;
+      return static_cast<int>(std::min<int64_t>(std::max<int64_t>(nmax, 1), def));
+    }
+    if (a == SCHED_AELL) {
+      const int64_t fit = lds_bitmaps < static_cast<size_t>(lds_max)
+                              ? static_cast<int64_t>((static_cast<size_t>(lds_max) - lds_bitmaps) / 8) : 0;
+      return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(std::max<int64_t>(nmax, 1), fit)));
+    }
+    return 0;
+  };
+  auto lds_for = [&](int a) -> size_t { return lds_bitmaps + 8 * static_cast<size_t>(cap_v_for(a)); };
+  // the adaptive policy runs the A_min passes and then the A_l passes; each
+  // kernel skips the instances that k_prepare assigned to the other policy
+  const int sim_algos[2] = {algo == SCHED_ADAPTIVE ? SCHED_AMIN : static_cast<int>(algo), SCHED_AELL};
+  const int n_sim = algo == SCHED_ADAPTIVE ? 2 : 1;
+  for (int a = 0; a < n_sim; ++a)
+    if (lds_for(sim_algos[a]) > static_cast<size_t>(lds_max)) return SCHED_E_UNSUPPORTED;
 
   const size_t N = static_cast<size_t>(in->total_requests);
   const size_t K = static_cast<size_t>(in->num_instances);
@@ -887,6 +1053,7 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   const size_t o_rec = off; off = align_up(off + 8 * N, 256);
   const size_t o_rk = off; off = align_up(off + 4 * N, 256);
   const size_t o_cap = off; off = align_up(off + 4 * K, 256);
+  const size_t o_alg = off; off = align_up(off + (algo == SCHED_ADAPTIVE ? 4 * K : 0), 256);
   void* ws = nullptr;
   if (hipMallocAsync(&ws, off, st) != hipSuccess) return SCHED_E_HIP;
   char* base = static_cast<char*>(ws);
@@ -915,34 +1082,33 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   P.rec = reinterpret_cast<uint2*>(base + o_rec);
   P.rank_of = reinterpret_cast<int32_t*>(base + o_rk);
   P.cap = reinterpret_cast<int32_t*>(base + o_cap);
+  P.algo_of = algo == SCHED_ADAPTIVE ? reinterpret_cast<int32_t*>(base + o_alg) : nullptr;
+  P.algo_used = out->algo_used;
   P.nw_max = nw;
   P.nw1_max = nw1;
-  P.cap_v = cap_v;
 
   hipError_t err = hipSuccess;
   const dim3 grid(P.K), block(64);
   switch (algo) {
     case SCHED_AMAX: hipLaunchKernelGGL((sk::k_prepare<SCHED_AMAX>), grid, block, 0, st, P); break;
     case SCHED_AMIN: hipLaunchKernelGGL((sk::k_prepare<SCHED_AMIN>), grid, block, 0, st, P); break;
-    default: hipLaunchKernelGGL((sk::k_prepare<SCHED_HSF>), grid, block, 0, st, P); break;
+    case SCHED_HSF: hipLaunchKernelGGL((sk::k_prepare<SCHED_HSF>), grid, block, 0, st, P); break;
+    case SCHED_AELL: hipLaunchKernelGGL((sk::k_prepare<SCHED_AELL>), grid, block, 0, st, P); break;
+    default: hipLaunchKernelGGL((sk::k_prepare<SCHED_ADAPTIVE>), grid, block, 0, st, P); break;
   }
   err = hipGetLastError();
-  for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass) {
-    if (lds > 65536) {
-      switch (algo) {
-        case SCHED_AMAX: err = set_lds_limit<SCHED_AMAX>(tiers[pass], pass > 0, static_cast<int>(lds)); break;
-        case SCHED_AMIN: err = set_lds_limit<SCHED_AMIN>(tiers[pass], pass > 0, static_cast<int>(lds)); break;
-        default: err = set_lds_limit<SCHED_HSF>(tiers[pass], pass > 0, static_cast<int>(lds)); break;
-      }
-    }
+  for (int a = 0; a < n_sim && err == hipSuccess; ++a) {
+    const size_t lds = lds_for(sim_algos[a]);
+    for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass)
+      if (lds > 65536) err = set_lds_limit_any(sim_algos[a], tiers[pass], pass > 0, static_cast<int>(lds));
   }
   if (err == hipSuccess && o.event_before) err = hipEventRecord(static_cast<hipEvent_t>(o.event_before), st);
-  for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass) {
-    P.retry_status = pass + 1 < n_tiers ? sk::kRetry : SCHED_E_UNSUPPORTED;
-    switch (algo) {
-      case SCHED_AMAX: err = launch_sim<SCHED_AMAX>(tiers[pass], pass > 0, P, lds, st); break;
-      case SCHED_AMIN: err = launch_sim<SCHED_AMIN>(tiers[pass], pass > 0, P, lds, st); break;
-      default: err = launch_sim<SCHED_HSF>(tiers[pass], pass > 0, P, lds, st); break;
+  for (int a = 0; a < n_sim && err == hipSuccess; ++a) {
+    P.cap_v = cap_v_for(sim_algos[a]);
+    const size_t lds = lds_for(sim_algos[a]);
+    for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass) {
+      P.retry_status = pass + 1 < n_tiers ? sk::kRetry : SCHED_E_UNSUPPORTED;
+      err = launch_sim_any(sim_algos[a], tiers[pass], pass > 0, P, lds, st);
     }
   }
   if (err == hipSuccess && o.event_after) err = hipEventRecord(static_cast<hipEvent_t>(o.event_after), st);

@@ -183,6 +183,10 @@ WORKLOADS: Dict[str, Workload] = {
         Workload("sweep65536_n2000_m32768", 5, 65536, 2000, 32768,
                  "65536 instances, n=2000 at t=0; s~U{1..128}; o: 70% U{1..64}, 30% U{512..1024}; geometric "
                  "bins alpha in {0,0.25,...,2.0} (8 blocks of 7281, last 7288); M=32768"),
+        Workload("twopoint4096_n1000_m16384", 6, 4096, 1000, 16384,
+                 "4096 instances, n=1000 at t=0; two-point outputs (Section 5.1): per instance l_k~U{2..64}, "
+                 "u_k=ceil(l_k/alpha_k), alpha_k in {1/10,1/5,3/10,2/5,1/2,3/5} (6 blocks of 682, last 686); "
+                 "o=u_k with probability 1/2, else l_k; interval [l_k,u_k]; s~U{1..64}; M=16384"),
     ]
 }
 
@@ -197,6 +201,7 @@ def _alpha_blocks(num_instances: int, alphas: Sequence[Fraction]) -> np.ndarray:
 _ALPHAS = {
     2: [Fraction(1, 10), Fraction(1, 2), Fraction(1, 1)],
     5: [Fraction(k, 4) for k in range(9)],
+    6: [Fraction(1, 10), Fraction(1, 5), Fraction(3, 10), Fraction(2, 5), Fraction(1, 2), Fraction(3, 5)],
 }
 
 
@@ -264,6 +269,19 @@ def generate(name: str, seed: int = 0, instance_ids: Optional[Sequence[int]] = N
             if m.any():
                 l[m], u[m] = _bins_for(al, o[m], 1024)
         meta["alpha"] = [str(_ALPHAS[5][i]) for i in aidx]
+    elif wid == 6:
+        arr = np.zeros((K, n), np.int64)
+        s = uniform_int(R(F_PROMPT), 1, 64)
+        lk = uniform_int(raw64(seed, wid, F_U1, ids, 1), 2, 64)[:, 0]
+        aidx = _alpha_blocks(w.num_instances, _ALPHAS[6])[ids]
+        num = np.array([_ALPHAS[6][i].numerator for i in aidx], np.int64)
+        den = np.array([_ALPHAS[6][i].denominator for i in aidx], np.int64)
+        uk = (lk * den + num - 1) // num          # ceil(l / alpha), exact
+        long_ = uniform01(R(F_MIX)) < 0.5
+        o = np.where(long_, uk[:, None], lk[:, None]).astype(np.int64)
+        l = np.repeat(lk[:, None], n, axis=1)
+        u = np.repeat(uk[:, None], n, axis=1)
+        meta["alpha"] = [str(_ALPHAS[6][i]) for i in aidx]
     else:  # pragma: no cover
         raise ValueError(name)
 

@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strerror(lib):
-    assert lib.sched_version() == 100
+    assert lib.sched_version() == 110
     for code in (0, -1, -2, -3, -4, -5, -6, -7):
         assert B.strerror(code) and B.strerror(code) != "unknown code"
     assert B.strerror(12345) == "unknown code"
@@ -45,7 +45,7 @@ def _inst(K=1, nmax=4, N=4, offsets=1, prompt=1, output=1, lower=1, upper=1):
 
 def _res(**kw):
     d = dict(completion=0x1000, evictions=None, total_latency=0x1000, makespan=None, request_steps=None,
-             total_evictions=None, status=0x1000)
+             total_evictions=None, status=0x1000, algo_used=None)
     d.update(kw)
     return B.SchedResults(*[d[k] for k, _ in B.SchedResults._fields_])
 
@@ -68,6 +68,11 @@ def test_host_validation(lib):
     assert call(lib, _inst(output=None)) == B.E_INVAL
     assert call(lib, _inst(lower=None), algo=B.AMIN) == B.E_INVAL
     assert call(lib, _inst(upper=None), algo=B.AMAX) == B.E_INVAL
+    for algo in (B.AELL, B.ADAPTIVE):  # both bounds are needed
+        assert call(lib, _inst(lower=None), algo=algo) == B.E_INVAL
+        assert call(lib, _inst(upper=None), algo=algo) == B.E_INVAL
+    assert call(lib, _inst(), algo=5) == B.E_INVAL
+    assert call(lib, _inst(), algo=-1) == B.E_INVAL
     assert call(lib, _inst(), res=_res(status=None)) == B.E_INVAL
     assert call(lib, _inst(), res=_res(completion=None)) == B.E_INVAL
     assert call(lib, _inst(), res=_res(total_latency=None)) == B.E_INVAL

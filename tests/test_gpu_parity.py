@@ -16,7 +16,7 @@ from paper_2508_14544_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
 
-ALGOS = {"amax": O.AMAX, "amin": O.AMIN, "hsf": O.HSF}
+ALGOS = {"amax": O.AMAX, "amin": O.AMIN, "hsf": O.HSF, "aell": O.AELL, "adaptive": O.ADAPTIVE}
 
 
 def _say(msg):

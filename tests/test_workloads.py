@@ -90,3 +90,19 @@ def test_alpha_blocks():
     assert np.bincount(idx).tolist() == [1365, 1365, 1366]
     idx = W._alpha_blocks(65536, list(range(9)))
     assert np.bincount(idx).tolist() == [7281] * 8 + [7288]
+
+
+def test_twopoint_recipe():
+    b = W.generate("twopoint4096_n1000_m16384", 0, instance_ids=[0, 681, 682, 2045, 2046, 4095])
+    alphas = [Fraction(1, 10), Fraction(1, 10), Fraction(1, 5), Fraction(3, 10), Fraction(2, 5), Fraction(3, 5)]
+    for j in range(b.num_instances):
+        inst = b.instance(j)
+        lk, uk = int(inst["lower"][0]), int(inst["upper"][0])
+        assert (inst["lower"] == lk).all() and (inst["upper"] == uk).all()
+        assert 2 <= lk <= 64
+        a = alphas[j]
+        assert uk == -((-lk * a.denominator) // a.numerator)  # ceil(l / alpha)
+        assert set(np.unique(inst["output"])) <= {lk, uk}
+        assert 0.4 < (inst["output"] == uk).mean() < 0.6
+        assert (inst["arrival"] == 0).all()
+        assert str(a) == b.meta["alpha"][j]
