@@ -123,7 +123,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="batch4096_n1000_m16384")
-    ap.add_argument("--algo", default="amin", choices=["amin", "amax", "hsf"])
+    ap.add_argument("--algo", default="amin", choices=["amin", "amax", "hsf", "aell", "adaptive"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--running-capacity", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
@@ -216,7 +216,8 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": args.workload,
-            "algo": {"amin": "A_min", "amax": "A_max", "hsf": "H-SF"}[args.algo],
+            "algo": {"amin": "A_min", "amax": "A_max", "hsf": "H-SF", "aell": "A_l",
+                     "adaptive": "adaptive A_min/A_l"}[args.algo],
             "instances": batch.num_instances,
             "requests_per_instance": W.WORKLOADS[args.workload].n,
             "M": batch.M,
@@ -225,6 +226,9 @@ def main():
             "instance_steps_per_step": int(g["makespan"].astype(np.int64).sum()),
             "requests_x_makespan_per_step": int((np.diff(batch.offsets) * g["makespan"].astype(np.int64)).sum()),
             "instances_subset": subset or None,
+            "instances_per_policy": ({"A_min": int((g["algo_used"] == B.AMIN).sum()),
+                                      "A_l": int((g["algo_used"] == B.AELL).sum())}
+                                     if args.algo == "adaptive" else None),
             "all_status_ok": status_ok,
         },
         "roofline": {
