@@ -345,3 +345,69 @@ def random_small(seed: int, num_instances: int, n_max: int, *, s_max: int = 6, o
         a = np.sort(uniform_int(ra[k, :n], 0, 2 * o_max)) if arrivals else np.zeros(n, np.int64)
         out.append({"arrival": a, "prompt": s, "output": o, "lower": l, "upper": u})
     return from_lists(M, out, name=f"random_small_{seed}")
+
+
+# ---------------------------------------------------------------------------
+# Analogue of the paper's experiments (Section 6) in unit time steps.
+# ---------------------------------------------------------------------------
+# The paper samples 2000 conversations of LMSYS-Chat-1M: prompt sizes 1..468
+# (mean 41, median 11, variance 4961), output lengths 1..883 (mean 85, median
+# 43, variance 9702).  The data is not available here; these draws come from
+# discretised log-normals round(exp(mu + sigma Z)) conditioned on the same
+# ranges, fitted to those statistics (prompts: mu 2.338, sigma 2.050 -> mean
+# 40.0, median 11, variance 5084; outputs: mu 3.821, sigma 1.100 -> mean 79.3,
+# median 45, variance 9933).  Sampling is exact inversion of the finite CDF.
+EXP_PROMPT = (2.338, 2.050, 1, 468)
+EXP_OUTPUT = (3.821, 1.100, 1, 883)
+EXP_M = 16384            # the paper does not state its memory budget
+EXP_POOL = 2000          # requests drawn per replicate; size-n instances take the first n
+EXP_SETTINGS = ("exp1", "exp2", "exp3_x10", "exp3_x95", "exp3_x99")
+
+
+def _lognormal_table(mu: float, sigma: float, lo: int, hi: int):
+    import math
+    ks = np.arange(lo, hi + 1, dtype=np.int64)
+    cdf = lambda z: 0.5 * math.erfc(-z / math.sqrt(2.0))
+    lo_edge = [(math.log(k - 0.5) - mu) / sigma if k > 0.5 else -np.inf for k in ks]
+    hi_edge = [(math.log(k + 0.5) - mu) / sigma for k in ks]
+    p = np.array([cdf(b) - (0.0 if a == -np.inf else cdf(a)) for a, b in zip(lo_edge, hi_edge)])
+    c = np.cumsum(p / p.sum())
+    c[-1] = 1.0
+    return ks, c
+
+
+def _draw_table(table, r: np.ndarray) -> np.ndarray:
+    ks, c = table
+    return ks[np.minimum(np.searchsorted(c, uniform01(r), side="right"), len(ks) - 1)]
+
+
+def experiment(setting: str, n: int, replicates: int, seed: int = 0) -> Instances:
+    """`replicates` instances of n requests for one prediction setting of Section 6.
+
+    exp1: every interval is [1, 1000] (rough prediction).
+    exp2: the bucket [100k+1, 100(k+1)] that holds o (non-overlapping classes).
+    exp3_xNN: [max(1, floor((1-x) o)), ceil((1+x) o)] with x = NN/100 (exact).
+    All requests arrive at step 0.  Replicate r draws a pool of EXP_POOL
+    requests once; its size-n instance is the first n of them, so sizes are
+    nested samples of one pool, as in the paper's subsets of its 2000.
+    """
+    if setting not in EXP_SETTINGS or not (1 <= n <= EXP_POOL):
+        raise ValueError(setting)
+    wid = 7
+    ids = np.arange(replicates, dtype=np.int64)
+    s = _draw_table(_lognormal_table(*EXP_PROMPT), raw64(seed, wid, F_PROMPT, ids, EXP_POOL))[:, :n]
+    o = _draw_table(_lognormal_table(*EXP_OUTPUT), raw64(seed, wid, F_OUTPUT, ids, EXP_POOL))[:, :n]
+    if setting == "exp1":
+        l, u = np.ones_like(o), np.full_like(o, 1000)
+    elif setting == "exp2":
+        k = (o - 1) // 100
+        l, u = 100 * k + 1, 100 * (k + 1)
+    else:
+        x = int(setting.split("_x")[1])
+        l = np.maximum(1, ((100 - x) * o) // 100)
+        u = -((-(100 + x) * o) // 100)
+    K = replicates
+    offsets = np.arange(K + 1, dtype=np.int64) * n
+    c32 = lambda v: np.ascontiguousarray(v.reshape(-1), dtype=np.int32)
+    return Instances(f"{setting}_n{n}", EXP_M, offsets, c32(np.zeros((K, n), np.int64)), c32(s), c32(o),
+                     c32(l), c32(u), ids, {"seed": seed, "setting": setting})

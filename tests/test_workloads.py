@@ -106,3 +106,24 @@ def test_twopoint_recipe():
         assert 0.4 < (inst["output"] == uk).mean() < 0.6
         assert (inst["arrival"] == 0).all()
         assert str(a) == b.meta["alpha"][j]
+
+
+def test_experiment_recipe():
+    # Section 6's statistics (prompts mean 41, median 11; outputs mean 85, median 43)
+    # approximately, nested sizes, and the three interval settings
+    b = W.experiment("exp1", 2000, 16)
+    s, o = b.prompt, b.output
+    assert 1 <= s.min() and s.max() <= 468 and 1 <= o.min() and o.max() <= 883
+    assert 36 < s.mean() < 45 and np.median(s) in (10, 11, 12)
+    assert 72 < o.mean() < 88 and 40 <= np.median(o) <= 48
+    assert (b.lower == 1).all() and (b.upper == 1000).all() and (b.arrival == 0).all()
+    small = W.experiment("exp1", 200, 16)
+    for k in range(16):
+        assert (small.instance(k)["output"] == b.instance(k)["output"][:200]).all()
+    e2 = W.experiment("exp2", 2000, 4)
+    assert ((e2.lower - 1) % 100 == 0).all() and (e2.upper - e2.lower == 99).all()
+    assert ((e2.lower <= e2.output) & (e2.output <= e2.upper)).all()
+    e3 = W.experiment("exp3_x95", 2000, 4)
+    oo = e3.output.astype(np.int64)
+    assert (e3.lower == np.maximum(1, 5 * oo // 100)).all()
+    assert (e3.upper == -((-195 * oo) // 100)).all()
