@@ -24,8 +24,8 @@ from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
-AMAX, AMIN, HSF, AELL, ADAPTIVE = 0, 1, 2, 3, 4
-ALGOS = {"amax": AMAX, "amin": AMIN, "hsf": HSF, "aell": AELL, "adaptive": ADAPTIVE}
+AMAX, AMIN, HSF, AELL, ADAPTIVE, ARANDOM = 0, 1, 2, 3, 4, 5
+ALGOS = {"amax": AMAX, "amin": AMIN, "hsf": HSF, "aell": AELL, "adaptive": ADAPTIVE, "arandom": ARANDOM}
 OK, E_INVAL, E_INTERVAL, E_TOO_BIG, E_STEP_CAP, E_ARRIVAL = 0, -1, -2, -3, -4, -7
 EV_START, EV_EVICT, EV_COMPLETE = 0, 1, 2
 STAT_NAMES = ["max_running", "max_evicted_waiting", "max_waiting", "steps", "tests", "evict_events", "work"]
@@ -60,7 +60,7 @@ def _load():
             P32 = ctypes.POINTER(ctypes.c_int32)
             P64 = ctypes.POINTER(ctypes.c_int64)
             lib.orc_simulate.restype = ctypes.c_int
-            lib.orc_simulate.argtypes = [ctypes.c_int32, P32, P32, P32, P32, P32, ctypes.c_int32,
+            lib.orc_simulate.argtypes = [ctypes.c_int32, P32, P32, P32, P32, P32, P32, ctypes.c_int32,
                                          ctypes.c_int64, ctypes.c_int64, P32, P32, P64, P64, P64,
                                          P64, P64, ctypes.POINTER(_Event), ctypes.c_int64, P64]
             lib.orc_default_step_cap.restype = ctypes.c_int64
@@ -92,6 +92,7 @@ def simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap: int = 
     s = _c32(inst["prompt"])
     lo = _c32(inst.get("lower"))
     up = _c32(inst.get("upper"))
+    pr = _c32(inst.get("priority"))
     comp = np.empty(n, np.int32)
     ev = np.empty(n, np.int32)
     tel, mk, rs, te, nev = (ctypes.c_int64() for _ in range(5))
@@ -102,13 +103,13 @@ def simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap: int = 
         cap_ev = 1 << 16
         evbuf = (_Event * cap_ev)()
     P64 = ctypes.POINTER(ctypes.c_int64)
-    status = lib.orc_simulate(n, _p32(a), _p32(s), _p32(o), _p32(lo), _p32(up), int(algo), int(M),
+    status = lib.orc_simulate(n, _p32(a), _p32(s), _p32(o), _p32(lo), _p32(up), _p32(pr), int(algo), int(M),
                               int(step_cap), _p32(comp), _p32(ev), ctypes.byref(tel), ctypes.byref(mk),
                               ctypes.byref(rs), ctypes.byref(te), st_arr.ctypes.data_as(P64),
                               evbuf if events else ctypes.POINTER(_Event)(), cap_ev, ctypes.byref(nev))
     if events and nev.value > cap_ev:
         evbuf = (_Event * nev.value)()
-        status = lib.orc_simulate(n, _p32(a), _p32(s), _p32(o), _p32(lo), _p32(up), int(algo), int(M),
+        status = lib.orc_simulate(n, _p32(a), _p32(s), _p32(o), _p32(lo), _p32(up), _p32(pr), int(algo), int(M),
                                   int(step_cap), _p32(comp), _p32(ev), ctypes.byref(tel), ctypes.byref(mk),
                                   ctypes.byref(rs), ctypes.byref(te), st_arr.ctypes.data_as(P64),
                                   evbuf, nev.value, ctypes.byref(nev))
@@ -192,7 +193,7 @@ def literal_simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap
     arr = [int(x) for x in inst["arrival"]] if inst.get("arrival") is not None else [0] * n
     if algo == AMAX:
         plan = [int(x) for x in inst["upper"]]
-    elif algo == HSF:
+    elif algo in (HSF, ARANDOM):
         plan = list(o)
     else:
         plan = [int(x) for x in inst["lower"]]
@@ -248,7 +249,12 @@ def literal_simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap
         # in-progress runs: (start, prompt, planned length from its start)
         in_progress = [(start[i], s[i], max(plan[i], t + 1 - start[i])) for i in start]
         in_progress += [(t - o[i], s[i], o[i]) for i in finished_now]
-        order_key = (lambda r: (queue_pos[r], r)) if algo == AELL else (lambda r: (plan[r], r))
+        if algo == AELL:
+            order_key = lambda r: (queue_pos[r], r)
+        elif algo == ARANDOM:
+            order_key = lambda r: (int(inst["priority"][r]), r)
+        else:
+            order_key = lambda r: (plan[r], r)
         order = sorted((w for w in waiting if eligible_from[w] <= t), key=order_key)
         chosen: List[int] = []
         for w in order:
@@ -396,8 +402,8 @@ def audit(inst: Dict[str, Sequence[int]], algo: int, M: int, result: Dict[str, o
         assert comp[i] == final_start[i] + o[i], "completion mismatch"
         assert comp[i] >= arr[i] + o[i]
         assert int(result["evictions"][i]) == n_evict[i]
-    if algo in (AMAX, HSF):
-        assert sum(n_evict) == 0, "A_max/H-SF never cancel"
+    if algo in (AMAX, HSF, ARANDOM):
+        assert sum(n_evict) == 0, "A_max, H-SF and A_random never cancel"
     # equation (1) before and after the eviction point of every step
     horizon = max((r[2] for r in runs), default=0)
     for tau in range(0, horizon + 1):

@@ -21,6 +21,9 @@
  *     (promoted requests keep their promotion order); it may restart at once.
  *   - The adaptive switch of Section 5.1 between A_min and A_l at
  *     alpha* = (3 - sqrt 5)/2, from Theorems 5.1 and 5.2.
+ *   - The auxiliary A_random (Appendix, proof of Theorem 3.1): plan with the
+ *     true o and add waiting requests in a given random order while equation
+ *     (2) holds (the order arrives as per-request priorities).
  *   - Equation (3) (total end-to-end latency).
  * Readings where the paper is silent (each listed in the design notes):
  *   memory of a run counts at both its start and its completion step; a
@@ -39,7 +42,8 @@ enum { NOT_ARRIVED = 0, WAITING = 1, RUNNING = 2, DONE = 3 };
 
 /* ---------------------------------------------------------------------------
  * Waiting set: binary min-heap of request indices ordered by (key, index), where
- * key is the planning length (A_max, A_min, H-SF) or the queue position (A_l).
+ * key is the planning length (A_max, A_min, H-SF), the queue position (A_l) or
+ * the priority (A_random).
  * Only "peek the smallest" and "remove the smallest" are needed, because the
  * admission walk stops at the first request that does not fit.
  * ------------------------------------------------------------------------- */
@@ -176,7 +180,7 @@ int32_t orc_adaptive_choice(int32_t n, const int32_t* l, const int32_t* u) {
 }
 
 int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o,
-                 const int32_t* l, const int32_t* u, int32_t algo, int64_t M,
+                 const int32_t* l, const int32_t* u, const int32_t* prio, int32_t algo, int64_t M,
                  int64_t step_cap, int32_t* completion, int32_t* evictions,
                  int64_t* tel, int64_t* makespan, int64_t* request_steps,
                  int64_t* total_evictions, int64_t* stats, orc_event_t* events,
@@ -189,7 +193,8 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
   *total_evictions = 0;
   if (n_events) *n_events = 0;
   if (n < 0 || M <= 0 || (n > 0 && (!s || !o || !completion))) return ORC_E_INVAL;
-  if (algo < ORC_AMAX || algo > ORC_ADAPTIVE) return ORC_E_INVAL;
+  if (algo < ORC_AMAX || algo > ORC_ARANDOM) return ORC_E_INVAL;
+  if (n > 0 && algo == ORC_ARANDOM && !prio) return ORC_E_INVAL;
   if (n > 0 && (algo == ORC_AMIN || algo == ORC_AELL || algo == ORC_ADAPTIVE) && !l) return ORC_E_INVAL;
   if (n > 0 && (algo == ORC_AMAX || algo == ORC_AELL || algo == ORC_ADAPTIVE) && !u) return ORC_E_INVAL;
   if (algo == ORC_ADAPTIVE) algo = orc_adaptive_choice(n, l, u);
@@ -218,13 +223,13 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
   int64_t* qpos = (int64_t*)malloc(sizeof(int64_t) * n);
   int32_t* promoted = (int32_t*)malloc(sizeof(int32_t) * n);
   int64_t n_promotions = 0;
-  heap_t waiting = {heap_mem, 0, algo == ORC_AELL ? qpos : est};
+  heap_t waiting = {heap_mem, 0, algo == ORC_AELL || algo == ORC_ARANDOM ? qpos : est};
 
   /* Planning length: u (A_max, Alg. 1), o (H-SF, Alg. 3), o~ initialised to l
    * (A_min, Alg. 2 and Alg. 4; A_l, Alg. 5). */
   for (int32_t i = 0; i < n; i++) {
-    est[i] = (algo == ORC_AMAX) ? u[i] : (algo == ORC_HSF) ? o[i] : l[i];
-    qpos[i] = i;
+    est[i] = (algo == ORC_AMAX) ? u[i] : (algo == ORC_HSF || algo == ORC_ARANDOM) ? o[i] : l[i];
+    qpos[i] = algo == ORC_ARANDOM ? prio[i] : i;
   }
 
   int32_t n_running = 0, n_deferred = 0, n_done = 0, next_arrival = 0;

@@ -20,7 +20,11 @@ extern "C" {
  * ORC_ADAPTIVE: per instance, A_l when the ratio alpha = (sum l)/(sum u) is
  * below alpha* = (3 - sqrt 5)/2 (where Theorem 5.2's bound for A_l is below
  * Theorem 5.1's for A_min, Section 5.1), A_min otherwise. */
-enum { ORC_AMAX = 0, ORC_AMIN = 1, ORC_HSF = 2, ORC_AELL = 3, ORC_ADAPTIVE = 4 };
+/* ORC_ARANDOM: the auxiliary policy A_random (Appendix, used in the proof of
+ * Theorem 3.1): plan with the true o and walk the waiting requests in a random
+ * order given by the caller as per-request priorities (ascending, ties by
+ * index). */
+enum { ORC_AMAX = 0, ORC_AMIN = 1, ORC_HSF = 2, ORC_AELL = 3, ORC_ADAPTIVE = 4, ORC_ARANDOM = 5 };
 
 enum {
   ORC_OK = 0,
@@ -60,8 +64,10 @@ enum {
  *   l, u    : predicted interval bounds; l is needed for A_min, u for A_max,
  *             both for A_l and the adaptive choice (either may be NULL when the
  *             algorithm does not read it).
- *   algo    : ORC_AMAX, ORC_AMIN, ORC_HSF, ORC_AELL or ORC_ADAPTIVE (which
- *             simulates orc_adaptive_choice's algorithm).
+ *   prio    : per-request priorities (the random order of A_random); needed
+ *             only for ORC_ARANDOM (NULL otherwise).
+ *   algo    : ORC_AMAX, ORC_AMIN, ORC_HSF, ORC_AELL, ORC_ADAPTIVE (which
+ *             simulates orc_adaptive_choice's algorithm) or ORC_ARANDOM.
  *   M       : KV-cache budget in tokens (> 0).
  *   step_cap: last step index that may be simulated; <= 0 selects the default
  *             min(2^30, 4*(max a + sum(o+1)) + 64).
@@ -73,7 +79,7 @@ enum {
  * Returns the instance status (ORC_OK or a negative code).
  */
 int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o,
-                 const int32_t* l, const int32_t* u, int32_t algo, int64_t M,
+                 const int32_t* l, const int32_t* u, const int32_t* prio, int32_t algo, int64_t M,
                  int64_t step_cap, int32_t* completion, int32_t* evictions,
                  int64_t* tel, int64_t* makespan, int64_t* request_steps,
                  int64_t* total_evictions, int64_t* stats, orc_event_t* events,

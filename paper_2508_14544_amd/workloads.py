@@ -114,6 +114,7 @@ class Instances:
     upper: Optional[np.ndarray]   # int32 [N]
     instance_ids: np.ndarray      # int64 [K] ids within the full workload
     meta: Dict[str, object] = field(default_factory=dict)
+    priority: Optional[np.ndarray] = None   # int32 [N]: the random order of A_random
 
     @property
     def num_instances(self) -> int:
@@ -134,11 +135,12 @@ class Instances:
         d = {"arrival": self.arrival[b:e], "prompt": self.prompt[b:e], "output": self.output[b:e]}
         d["lower"] = None if self.lower is None else self.lower[b:e]
         d["upper"] = None if self.upper is None else self.upper[b:e]
+        d["priority"] = None if self.priority is None else self.priority[b:e]
         return d
 
     def subset(self, ks: Sequence[int]) -> "Instances":
         ks = list(ks)
-        parts = {f: [] for f in ("arrival", "prompt", "output", "lower", "upper")}
+        parts = {f: [] for f in ("arrival", "prompt", "output", "lower", "upper", "priority")}
         offs = [0]
         for k in ks:
             d = self.instance(k)
@@ -150,7 +152,8 @@ class Instances:
         return Instances(self.name, self.M, np.array(offs, dtype=np.int64), cat("arrival"), cat("prompt"),
                          cat("output"), None if self.lower is None else cat("lower"),
                          None if self.upper is None else cat("upper"),
-                         self.instance_ids[ks].copy(), dict(self.meta))
+                         self.instance_ids[ks].copy(), dict(self.meta),
+                         None if self.priority is None else cat("priority"))
 
 
 # ---------------------------------------------------------------------------
@@ -294,7 +297,7 @@ def generate(name: str, seed: int = 0, instance_ids: Optional[Sequence[int]] = N
 def from_lists(M: int, instances: List[Dict[str, Sequence[int]]], name: str = "custom") -> Instances:
     """Pack hand-written instances (dicts with keys arrival/prompt/output/lower/upper) into CSR."""
     offs = [0]
-    cols: Dict[str, list] = {f: [] for f in ("arrival", "prompt", "output", "lower", "upper")}
+    cols: Dict[str, list] = {f: [] for f in ("arrival", "prompt", "output", "lower", "upper", "priority")}
     has = {f: True for f in cols}
     for d in instances:
         n = len(d["output"])
@@ -313,7 +316,8 @@ def from_lists(M: int, instances: List[Dict[str, Sequence[int]]], name: str = "c
     arr = lambda f: np.array(cols[f], dtype=np.int32) if has[f] else None
     K = len(instances)
     return Instances(name, int(M), np.array(offs, dtype=np.int64), arr("arrival"), arr("prompt"),
-                     arr("output"), arr("lower"), arr("upper"), np.arange(K, dtype=np.int64))
+                     arr("output"), arr("lower"), arr("upper"), np.arange(K, dtype=np.int64),
+                     priority=arr("priority"))
 
 
 def random_small(seed: int, num_instances: int, n_max: int, *, s_max: int = 6, o_max: int = 8,
@@ -411,3 +415,16 @@ def experiment(setting: str, n: int, replicates: int, seed: int = 0) -> Instance
     c32 = lambda v: np.ascontiguousarray(v.reshape(-1), dtype=np.int32)
     return Instances(f"{setting}_n{n}", EXP_M, offsets, c32(np.zeros((K, n), np.int64)), c32(s), c32(o),
                      c32(l), c32(u), ids, {"seed": seed, "setting": setting})
+
+
+def with_random_order(batch: Instances, seed: int = 0) -> Instances:
+    """A copy of `batch` with A_random's random order: per instance a uniformly
+    random permutation of 0..n-1 (ranks of i.i.d. 64-bit draws, keyed by the
+    instance's workload id), given as per-request priorities."""
+    import dataclasses
+    pr = np.empty(batch.total_requests, np.int32)
+    for k in range(batch.num_instances):
+        b, e = int(batch.offsets[k]), int(batch.offsets[k + 1])
+        r = raw64(seed, 200, 0, np.array([batch.instance_ids[k]], np.int64), e - b)[0]
+        pr[b:e] = np.argsort(np.argsort(r, kind="stable"), kind="stable").astype(np.int32)
+    return dataclasses.replace(batch, priority=pr)

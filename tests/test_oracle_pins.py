@@ -356,3 +356,46 @@ def test_aell_c_oracle_equals_literal_and_audit(seed):
             O.audit(inst, algo, b.M, r)
             n_prom += r["total_evictions"]
     assert n_prom > 0
+
+
+def test_arandom_reductions():
+    # A_random plans with the true o (like H-SF) and walks a given random order;
+    # with the order of H-SF's key (o, index) it is H-SF bit-exactly
+    b = W.random_small(21, 40, 9, s_max=5, o_max=9, M=25)
+    for k in range(b.num_instances):
+        inst = dict(b.instance(k))
+        o = np.asarray(inst["output"])
+        rank = np.empty(len(o), np.int32)
+        rank[np.lexsort((np.arange(len(o)), o))] = np.arange(len(o))
+        inst["priority"] = rank
+        assert same(O.simulate(inst, O.ARANDOM, b.M), O.simulate(inst, O.HSF, b.M))
+
+
+def test_arandom_theorem31_random_order_bound_soft():
+    # Appendix (proof of Theorem 3.1): CR(A_random) <= (1 + 1/alpha)/2 + O(1/M),
+    # in expectation over the random order; checked on the mean over 12 random
+    # orders of two-point instances (the worst case of that theorem), M large.
+    l, u = 5, 20
+    rng = np.random.default_rng(3)
+    n = 600
+    o = rng.choice([l, u], n)
+    base = {"prompt": np.ones(n, int), "output": o, "lower": np.full(n, l), "upper": np.full(n, u)}
+    M = 40 * (1 + u)
+    hsf = O.simulate(base, O.HSF, M)["tel"]
+    tels = []
+    for rep in range(12):
+        inst = dict(base, priority=rng.permutation(n).astype(np.int32))
+        r = O.simulate(inst, O.ARANDOM, M, events=True)
+        O.audit(inst, O.ARANDOM, M, r)
+        tels.append(r["tel"])
+    assert np.mean(tels) / hsf <= (1 + u / l) / 2
+
+
+@pytest.mark.parametrize("seed", range(2))
+def test_arandom_c_oracle_equals_literal(seed):
+    b = W.with_random_order(W.random_small(seed + 30, 60, 8, s_max=5, o_max=9, M=24, arrivals=(seed == 1)), seed)
+    for k in range(b.num_instances):
+        inst = b.instance(k)
+        r = O.simulate(inst, O.ARANDOM, b.M, events=True)
+        assert same(r, O.literal_simulate(inst, O.ARANDOM, b.M))
+        O.audit(inst, O.ARANDOM, b.M, r)
