@@ -123,7 +123,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="batch4096_n1000_m16384")
-    ap.add_argument("--algo", default="amin", choices=["amin", "amax", "hsf", "aell", "adaptive"])
+    ap.add_argument("--algo", default="amin", choices=["amin", "amax", "hsf", "aell", "adaptive", "arandom"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--running-capacity", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
@@ -152,6 +152,8 @@ def main():
     subset = [int(x) for x in args.instances.split(",") if x.strip()]
     if subset:
         batch = batch.subset(subset)
+    if args.algo == "arandom":   # A_random's random order is an input, drawn by the generator
+        batch = W.with_random_order(batch, args.seed)
     dev = torch.device("cuda:0")
     torch.cuda.synchronize()
     h0 = time.perf_counter()
@@ -159,7 +161,8 @@ def main():
     torch.cuda.synchronize()
     h2d_ms = (time.perf_counter() - h0) * 1e3
     h2d_bytes = sum(int(t.numel()) * t.element_size() for t in
-                    (db.offsets, db.arrival, db.prompt, db.output, db.lower, db.upper) if t is not None)
+                    (db.offsets, db.arrival, db.prompt, db.output, db.lower, db.upper, db.priority)
+                    if t is not None)
     out = B.alloc_results(db)
     stream = torch.cuda.current_stream(dev)
     kw = dict(stream=stream, running_capacity=args.running_capacity)
@@ -217,7 +220,7 @@ def main():
         "config": {
             "workload": args.workload,
             "algo": {"amin": "A_min", "amax": "A_max", "hsf": "H-SF", "aell": "A_l",
-                     "adaptive": "adaptive A_min/A_l"}[args.algo],
+                     "adaptive": "adaptive A_min/A_l", "arandom": "A_random"}[args.algo],
             "instances": batch.num_instances,
             "requests_per_instance": W.WORKLOADS[args.workload].n,
             "M": batch.M,

@@ -30,6 +30,10 @@
  *               competitive-ratio bound of Theorem 5.2 for A_l is the smaller
  *               one; Theorem 5.1 bounds A_min), SCHED_AMIN otherwise.  The
  *               comparison is exact: (3U - 2L)^2 > 5U^2.
+ *   SCHED_ARANDOM  The auxiliary A_random (Appendix, in the proof of Theorem
+ *               3.1): plan with the true o_i like H-SF, but walk the waiting
+ *               requests in a random order, given as per-request priorities
+ *               (ascending; ties by index) drawn by the caller.
  * Each step, waiting requests are tried in ascending (planning length, index)
  * order (A_l: the queue order above) and the longest prefix that keeps
  * equation (2) is started.  Ties break by ascending request index.  Requests
@@ -56,7 +60,8 @@ typedef enum {
   SCHED_AMIN = 1,
   SCHED_HSF = 2,
   SCHED_AELL = 3,
-  SCHED_ADAPTIVE = 4
+  SCHED_ADAPTIVE = 4,
+  SCHED_ARANDOM = 5
 } sched_algo_t;
 
 /* Return codes of the calls (synchronous) and per-instance status values
@@ -72,8 +77,9 @@ enum {
   SCHED_E_STEP_CAP = -4,    /* status: unfinished requests when the step cap was passed        */
   SCHED_E_HIP = -5,         /* call: a HIP runtime call failed                                  */
   SCHED_E_UNSUPPORTED = -6, /* call: capacity request beyond what the kernels hold.
-                               status: o, u or l >= 2^15, s >= 2^16, n >= 2^17, or the running
-                               or evicted set outgrew its capacity                              */
+                               status: o, u or l >= 2^15, s >= 2^16, n >= 2^17, a priority
+                               outside [0, 2^15), or the running or evicted set outgrew its
+                               capacity                                                          */
   SCHED_E_ARRIVAL = -7      /* status: an arrival < 0 or arrivals not non-decreasing in index  */
 };
 
@@ -89,6 +95,8 @@ typedef struct {
   const int32_t* output;    /* [N] true output length o_i (the simulated world)         */
   const int32_t* lower;     /* [N] l_i; required for SCHED_AMIN, SCHED_AELL, SCHED_ADAPTIVE */
   const int32_t* upper;     /* [N] u_i; required for SCHED_AMAX, SCHED_AELL, SCHED_ADAPTIVE */
+  const int32_t* priority;  /* [N] A_random's order (ascending, ties by index); required for
+                               SCHED_ARANDOM, unused otherwise                              */
 } sched_instances_t;
 
 /* Outputs.  Per request: completion step C_i (-1 if it never completed) and

@@ -15,8 +15,8 @@ from typing import Dict, Optional
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libschedsim.so")
 
-AMAX, AMIN, HSF, AELL, ADAPTIVE = 0, 1, 2, 3, 4
-ALGOS = {"amax": AMAX, "amin": AMIN, "hsf": HSF, "aell": AELL, "adaptive": ADAPTIVE}
+AMAX, AMIN, HSF, AELL, ADAPTIVE, ARANDOM = 0, 1, 2, 3, 4, 5
+ALGOS = {"amax": AMAX, "amin": AMIN, "hsf": HSF, "aell": AELL, "adaptive": ADAPTIVE, "arandom": ARANDOM}
 OK, E_INVAL, E_INTERVAL, E_TOO_BIG, E_STEP_CAP, E_HIP, E_UNSUPPORTED, E_ARRIVAL = 0, -1, -2, -3, -4, -5, -6, -7
 
 # every symbol include/schedsim.h declares
@@ -34,6 +34,7 @@ class SchedInstances(ctypes.Structure):
         ("output", ctypes.c_void_p),
         ("lower", ctypes.c_void_p),
         ("upper", ctypes.c_void_p),
+        ("priority", ctypes.c_void_p),
     ]
 
 
@@ -110,6 +111,7 @@ class DeviceBatch:
     output: object
     lower: object
     upper: object
+    priority: object = None
 
     @property
     def num_instances(self) -> int:
@@ -129,7 +131,7 @@ def to_device(batch, device="cuda") -> DeviceBatch:
 
     return DeviceBatch(batch.M, batch.max_requests, t(batch.offsets, torch.int64), t(batch.arrival, torch.int32),
                        t(batch.prompt, torch.int32), t(batch.output, torch.int32), t(batch.lower, torch.int32),
-                       t(batch.upper, torch.int32))
+                       t(batch.upper, torch.int32), t(getattr(batch, "priority", None), torch.int32))
 
 
 def alloc_results(db: DeviceBatch, evictions: bool = True):
@@ -158,7 +160,7 @@ def simulate_into(db: DeviceBatch, algo: int, out: Dict[str, object], *, M: Opti
         stream = torch.cuda.current_stream(db.output.device)
     inst = SchedInstances(db.num_instances, db.max_requests, db.total_requests, _ptr(db.offsets), _ptr(db.arrival),
                           _ptr(db.prompt), _ptr(db.output), _ptr(db.lower) if pass_lower else None,
-                          _ptr(db.upper) if pass_upper else None)
+                          _ptr(db.upper) if pass_upper else None, _ptr(db.priority))
     res = SchedResults(_ptr(out["completion"]), _ptr(out.get("evictions")), _ptr(out["tel"]),
                        _ptr(out.get("makespan")), _ptr(out.get("request_steps")), _ptr(out.get("total_evictions")),
                        _ptr(out["status"]), _ptr(out.get("algo_used")))

@@ -57,6 +57,7 @@ struct Params {
   const int32_t* output;
   const int32_t* lower;
   const int32_t* upper;
+  const int32_t* priority;
   int32_t* completion;
   int32_t* evictions;
   int64_t* total_latency;
@@ -99,6 +100,7 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
   // both (their sums pick the policy) and validates with the one it picks
   constexpr bool kReadL = ALGO == SCHED_AMIN || ALGO == SCHED_AELL || ALGO == SCHED_ADAPTIVE;
   constexpr bool kReadU = ALGO == SCHED_AMAX || ALGO == SCHED_AELL || ALGO == SCHED_ADAPTIVE;
+  constexpr bool kReadP = ALGO == SCHED_ARANDOM;
   bool arr_bad = false, int_bad = false, big_bad = false, unsup = (n >= (1 << kIdxBits));
   bool bad_l = false, unsup_l = false, bad_u = false, big_u = false, unsup_u = false;
   int64_t max_a = 0, sum_o = 0, sum_l = 0, sum_u = 0;
@@ -106,13 +108,14 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
   for (int c = 0; c < n; c += 64) {
     const int i = c + lane;
     const bool act = i < n;
-    int32_t a = 0, s = 0, o = 1, lo = 1, up = 1;
+    int32_t a = 0, s = 0, o = 1, lo = 1, up = 1, pr = 0;
     if (act) {
       a = P.arrival ? P.arrival[b + i] : 0;
       s = P.prompt[b + i];
       o = P.output[b + i];
       if (kReadL) lo = P.lower[b + i];
       if (kReadU) up = P.upper[b + i];
+      if (kReadP) pr = P.priority[b + i];
     }
     int32_t ap = __shfl_up(a, 1, 64);
     if (lane == 0) ap = prev_last;
@@ -124,7 +127,7 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
       if (up < o) bad_u = true;
       if (static_cast<int64_t>(s) + o > P.M) big_bad = true;
       if (static_cast<int64_t>(s) + up > P.M) big_u = true;
-      if (o >= kEstLimit || s >= kPromptLimit) unsup = true;
+      if (o >= kEstLimit || s >= kPromptLimit || pr < 0 || pr >= kEstLimit) unsup = true;
       if (lo >= kEstLimit) unsup_l = true;
       if (up >= kEstLimit) unsup_u = true;
       max_a = a > max_a ? a : max_a;
@@ -178,11 +181,15 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
   }
   if (status != SCHED_OK || n == 0) return;
 
-  // ---- keys (est0 << 17 | index), est0 = u (A_max), l (A_min, A_l), o (H-SF)
+  // ---- keys (k0 << 17 | index), k0 = u (A_max), l (A_min, A_l), o (H-SF), the
+  // priority (A_random, which plans with o)
   for (int c = 0; c < n; c += 64) {
     const int i = c + lane;
     if (i < n) {
-      int32_t est = (algo == SCHED_AMAX) ? P.upper[b + i] : (algo == SCHED_HSF) ? P.output[b + i] : P.lower[b + i];
+      int32_t est = (algo == SCHED_AMAX)   ? P.upper[b + i]
+                    : (algo == SCHED_HSF)  ? P.output[b + i]
+                    : (algo == SCHED_ARANDOM) ? P.priority[b + i]
+                                           : P.lower[b + i];
       P.sort_a[b + i] = (static_cast<uint32_t>(est) << kIdxBits) | static_cast<uint32_t>(i);
     }
   }
@@ -443,9 +450,9 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
     c_fromF = f_rank >= 0 && (ALGO == SCHED_AELL || f_key < v_key);                  \
     c_key = c_fromF ? f_key : v_key;                                                 \
     const uint32_t so_ = c_fromF ? f_so : v_so;                                      \
-    c_est = static_cast<int32_t>(c_key >> kIdxBits);                                 \
     c_s = static_cast<int32_t>(so_ & 0xFFFFu);                                       \
     c_o = static_cast<int32_t>(so_ >> 16);                                           \
+    c_est = ALGO == SCHED_ARANDOM ? c_o : static_cast<int32_t>(c_key >> kIdxBits);   \
     c_u = c_fromF ? f_u : v_u;                                                       \
   } while (0)
     // BODY with the compile-time row index r equal to the uniform row RR_
@@ -942,6 +949,7 @@ hipError_t set_lds_limit_any(int algo, int rows, bool retry, int bytes) {
     case SCHED_AMAX: return set_lds_limit<SCHED_AMAX>(rows, retry, bytes);
     case SCHED_AMIN: return set_lds_limit<SCHED_AMIN>(rows, retry, bytes);
     case SCHED_HSF: return set_lds_limit<SCHED_HSF>(rows, retry, bytes);
+    case SCHED_ARANDOM: return set_lds_limit<SCHED_ARANDOM>(rows, retry, bytes);
     default: return set_lds_limit<SCHED_AELL>(rows, retry, bytes);
   }
 }
@@ -951,6 +959,7 @@ hipError_t launch_sim_any(int algo, int rows, bool retry, const sk::Params& P, s
     case SCHED_AMAX: return launch_sim<SCHED_AMAX>(rows, retry, P, lds, st);
     case SCHED_AMIN: return launch_sim<SCHED_AMIN>(rows, retry, P, lds, st);
     case SCHED_HSF: return launch_sim<SCHED_HSF>(rows, retry, P, lds, st);
+    case SCHED_ARANDOM: return launch_sim<SCHED_ARANDOM>(rows, retry, P, lds, st);
     default: return launch_sim<SCHED_AELL>(rows, retry, P, lds, st);
   }
 }
@@ -961,7 +970,7 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 extern "C" {
 
-int sched_version(void) { return 110; }
+int sched_version(void) { return 120; }
 
 const char* sched_strerror(int code) {
   switch (code) {
@@ -980,7 +989,7 @@ const char* sched_strerror(int code) {
 int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t M,
                         const sched_results_t* out, void* stream, const sched_options_t* opts) {
   if (!in || !out) return SCHED_E_INVAL;
-  if (algo < SCHED_AMAX || algo > SCHED_ADAPTIVE) return SCHED_E_INVAL;
+  if (algo < SCHED_AMAX || algo > SCHED_ARANDOM) return SCHED_E_INVAL;
   const bool need_l = algo == SCHED_AMIN || algo == SCHED_AELL || algo == SCHED_ADAPTIVE;
   const bool need_u = algo == SCHED_AMAX || algo == SCHED_AELL || algo == SCHED_ADAPTIVE;
   if (M <= 0 || M >= (int64_t(1) << 30)) return SCHED_E_INVAL;
@@ -990,6 +999,7 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   if (in->total_requests > 0 && (!in->prompt || !in->output || !out->completion)) return SCHED_E_INVAL;
   if (in->total_requests > 0 && need_l && !in->lower) return SCHED_E_INVAL;
   if (in->total_requests > 0 && need_u && !in->upper) return SCHED_E_INVAL;
+  if (in->total_requests > 0 && algo == SCHED_ARANDOM && !in->priority) return SCHED_E_INVAL;
   if (in->max_requests >= (1 << sk::kIdxBits)) return SCHED_E_UNSUPPORTED;
   sched_options_t o{};
   if (opts) o = *opts;
@@ -1068,6 +1078,7 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   P.output = in->output;
   P.lower = in->lower;
   P.upper = in->upper;
+  P.priority = in->priority;
   P.completion = out->completion;
   P.evictions = out->evictions;
   P.total_latency = out->total_latency;
@@ -1094,6 +1105,7 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
     case SCHED_AMIN: hipLaunchKernelGGL((sk::k_prepare<SCHED_AMIN>), grid, block, 0, st, P); break;
     case SCHED_HSF: hipLaunchKernelGGL((sk::k_prepare<SCHED_HSF>), grid, block, 0, st, P); break;
     case SCHED_AELL: hipLaunchKernelGGL((sk::k_prepare<SCHED_AELL>), grid, block, 0, st, P); break;
+    case SCHED_ARANDOM: hipLaunchKernelGGL((sk::k_prepare<SCHED_ARANDOM>), grid, block, 0, st, P); break;
     default: hipLaunchKernelGGL((sk::k_prepare<SCHED_ADAPTIVE>), grid, block, 0, st, P); break;
   }
   err = hipGetLastError();

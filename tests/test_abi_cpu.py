@@ -32,15 +32,15 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strerror(lib):
-    assert lib.sched_version() == 110
+    assert lib.sched_version() == 120
     for code in (0, -1, -2, -3, -4, -5, -6, -7):
         assert B.strerror(code) and B.strerror(code) != "unknown code"
     assert B.strerror(12345) == "unknown code"
 
 
-def _inst(K=1, nmax=4, N=4, offsets=1, prompt=1, output=1, lower=1, upper=1):
+def _inst(K=1, nmax=4, N=4, offsets=1, prompt=1, output=1, lower=1, upper=1, priority=1):
     f = lambda v: None if v is None else 0x1000  # non-null dummies; never dereferenced here
-    return B.SchedInstances(K, nmax, N, f(offsets), None, f(prompt), f(output), f(lower), f(upper))
+    return B.SchedInstances(K, nmax, N, f(offsets), None, f(prompt), f(output), f(lower), f(upper), f(priority))
 
 
 def _res(**kw):
@@ -71,7 +71,8 @@ def test_host_validation(lib):
     for algo in (B.AELL, B.ADAPTIVE):  # both bounds are needed
         assert call(lib, _inst(lower=None), algo=algo) == B.E_INVAL
         assert call(lib, _inst(upper=None), algo=algo) == B.E_INVAL
-    assert call(lib, _inst(), algo=5) == B.E_INVAL
+    assert call(lib, _inst(priority=None), algo=B.ARANDOM) == B.E_INVAL
+    assert call(lib, _inst(), algo=6) == B.E_INVAL
     assert call(lib, _inst(), algo=-1) == B.E_INVAL
     assert call(lib, _inst(), res=_res(status=None)) == B.E_INVAL
     assert call(lib, _inst(), res=_res(completion=None)) == B.E_INVAL
