@@ -141,6 +141,26 @@ int sched_simulate_opts(const sched_instances_t* instances, sched_algo_t algo, i
                         const sched_results_t* results, void* stream,
                         const sched_options_t* opts);
 
+/* The hindsight optimum of tiny instances (n_k <= 8): the minimum total
+ * latency (equation (3)) over every non-preemptive schedule that knows the
+ * true outputs and keeps equation (1) (the OPT of the competitive analysis,
+ * Section 2), by exhaustive branch and bound, one GPU lane per instance.
+ * Reads offsets, arrival (NULL = all 0), prompt and output of `instances`
+ * (device pointers; lower, upper and priority are ignored).  upper_bound
+ * (device, [K] or NULL) may give, per instance, the total latency of a known
+ * feasible schedule (e.g. a policy's), which only speeds the search up
+ * (values <= 0 are ignored; a bound that is not achievable gives a wrong
+ * answer, since the search looks only for strictly better schedules).  Writes, per
+ * instance, total_latency[K] and status[K] (SCHED_OK, SCHED_E_ARRIVAL,
+ * SCHED_E_INTERVAL for o < 1 or s < 0, SCHED_E_TOO_BIG for s + o > M,
+ * SCHED_E_INVAL for bad offsets, SCHED_E_STEP_CAP when the search exceeded
+ * node_cap nodes (total_latency then holds the best schedule found, an upper
+ * bound)), and, if nodes is not NULL, nodes[K] searched.  node_cap <= 0
+ * selects 2^22.  Returns SCHED_E_UNSUPPORTED if max_requests > 8 (nothing
+ * queued), SCHED_E_INVAL for NULL pointers or M outside (0, 2^30). */
+int sched_optimum(const sched_instances_t* instances, int64_t M, const int64_t* upper_bound,
+                  int64_t* total_latency, int32_t* status, int64_t* nodes, int64_t node_cap, void* stream);
+
 /* Human-readable text for a return or status code (static storage). */
 const char* sched_strerror(int code);
 

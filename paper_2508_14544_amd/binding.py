@@ -20,7 +20,7 @@ ALGOS = {"amax": AMAX, "amin": AMIN, "hsf": HSF, "aell": AELL, "adaptive": ADAPT
 OK, E_INVAL, E_INTERVAL, E_TOO_BIG, E_STEP_CAP, E_HIP, E_UNSUPPORTED, E_ARRIVAL = 0, -1, -2, -3, -4, -5, -6, -7
 
 # every symbol include/schedsim.h declares
-EXPORTED = ("sched_simulate", "sched_simulate_opts", "sched_strerror", "sched_version")
+EXPORTED = ("sched_optimum", "sched_simulate", "sched_simulate_opts", "sched_strerror", "sched_version")
 
 
 class SchedInstances(ctypes.Structure):
@@ -82,6 +82,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.sched_strerror.argtypes = [ctypes.c_int]
         lib.sched_version.restype = ctypes.c_int
         lib.sched_version.argtypes = []
+        lib.sched_optimum.restype = ctypes.c_int
+        lib.sched_optimum.argtypes = [ctypes.POINTER(SchedInstances), ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
         _lib = lib
     return _lib
 
@@ -177,4 +180,27 @@ def simulate(db: DeviceBatch, algo: int, **kw) -> Dict[str, object]:
     """Allocate outputs, queue the simulation and return the output tensors (not synchronised)."""
     out = alloc_results(db)
     simulate_into(db, algo, out, **kw)
+    return out
+
+
+def optimum(db: DeviceBatch, *, M: Optional[int] = None, node_cap: int = 0, upper_bound=None,
+            stream=None) -> Dict[str, object]:
+    """Queue ``sched_optimum`` (hindsight optimum, instances of at most 8 requests); returns
+    device tensors total_latency, status and nodes (not synchronised).  `upper_bound`: an
+    optional int64 device tensor [K] of achievable totals (e.g. a policy's) to prune with."""
+    import torch
+    lib = load_library()
+    if stream is None:
+        stream = torch.cuda.current_stream(db.output.device)
+    dev = db.output.device
+    K = db.num_instances
+    out = {"tel": torch.empty(K, dtype=torch.int64, device=dev), "status": torch.empty(K, dtype=torch.int32, device=dev),
+           "nodes": torch.empty(K, dtype=torch.int64, device=dev)}
+    inst = SchedInstances(K, db.max_requests, db.total_requests, _ptr(db.offsets), _ptr(db.arrival),
+                          _ptr(db.prompt), _ptr(db.output), None, None, None)
+    code = lib.sched_optimum(ctypes.byref(inst), int(db.M if M is None else M), _ptr(upper_bound), _ptr(out["tel"]),
+                             _ptr(out["status"]), _ptr(out["nodes"]), int(node_cap),
+                             ctypes.c_void_p(stream.cuda_stream))
+    if code != OK:
+        raise SchedError(code)
     return out

@@ -8,7 +8,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libschedsim.so")
-SOURCES = [os.path.join(PKG, "csrc", "sched_kernels.hip")]
+SOURCES = [os.path.join(PKG, "csrc", "sched_kernels.hip"), os.path.join(PKG, "csrc", "opt_kernels.hip")]
 HEADERS = [os.path.join(PKG, "csrc", "wave.hpp"), os.path.join(ROOT, "include", "schedsim.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

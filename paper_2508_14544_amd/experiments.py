@@ -71,6 +71,46 @@ def run(replicates: int = 64, sizes=SIZES, settings=W.EXP_SETTINGS, policies=POL
     return rows, summary
 
 
+def cr_study(num_instances: int = 1 << 18, sizes=(4, 6, 8), seed: int = 0, M: int = 12, o_max: int = 6,
+             alphas=(None, 1, 2), log=None):
+    """Empirical competitive ratios against the hindsight optimum on many tiny
+    instances (all requests at step 0): for each size and interval recipe, the
+    optimum comes from ``sched_optimum`` and each policy's total latency from
+    ``sched_simulate``; reports the largest and the mean ratio per policy."""
+    import torch
+    from fractions import Fraction
+    B.load_library()
+    rows = []
+    gpu_ms_opt = 0.0
+    for n in sizes:
+        for al in alphas:
+            alpha = None if al is None else Fraction(al)
+            batch = W.tiny(seed, num_instances, n, M=M, o_max=o_max, alpha=alpha)
+            db = B.to_device(batch)
+            hsf = B.simulate(db, B.HSF)   # an achievable total: prunes the search
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            opt = B.optimum(db, upper_bound=hsf["tel"])
+            e1.record()
+            torch.cuda.synchronize()
+            gpu_ms_opt += e0.elapsed_time(e1)
+            ot = opt["tel"].cpu().numpy().astype(np.float64)
+            ok = opt["status"].cpu().numpy() == 0
+            for pol in ("amax", "amin", "hsf", "aell", "adaptive"):
+                out = B.simulate(db, B.ALGOS[pol])
+                torch.cuda.synchronize()
+                tel = out["tel"].cpu().numpy().astype(np.float64)
+                good = ok & (out["status"].cpu().numpy() == 0)
+                ratio = tel[good] / ot[good]
+                rows.append({"n": n, "intervals": "random" if al is None else f"geometric alpha={al}",
+                             "policy": pol, "instances": int(good.sum()), "max_ratio": float(ratio.max()),
+                             "mean_ratio": float(ratio.mean()),
+                             "opt_nodes_mean": float(opt["nodes"].cpu().numpy()[ok].mean())})
+                if log:
+                    log(f"n={n} alpha={al} {pol}: max {ratio.max():.4f} mean {ratio.mean():.4f}")
+    return rows, {"opt_gpu_ms": gpu_ms_opt, "opt_instances": num_instances * len(sizes) * len(alphas)}
+
+
 def markdown(rows, policies=POLICIES) -> str:
     out = []
     for setting in W.EXP_SETTINGS:
@@ -95,7 +135,20 @@ def main(argv=None):
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--sizes", default=",".join(map(str, SIZES)))
     ap.add_argument("--json", default="")
+    ap.add_argument("--cr", action="store_true", help="run the competitive-ratio study on tiny instances instead")
+    ap.add_argument("--cr-instances", type=int, default=1 << 18)
     a = ap.parse_args(argv)
+    if a.cr:
+        rows, summary = cr_study(a.cr_instances, seed=a.seed, log=lambda m: print(m, file=sys.stderr, flush=True))
+        print("| n | intervals | policy | instances | max TEL/OPT | mean TEL/OPT |")
+        print("|---|---|---|---|---|---|")
+        for r in rows:
+            print(f"| {r['n']} | {r['intervals']} | {r['policy']} | {r['instances']} | {r['max_ratio']:.4f} | "
+                  f"{r['mean_ratio']:.4f} |")
+        print(json.dumps(summary))
+        if a.json:
+            json.dump({"rows": rows, "summary": summary}, open(a.json, "w"), indent=1)
+        return
     sizes = tuple(int(x) for x in a.sizes.split(","))
     t0 = time.perf_counter()
     rows, summary = run(a.replicates, sizes=sizes, seed=a.seed,

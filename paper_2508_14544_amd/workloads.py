@@ -428,3 +428,25 @@ def with_random_order(batch: Instances, seed: int = 0) -> Instances:
         r = raw64(seed, 200, 0, np.array([batch.instance_ids[k]], np.int64), e - b)[0]
         pr[b:e] = np.argsort(np.argsort(r, kind="stable"), kind="stable").astype(np.int32)
     return dataclasses.replace(batch, priority=pr)
+
+
+def tiny(seed: int, num_instances: int, n: int, *, s_max: int = 3, o_max: int = 6, M: int = 12,
+         alpha: Optional[Fraction] = None) -> Instances:
+    """Many small instances of exactly n requests at step 0 (vectorised), for
+    empirical competitive ratios against the hindsight optimum: s ~ U{0..s_max},
+    o ~ U{1..o_max}, interval [l, u] = the geometric bin of o for `alpha`
+    (default: l = max(1, o - U{0..o_max}), u = o + U{0..o_max}), s lowered so
+    that s + u <= M."""
+    ids = np.arange(num_instances, dtype=np.int64)
+    wid = 101
+    o = uniform_int(raw64(seed, wid, F_OUTPUT, ids, n), 1, o_max)
+    if alpha is None:
+        l = np.maximum(1, o - uniform_int(raw64(seed, wid, F_U1, ids, n), 0, o_max))
+        u = o + uniform_int(raw64(seed, wid, F_U2, ids, n), 0, o_max)
+    else:
+        l, u = _bins_for(alpha, o, o_max)
+    s = np.minimum(uniform_int(raw64(seed, wid, F_PROMPT, ids, n), 0, s_max), np.maximum(0, M - u))
+    offsets = np.arange(num_instances + 1, dtype=np.int64) * n
+    c32 = lambda v: np.ascontiguousarray(v.reshape(-1), dtype=np.int32)
+    return Instances(f"tiny_n{n}", M, offsets, c32(np.zeros_like(o)), c32(s), c32(o), c32(l), c32(u), ids,
+                     {"seed": seed})

@@ -1,0 +1,83 @@
+"""The hindsight optimum of tiny instances on the GPU (sched_optimum) against
+the oracle's exhaustive search, and the paper's printed OPT values."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2508_14544_amd import workloads as W
+from test_gpu_parity import B  # noqa: F401 (fixture)
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_opt(B, batch, **kw):
+    import torch
+    db = B.to_device(batch)
+    out = B.optimum(db, **kw)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def test_paper_examples_opt(B):
+    here = os.path.join(os.path.dirname(__file__), "golden")
+    n_checked = 0
+    for f in sorted(x for x in os.listdir(here) if x.endswith(".json")):
+        g = json.load(open(os.path.join(here, f)))
+        if "instance" in g and "opt_tel" in g:
+            batch = W.from_lists(g["M"], [g["instance"]], name=f)
+            r = gpu_opt(B, batch)
+            assert int(r["status"][0]) == 0 and int(r["tel"][0]) == g["opt_tel"], f
+            n_checked += 1
+    assert n_checked >= 2
+
+
+@pytest.mark.parametrize("seed,arrivals", [(0, False), (1, True), (2, False)])
+def test_random_tiny_against_oracle(B, seed, arrivals):
+    b = W.random_small(seed + 40, 30, 6, s_max=3, o_max=5, M=12, arrivals=arrivals)
+    r = gpu_opt(B, b)
+    assert (r["status"] == 0).all()
+    ref = [O.opt_tel(b.instance(k), b.M) for k in range(b.num_instances)]
+    assert r["tel"].tolist() == ref
+    # OPT is a lower bound of every policy (per instance); a policy's total as
+    # the starting bound gives the same optimum
+    import torch
+    for algo in (O.AMAX, O.AMIN, O.HSF):
+        tel = O.simulate_batch(b, algo)["tel"]
+        assert (r["tel"] <= tel).all()
+        rb = gpu_opt(B, b, upper_bound=torch.from_numpy(tel).cuda())
+        assert rb["tel"].tolist() == ref
+
+
+def test_closed_forms(B):
+    from test_oracle_pins import spt_single_machine_tel
+    rng = np.random.default_rng(11)
+    excl, roomy = [], []
+    for _ in range(200):
+        n = int(rng.integers(1, 9))
+        o = rng.integers(1, 8, n).tolist()
+        excl.append({"prompt": rng.integers(11, 14, n).tolist(), "output": o})
+        roomy.append({"prompt": rng.integers(0, 3, n).tolist(), "output": o})
+    r = gpu_opt(B, W.from_lists(20, excl, name="opt_exclusive"))
+    assert (r["status"] == 0).all()
+    assert r["tel"].tolist() == [spt_single_machine_tel(i["output"]) for i in excl]
+    r = gpu_opt(B, W.from_lists(16 + 7 * 8, roomy, name="opt_roomy"))
+    assert (r["status"] == 0).all()
+    assert r["tel"].tolist() == [sum(i["output"]) for i in roomy]
+
+
+def test_statuses_and_node_cap(B):
+    good = {"arrival": [0, 0, 1], "prompt": [1, 2, 1], "output": [3, 2, 4]}
+    insts = [good, dict(good, arrival=[1, 0, 1]), dict(good, output=[0, 2, 4]), dict(good, prompt=[1, 2, 9]),
+             {"arrival": [], "prompt": [], "output": []}]
+    r = gpu_opt(B, W.from_lists(10, insts, name="opt_status"))
+    assert r["status"].tolist() == [0, O.E_ARRIVAL, O.E_INTERVAL, O.E_TOO_BIG, 0]
+    assert r["tel"][0] == O.opt_tel(good, 10) and r["tel"][4] == 0
+    b = W.random_small(3, 20, 8, s_max=2, o_max=8, M=14, arrivals=False)
+    capped = gpu_opt(B, b, node_cap=5)
+    full = gpu_opt(B, b)
+    hit = capped["status"] == O.E_STEP_CAP
+    assert hit.any()
+    assert (capped["tel"][hit] >= full["tel"][hit]).all()   # an upper bound when the search was cut

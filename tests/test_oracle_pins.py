@@ -145,6 +145,32 @@ def test_opt_is_a_lower_bound(seed):
             assert opt <= O.simulate(inst, algo, b.M)["tel"]
 
 
+def spt_single_machine_tel(o):
+    """Sum of completion times when runs cannot overlap: a run of output o
+    occupies o + 1 steps and shortest-first sequencing is optimal (Smith's
+    rule); the j-th run in ascending o completes at sum_{k<=j}(o_k + 1) - 1."""
+    t, total = 0, 0
+    for x in sorted(int(v) for v in o):
+        total += t + x
+        t += x + 1
+    return total
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_opt_closed_forms(seed):
+    rng = np.random.default_rng(seed)
+    for _ in range(15):
+        n = int(rng.integers(1, 6))
+        o = rng.integers(1, 8, n)
+        # two prompts together exceed M: no two runs ever overlap
+        M = 20
+        inst = {"prompt": rng.integers(11, 14, n), "output": o}
+        assert O.opt_tel(inst, M) == spt_single_machine_tel(o)
+        # room for every run at once: each completes at o
+        inst = {"prompt": rng.integers(0, 5, n), "output": o}
+        assert O.opt_tel(inst, int(sum(inst["prompt"]) + sum(o))) == int(sum(o))
+
+
 def test_reduction_exact_predictions_all_equal():
     from fractions import Fraction
     b = W.random_small(7, 100, 10, s_max=6, o_max=10, M=30, alpha=Fraction(0))
