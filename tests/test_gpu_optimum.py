@@ -58,9 +58,11 @@ def test_closed_forms(B):
     for _ in range(200):
         n = int(rng.integers(1, 9))
         o = rng.integers(1, 8, n).tolist()
-        excl.append({"prompt": rng.integers(11, 14, n).tolist(), "output": o})
+        # runs that never overlap leave the search only its weak bound (sum of
+        # o): every order is explored, so keep these to n <= 6
+        excl.append({"prompt": rng.integers(11, 14, min(n, 6)).tolist(), "output": o[:6]})
         roomy.append({"prompt": rng.integers(0, 3, n).tolist(), "output": o})
-    r = gpu_opt(B, W.from_lists(20, excl, name="opt_exclusive"))
+    r = gpu_opt(B, W.from_lists(20, excl, name="opt_exclusive"), node_cap=1 << 26)
     assert (r["status"] == 0).all()
     assert r["tel"].tolist() == [spt_single_machine_tel(i["output"]) for i in excl]
     r = gpu_opt(B, W.from_lists(16 + 7 * 8, roomy, name="opt_roomy"))
