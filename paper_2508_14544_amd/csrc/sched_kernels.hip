@@ -259,6 +259,9 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
 // Internal status of a first pass whose running set outgrew its register rows;
 // the retry pass (more rows) re-runs exactly those instances.
 constexpr int kRetry = -100;
+// Internal status of a body whose running set outgrew its rows when the same
+// wave re-runs the instance at once with a wider body.
+constexpr int kRetryInWave = -101;
 // r_end of an empty slot of the running set (below every planned end)
 constexpr int32_t kEmpty = INT32_MIN;
 // r_c of an empty slot (after every step)
@@ -274,17 +277,13 @@ __device__ __forceinline__ uint32_t uniform_u32(uint32_t v) {
   return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int32_t>(v)));
 }
 
-template <int ALGO, int ROWS, bool RETRY_PASS>
-__global__ __launch_bounds__(64) void k_simulate(Params P) {
+// Simulates instance k (whose validation status is st0) with ROWS register
+// rows and writes its outputs; a running set that outgrows the rows ends the
+// simulation with `retry_status` (the per-request outputs are then reset).
+template <int ALGO, int ROWS>
+__device__ __forceinline__ int sim_instance(const Params& P, const int k, const int st0, const int retry_status) {
   extern __shared__ uint64_t lds64[];
-  const int k = blockIdx.x;
   const int lane = threadIdx.x;
-  if (P.algo_of && P.algo_of[k] != ALGO) return;  // adaptive run: the other policy's instance
-  int st0 = P.status[k];
-  if (RETRY_PASS) {
-    if (st0 != kRetry) return;
-    st0 = SCHED_OK;
-  }
   const int64_t b = P.offsets[k];
   const int n = (st0 == SCHED_OK) ? static_cast<int>(P.offsets[k + 1] - b) : 0;
   const int32_t M = P.M;
@@ -771,7 +770,7 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
             mm = m ? m : mm;
           }
           if (rr < 0) {
-            status = P.retry_status;
+            status = retry_status;
             break;
           }
           fr_row = rr;
@@ -890,6 +889,35 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
     if (P.total_evictions) P.total_evictions[k] = tot_ev;
     P.status[k] = status;
   }
+  return status;
+}
+
+// One wave per instance.  RETRY_PASS: only instances handed over by an
+// earlier launch (status kRetry) run.
+template <int ALGO, int ROWS, bool RETRY_PASS>
+__global__ __launch_bounds__(64) void k_simulate(Params P) {
+  const int k = blockIdx.x;
+  if (P.algo_of && P.algo_of[k] != ALGO) return;  // adaptive run: the other policy's instance
+  int st0 = P.status[k];
+  if (RETRY_PASS) {
+    if (st0 != kRetry) return;
+    st0 = SCHED_OK;
+  }
+  sim_instance<ALGO, ROWS>(P, k, st0, P.retry_status);
+}
+
+// One wave per instance with 6 rows; an instance whose running set outgrows
+// them is simulated again at once by the same wave with 8 rows (its outputs
+// were reset; the fence orders that reset before the new run's writes and
+// atomics).  Held to 128 VGPRs so that four waves share a SIMD.
+template <int ALGO>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_simulate_6_8(Params P) {
+  const int k = blockIdx.x;
+  if (P.algo_of && P.algo_of[k] != ALGO) return;
+  if (sim_instance<ALGO, 6>(P, k, P.status[k], kRetryInWave) == kRetryInWave) {
+    __threadfence();
+    sim_instance<ALGO, 8>(P, k, SCHED_OK, P.retry_status);
+  }
 }
 #undef SK_LOAD_ARRIVALS
 #undef SK_PICK
@@ -908,14 +936,16 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
 // ---------------------------------------------------------------------------
 namespace {
 
-// Row counts of the register running set: a first pass, then retry passes
-// (RETRY_PASS kernels) for the instances whose running set outgrew it.
+// Kernel variants by register rows.  First launch: `rows`, and with rows2 > 0
+// an in-wave re-run with rows2 rows for instances that outgrow `rows`.  Retry
+// launch (retry = true): the instances an earlier launch handed over.
 template <int ALGO>
-const void* sim_kernel(int rows, bool retry) {
-  if (retry) {
+const void* sim_kernel(int rows, int rows2, bool retry) {
+  if (retry)
     return rows <= 8 ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, true>)
                      : reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true>);
-  }
+  if constexpr (ALGO != SCHED_AELL && ALGO != SCHED_AMIN)
+    if (rows2 > 0) return reinterpret_cast<const void*>(&sk::k_simulate_6_8<ALGO>);
   switch (rows) {
     case 1: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 1, false>);
     case 2: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 2, false>);
@@ -932,35 +962,41 @@ int rows_for(int64_t want) {
   return r <= 1 ? 1 : r <= 2 ? 2 : r <= 4 ? 4 : r <= 6 ? 6 : r <= 8 ? 8 : 16;
 }
 
+struct Tier {
+  int rows, rows2;
+  bool retry;
+};
+
 template <int ALGO>
-hipError_t launch_sim(int rows, bool retry, const sk::Params& P, size_t lds, hipStream_t st) {
+hipError_t launch_sim(const Tier& tr, const sk::Params& P, size_t lds, hipStream_t st) {
   sk::Params p = P;
   void* args[] = {&p};
-  return hipLaunchKernel(sim_kernel<ALGO>(rows, retry), dim3(P.K), dim3(64), args, lds, st);
+  return hipLaunchKernel(sim_kernel<ALGO>(tr.rows, tr.rows2, tr.retry), dim3(P.K), dim3(64), args, lds, st);
 }
 
 template <int ALGO>
-hipError_t set_lds_limit(int rows, bool retry, int bytes) {
-  return hipFuncSetAttribute(sim_kernel<ALGO>(rows, retry), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+hipError_t set_lds_limit(const Tier& tr, int bytes) {
+  return hipFuncSetAttribute(sim_kernel<ALGO>(tr.rows, tr.rows2, tr.retry),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
 }
 
-hipError_t set_lds_limit_any(int algo, int rows, bool retry, int bytes) {
+hipError_t set_lds_limit_any(int algo, const Tier& tr, int bytes) {
   switch (algo) {
-    case SCHED_AMAX: return set_lds_limit<SCHED_AMAX>(rows, retry, bytes);
-    case SCHED_AMIN: return set_lds_limit<SCHED_AMIN>(rows, retry, bytes);
-    case SCHED_HSF: return set_lds_limit<SCHED_HSF>(rows, retry, bytes);
-    case SCHED_ARANDOM: return set_lds_limit<SCHED_ARANDOM>(rows, retry, bytes);
-    default: return set_lds_limit<SCHED_AELL>(rows, retry, bytes);
+    case SCHED_AMAX: return set_lds_limit<SCHED_AMAX>(tr, bytes);
+    case SCHED_AMIN: return set_lds_limit<SCHED_AMIN>(tr, bytes);
+    case SCHED_HSF: return set_lds_limit<SCHED_HSF>(tr, bytes);
+    case SCHED_ARANDOM: return set_lds_limit<SCHED_ARANDOM>(tr, bytes);
+    default: return set_lds_limit<SCHED_AELL>(tr, bytes);
   }
 }
 
-hipError_t launch_sim_any(int algo, int rows, bool retry, const sk::Params& P, size_t lds, hipStream_t st) {
+hipError_t launch_sim_any(int algo, const Tier& tr, const sk::Params& P, size_t lds, hipStream_t st) {
   switch (algo) {
-    case SCHED_AMAX: return launch_sim<SCHED_AMAX>(rows, retry, P, lds, st);
-    case SCHED_AMIN: return launch_sim<SCHED_AMIN>(rows, retry, P, lds, st);
-    case SCHED_HSF: return launch_sim<SCHED_HSF>(rows, retry, P, lds, st);
-    case SCHED_ARANDOM: return launch_sim<SCHED_ARANDOM>(rows, retry, P, lds, st);
-    default: return launch_sim<SCHED_AELL>(rows, retry, P, lds, st);
+    case SCHED_AMAX: return launch_sim<SCHED_AMAX>(tr, P, lds, st);
+    case SCHED_AMIN: return launch_sim<SCHED_AMIN>(tr, P, lds, st);
+    case SCHED_HSF: return launch_sim<SCHED_HSF>(tr, P, lds, st);
+    case SCHED_ARANDOM: return launch_sim<SCHED_ARANDOM>(tr, P, lds, st);
+    default: return launch_sim<SCHED_AELL>(tr, P, lds, st);
   }
 }
 
@@ -970,7 +1006,7 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 extern "C" {
 
-int sched_version(void) { return 120; }
+int sched_version(void) { return 121; }
 
 const char* sched_strerror(int code) {
   switch (code) {
@@ -1009,17 +1045,33 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   const int64_t nmax = in->max_requests;
   if (o.running_capacity > 1024) return SCHED_E_UNSUPPORTED;
   const bool forced = o.running_capacity > 0;
-  // passes: the first covers up to 384 runs (every run of most instances);
-  // instances whose running set outgrows it are simulated again with 8, then 16 rows
-  int tiers[3] = {0, 0, 0};
-  int n_tiers = 1;
-  if (forced) {
-    tiers[0] = rows_for(o.running_capacity);
-  } else {
-    tiers[0] = rows_for(std::min<int64_t>(std::max<int64_t>(nmax, 1), 384));
-    if (nmax > 384) tiers[n_tiers++] = 8;
-    if (nmax > 512) tiers[n_tiers++] = 16;
-  }
+  // launches per policy.  The first covers up to 384 runs (every run of most
+  // instances); an instance that outgrows them is simulated again with 512,
+  // then with 1024.  A_max, H-SF and A_random re-run it at once in the same
+  // wave; A_l, whose 6-row kernel already needs the registers of four waves
+  // per SIMD, starts with 512; A_min (whose combined kernel spills more
+  // scalar registers) hands it to a retry launch.
+  auto tiers_for = [&](int a, Tier* out) -> int {
+    if (forced) {
+      out[0] = Tier{rows_for(o.running_capacity), 0, false};
+      return 1;
+    }
+    if (nmax <= 384) {
+      out[0] = Tier{rows_for(std::max<int64_t>(nmax, 1)), 0, false};
+      return 1;
+    }
+    int m = 0;
+    if (a == SCHED_AELL) {
+      out[m++] = Tier{8, 0, false};
+    } else if (a == SCHED_AMIN) {
+      out[m++] = Tier{6, 0, false};
+      out[m++] = Tier{8, 0, true};
+    } else {
+      out[m++] = Tier{6, 8, false};
+    }
+    if (nmax > 512) out[m++] = Tier{16, 0, true};
+    return m;
+  };
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   int dev = 0;
@@ -1111,16 +1163,20 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   err = hipGetLastError();
   for (int a = 0; a < n_sim && err == hipSuccess; ++a) {
     const size_t lds = lds_for(sim_algos[a]);
+    Tier tiers[3];
+    const int n_tiers = tiers_for(sim_algos[a], tiers);
     for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass)
-      if (lds > 65536) err = set_lds_limit_any(sim_algos[a], tiers[pass], pass > 0, static_cast<int>(lds));
+      if (lds > 65536) err = set_lds_limit_any(sim_algos[a], tiers[pass], static_cast<int>(lds));
   }
   if (err == hipSuccess && o.event_before) err = hipEventRecord(static_cast<hipEvent_t>(o.event_before), st);
   for (int a = 0; a < n_sim && err == hipSuccess; ++a) {
     P.cap_v = cap_v_for(sim_algos[a]);
     const size_t lds = lds_for(sim_algos[a]);
+    Tier tiers[3];
+    const int n_tiers = tiers_for(sim_algos[a], tiers);
     for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass) {
       P.retry_status = pass + 1 < n_tiers ? sk::kRetry : SCHED_E_UNSUPPORTED;
-      err = launch_sim_any(sim_algos[a], tiers[pass], pass > 0, P, lds, st);
+      err = launch_sim_any(sim_algos[a], tiers[pass], P, lds, st);
     }
   }
   if (err == hipSuccess && o.event_after) err = hipEventRecord(static_cast<hipEvent_t>(o.event_after), st);

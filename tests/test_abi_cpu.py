@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strerror(lib):
-    assert lib.sched_version() == 120
+    assert lib.sched_version() == 121
     for code in (0, -1, -2, -3, -4, -5, -6, -7):
         assert B.strerror(code) and B.strerror(code) != "unknown code"
     assert B.strerror(12345) == "unknown code"
