@@ -289,7 +289,8 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
   const int32_t M = P.M;
 
   int status = st0;
-  int64_t rsteps = 0, tot_ev = 0;
+  // counters live in vector registers (see wave::in_vgpr)
+  int64_t rsteps = wave::in_vgpr<int64_t>(0), tot_ev = wave::in_vgpr<int64_t>(0);
 
   if (st0 == SCHED_OK && n > 0) {
     uint64_t* L0 = lds64;
@@ -305,12 +306,15 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     __syncthreads();
 
     const int32_t cap = P.cap[k];
-    const uint2* rec = P.rec + b;
-    const int32_t* arrival = P.arrival ? P.arrival + b : nullptr;
-    const int32_t* rank_of = P.rank_of + b;
+    // array bases in vector registers, except for A_l, whose extra register
+    // row leaves no room for them within four waves per SIMD
+    auto base = [](auto* p) { return ALGO == SCHED_AELL ? p : wave::in_vgpr(p); };
+    const uint2* rec = base(P.rec + b);
+    const int32_t* arrival = P.arrival ? base(P.arrival + b) : nullptr;
+    const int32_t* rank_of = base(P.rank_of + b);
     const int32_t* upper_k = ALGO == SCHED_AELL ? P.upper + b : nullptr;
-    int32_t* completion = P.completion + b;
-    int32_t* evictions = P.evictions ? P.evictions + b : nullptr;
+    int32_t* completion = base(P.completion + b);
+    int32_t* evictions = P.evictions ? base(P.evictions + b) : nullptr;
 
     // running set: register rows; an empty slot has r_end = kEmpty, r_c = kNever,
     // r_key = ~0, which every scan below treats as neutral, so scans cover all rows
@@ -337,10 +341,6 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     uint32_t v_key = 0xFFFFFFFFu, v_so = 0;
     int32_t v_u = 0;
     int32_t n_done = 0;
-    // cached head of the waiting set (smaller key of the two heads)
-    bool c_any = false, c_fromF = false;
-    uint32_t c_key = 0;
-    int32_t c_est = 0, c_s = 0, c_o = 0, c_u = 0;
     // the head cannot start before retry_at; valid until the next event
     int32_t retry_at = 0;
 
@@ -442,18 +442,17 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     }                                                                                \
   } while (0)
     // the head of the waiting set: smaller key of the fresh and cancelled heads
-    // (A_l: every fresh request comes before the promoted ones)
+    // (A_l: every fresh request comes before the promoted ones); derived where
+    // it is used rather than carried through the loop
 #define SK_PICK()                                                                    \
-  do {                                                                               \
-    c_any = f_rank >= 0 || v_pos >= 0;                                               \
-    c_fromF = f_rank >= 0 && (ALGO == SCHED_AELL || f_key < v_key);                  \
-    c_key = c_fromF ? f_key : v_key;                                                 \
-    const uint32_t so_ = c_fromF ? f_so : v_so;                                      \
-    c_s = static_cast<int32_t>(so_ & 0xFFFFu);                                       \
-    c_o = static_cast<int32_t>(so_ >> 16);                                           \
-    c_est = ALGO == SCHED_ARANDOM ? c_o : static_cast<int32_t>(c_key >> kIdxBits);   \
-    c_u = c_fromF ? f_u : v_u;                                                       \
-  } while (0)
+  const bool c_any = f_rank >= 0 || v_pos >= 0;                                      \
+  const bool c_fromF = f_rank >= 0 && (ALGO == SCHED_AELL || f_key < v_key);         \
+  const uint32_t c_key = c_fromF ? f_key : v_key;                                    \
+  const uint32_t c_so = c_fromF ? f_so : v_so;                                       \
+  const int32_t c_s = static_cast<int32_t>(c_so & 0xFFFFu);                          \
+  const int32_t c_o = static_cast<int32_t>(c_so >> 16);                              \
+  const int32_t c_est = ALGO == SCHED_ARANDOM ? c_o : static_cast<int32_t>(c_key >> kIdxBits); \
+  const int32_t c_u = c_fromF ? f_u : v_u;
     // BODY with the compile-time row index r equal to the uniform row RR_
 #define SK_AT_ROW(RR_, BODY)                                                         \
   _Pragma("unroll") for (int r = 0; r < ROWS; ++r) {                                 \
@@ -523,10 +522,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
         SK_V_MERGE();
         heads_changed = true;
       }
-      if (heads_changed) {
-        SK_PICK();
-        event = true;
-      }
+      if (heads_changed) event = true;
 
       // ---- 2. completions at t; DT = memory they still hold at t (s + o each)
       int32_t DT = 0;
@@ -616,10 +612,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
           if (status != SCHED_OK) break;
           if (promoted) {
             event = true;
-            if (v_pos < 0) {
-              SK_V_HEAD();
-              SK_PICK();
-            }
+            if (v_pos < 0) SK_V_HEAD();
           }
         }
         // next event: a completion (A_l: or a planned end, where a run is promoted);
@@ -691,7 +684,9 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       // ---- 5. admission of the longest feasible prefix in key order
       bool stuck = true;          // the head cannot start before the next event
       int32_t wait_until = t + 1; // otherwise: not before this step
-      while (c_any) {
+      for (;;) {
+        SK_PICK();
+        if (!c_any) break;
         const int32_t s = c_s, est = c_est;
         const int32_t E = t + est;
         const int32_t tp1 = t + 1;
@@ -814,7 +809,6 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
           --nV;
           SK_V_FIND();
         }
-        SK_PICK();
         stuck = true;
         wait_until = t + 1;
         retry_at = 0;

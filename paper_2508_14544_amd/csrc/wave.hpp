@@ -49,6 +49,16 @@ __device__ __forceinline__ uint32_t writelane_u(uint32_t v, uint32_t s, int lane
 
 __device__ __forceinline__ int32_t uniform(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// The same value, held in vector registers: the compiler treats the result
+// as varying per lane.  For wave-uniform state that is used rarely (array
+// base addresses, counters), so that it does not take scalar registers
+// through the hot loops; loads and stores take vector addresses anyway.
+template <typename T>
+__device__ __forceinline__ T in_vgpr(T v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 template <int CTRL>
 __device__ __forceinline__ int32_t dpp(int32_t v) {
   return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
