@@ -23,6 +23,7 @@ sys.path.insert(0, ROOT)
 
 # MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = int32 VALU lane-operations per second
 PEAK_INT32_LANE_OPS = 256 * 4 * 16 * 2.4e9
+PEAK_LDS_BYTES = 256 * 128 * 2.4e9
 # algorithmic int32 lane-operations per simulated request-step ("Roofline")
 OPS_PER_REQUEST_STEP = 6
 METRIC = "simulated request-steps/sec (A_min, 4096×n=1000) + % VALU/LDS roofline"
@@ -50,6 +51,25 @@ def load_traffic(workload: str, algo: str):
     if d.get("kernel_source_hash") != kernel_source_hash():
         return None
     return d.get("hbm_bytes_per_launch")
+
+
+def probe_peaks():
+    """The int32 VALU and LDS throughput this GPU delivers, from the probe
+    kernels of libschedprobe.so (next to the published peaks the roofline
+    uses); None if the probe library is not built."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2508_14544_amd", "libschedprobe.so")
+    if not os.path.exists(path):
+        return None
+    lib = ctypes.CDLL(path)
+    for f in (lib.sched_probe_valu, lib.sched_probe_lds):
+        f.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+        f.restype = ctypes.c_int
+    v, l = ctypes.c_double(0), ctypes.c_double(0)
+    if lib.sched_probe_valu(4000, ctypes.byref(v)) != 0 or lib.sched_probe_lds(20000, ctypes.byref(l)) != 0:
+        return None
+    return {"int32_valu_TOPs": v.value / 1e12, "int32_valu_frac_of_published": v.value / PEAK_INT32_LANE_OPS,
+            "lds_read_TBs": l.value / 1e12, "lds_frac_of_published": l.value / PEAK_LDS_BYTES}
 
 
 class HipEvent:
@@ -129,6 +149,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-peak-probe", action="store_true", help="skip the VALU/LDS throughput probes")
     ap.add_argument("--instances", default="",
                     help="comma-separated instance ids: simulate only these (critical-path profiling)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -204,6 +225,7 @@ def main():
 
     achieved = OPS_PER_REQUEST_STEP * rs / (sim_avg_ms / 1e3)
     traffic = load_traffic(args.workload, args.algo)
+    measured_peaks = None if args.no_peak_probe else probe_peaks()
     result = {
         "metric": METRIC,
         "value": value,
@@ -245,6 +267,7 @@ def main():
             "kernel_ms": sim_avg_ms,
             "kernel_ms_median": float(np.median(sim_ms)),
             "ops_per_request_step": OPS_PER_REQUEST_STEP,
+            "measured_peaks": measured_peaks,
         },
         "transfers": {
             "note": "torch copies from/to pageable host memory, including allocation",

@@ -10,6 +10,9 @@ ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libschedsim.so")
 SOURCES = [os.path.join(PKG, "csrc", "sched_kernels.hip"), os.path.join(PKG, "csrc", "opt_kernels.hip")]
 HEADERS = [os.path.join(PKG, "csrc", "wave.hpp"), os.path.join(ROOT, "include", "schedsim.h")]
+# throughput probes for the roofline (measurement infrastructure, own library)
+PROBE_LIB = os.path.join(PKG, "libschedprobe.so")
+PROBE_SOURCES = [os.path.join(PKG, "csrc", "probe_kernels.hip")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -20,14 +23,19 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = True, extra=()) -> str:
-    """Compile every HIP source into libschedsim.so (always recompiles)."""
-    tmp = LIB + f".tmp{os.getpid()}"
-    cmd = [HIPCC, *FLAGS, *extra, *SOURCES, "-o", tmp]
+def _compile(sources, lib, verbose, extra):
+    tmp = lib + f".tmp{os.getpid()}"
+    cmd = [HIPCC, *FLAGS, *extra, *sources, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = True, extra=()) -> str:
+    """Compile libschedsim.so and libschedprobe.so (always recompiles)."""
+    _compile(SOURCES, LIB, verbose, extra)
+    _compile(PROBE_SOURCES, PROBE_LIB, verbose, extra)
     return LIB
 
 

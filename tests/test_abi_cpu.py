@@ -31,6 +31,21 @@ def test_exports_every_declared_symbol(lib):
         assert hasattr(lib, nm)
 
 
+def test_probe_library_exports_every_declared_symbol(lib):
+    # the throughput probes (include/schedprobe.h) live in their own library
+    txt = open(os.path.join(ROOT, "include", "schedprobe.h")).read()
+    names = sorted(set(re.findall(r"^int\s+(sched_probe_\w+)\s*\(", txt, re.M)))
+    assert names == ["sched_probe_lds", "sched_probe_valu"]
+    probe = ctypes.CDLL(os.path.join(ROOT, "paper_2508_14544_amd", "libschedprobe.so"))
+    for nm in names:
+        assert hasattr(probe, nm)
+        f = getattr(probe, nm)
+        f.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+        out = ctypes.c_double(0)
+        assert f(0, ctypes.byref(out)) == -1          # rejected before any GPU call
+        assert f(10, None) == -1
+
+
 def test_version_and_strerror(lib):
     assert lib.sched_version() == 121
     for code in (0, -1, -2, -3, -4, -5, -6, -7):
