@@ -308,7 +308,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     const int32_t cap = P.cap[k];
     // array bases in vector registers, except for A_l, whose extra register
     // row leaves no room for them within four waves per SIMD
-    auto base = [](auto* p) { return ALGO == SCHED_AELL ? p : wave::in_vgpr(p); };
+    auto base = [](auto* p) { return wave::in_vgpr(p); };
     const uint2* rec = base(P.rec + b);
     const int32_t* arrival = P.arrival ? base(P.arrival + b) : nullptr;
     const int32_t* rank_of = base(P.rank_of + b);
@@ -717,33 +717,36 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
           hmx = hv > hmx ? hv : hmx;
           fl += e >= E ? r_x[r] + cE : 0;
         }
-        if (wave::ballot(hmx > lim)) {
-          // each violating end improves by one per step, or leaves the window
-          int32_t fix = 0;
+        // both conditions in one ballot: the sum is left in every lane, so the
+        // passing case costs a single vector-to-scalar hand-off
+        const int32_t fv = wave::sum_i32_all(fl);
+        const bool end_bad = win && fv + s + est > M;
+        if (wave::ballot(hmx > lim || end_bad)) {
+          if (wave::ballot(hmx > lim)) {
+            // each violating end improves by one per step, or leaves the window
+            int32_t fix = 0;
 #pragma unroll
-          for (int r = 0; r < ROWS; ++r) {
-            const int32_t a = r_h[r] - lim, bb = r_end[r] - 1 - t;
-            const int32_t m = a < bb ? a : bb;
-            const bool in = static_cast<uint32_t>(r_end[r]) - lo2 <= span;
-            fix = (in && r_h[r] > lim && m > fix) ? m : fix;
+            for (int r = 0; r < ROWS; ++r) {
+              const int32_t a = r_h[r] - lim, bb = r_end[r] - 1 - t;
+              const int32_t m = a < bb ? a : bb;
+              const bool in = static_cast<uint32_t>(r_end[r]) - lo2 <= span;
+              fix = (in && r_h[r] > lim && m > fix) ? m : fix;
+            }
+            retry_at = t + wave::max_i32(fix);
+          } else {
+            // f at the sliding end only grows until it passes the next planned end
+            int32_t emin = kNever;
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+              const int32_t e = r_end[r];
+              emin = (e >= E && e < emin) ? e : emin;
+            }
+            retry_at = static_cast<int32_t>(wave::min_u32(static_cast<uint32_t>(emin))) - est + 1;
           }
-          retry_at = t + wave::max_i32(fix);
           wait_until = retry_at;
           break;
         }
-        const int32_t f = wave::sum_i32(fl);
-        if (win && f + s + est > M) {
-          // f at the sliding end only grows until it passes the next planned end
-          int32_t emin = kNever;
-#pragma unroll
-          for (int r = 0; r < ROWS; ++r) {
-            const int32_t e = r_end[r];
-            emin = (e >= E && e < emin) ? e : emin;
-          }
-          retry_at = static_cast<int32_t>(wave::min_u32(static_cast<uint32_t>(emin))) - est + 1;
-          wait_until = retry_at;
-          break;
-        }
+        const int32_t f = wave::uniform(fv);
         // admit: start at p = t; runs whose planned end is in (t+1, E] gain its share
         const int32_t xw = s - t + t_r;
         const int32_t hw = f + (xw + cE) + cE;
@@ -938,7 +941,7 @@ const void* sim_kernel(int rows, int rows2, bool retry) {
   if (retry)
     return rows <= 8 ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, true>)
                      : reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true>);
-  if constexpr (ALGO != SCHED_AELL && ALGO != SCHED_AMIN)
+  if constexpr (ALGO != SCHED_AELL)
     if (rows2 > 0) return reinterpret_cast<const void*>(&sk::k_simulate_6_8<ALGO>);
   switch (rows) {
     case 1: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 1, false>);
@@ -1057,9 +1060,6 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
     int m = 0;
     if (a == SCHED_AELL) {
       out[m++] = Tier{8, 0, false};
-    } else if (a == SCHED_AMIN) {
-      out[m++] = Tier{6, 0, false};
-      out[m++] = Tier{8, 0, true};
     } else {
       out[m++] = Tier{6, 8, false};
     }

@@ -106,6 +106,12 @@ __device__ __forceinline__ int32_t sum_i32(int32_t v) {
   return uniform(static_cast<int32_t>(r));
 }
 
+// The sum left in every lane (a vector value): for tests that combine it with
+// other per-lane conditions before a single ballot.
+__device__ __forceinline__ int32_t sum_i32_all(int32_t v) {
+  return static_cast<int32_t>(fold_in_row(fold_rows(static_cast<uint32_t>(v), OpAddU32{}), OpAddU32{}));
+}
+
 __device__ __forceinline__ uint32_t min_u32(uint32_t v) {
   const uint32_t r = fold_in_row(fold_rows(v, OpMinU32{}), OpMinU32{});
   return static_cast<uint32_t>(uniform(static_cast<int32_t>(r)));
