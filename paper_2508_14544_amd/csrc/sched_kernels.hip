@@ -402,11 +402,13 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
 #define SK_V_FIND()                                                                  \
   do {                                                                               \
     SK_V_SCAN(0, nVe)                                                                \
-    const uint32_t km_ = wave::min_u32(vb_k);                                        \
+    const uint32_t kv_ = wave::min_u32_all(vb_k);                                    \
+    const uint64_t at_ = wave::ballot(vb_k == kv_);                                  \
+    const uint32_t km_ = wave::uniform_u(kv_);                                       \
     v_key = km_;                                                                     \
     v_pos = -1;                                                                      \
     if (km_ != 0xFFFFFFFFu) {                                                        \
-      const int ln_ = __builtin_ctzll(wave::ballot(vb_k == km_));                    \
+      const int ln_ = __builtin_ctzll(at_);                                          \
       v_pos = wave::readlane(vb_p, ln_);                                             \
       v_so = wave::readlane_u(vb_s, ln_);                                            \
     }                                                                                \
@@ -416,9 +418,11 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
 #define SK_V_MERGE()                                                                 \
   do {                                                                               \
     SK_V_SCAN(nVe, nV)                                                               \
-    const uint32_t km_ = wave::min_u32(vb_k);                                        \
+    const uint32_t kv_ = wave::min_u32_all(vb_k);                                    \
+    const uint64_t at_ = wave::ballot(vb_k == kv_);                                  \
+    const uint32_t km_ = wave::uniform_u(kv_);                                       \
     if (km_ < v_key) {                                                               \
-      const int ln_ = __builtin_ctzll(wave::ballot(vb_k == km_));                    \
+      const int ln_ = __builtin_ctzll(at_);                                          \
       v_key = km_;                                                                   \
       v_pos = wave::readlane(vb_p, ln_);                                             \
       v_so = wave::readlane_u(vb_s, ln_);                                            \
@@ -577,13 +581,15 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
               best = lt ? kk : best;
               brow = lt ? r : brow;
             }
-            const uint32_t imin = wave::min_u32(best);
+            const uint32_t iv = wave::min_u32_all(best);
+            const uint64_t at = wave::ballot(best == iv);
+            const uint32_t imin = wave::uniform_u(iv);
             if (imin == 0xFFFFFFFFu) break;
             if (nV >= P.cap_v) {
               status = SCHED_E_UNSUPPORTED;
               break;
             }
-            const int ln = __builtin_ctzll(wave::ballot(best == imin));
+            const int ln = __builtin_ctzll(at);
             const int rr = wave::readlane(brow, ln);
             int32_t xk = 0, ck = 0, uk = 0;
             uint32_t kk = 0;
@@ -643,12 +649,14 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
               best = lt ? r_key[r] : best;
               brow = lt ? r : brow;
             }
-            const uint32_t kmin = wave::min_u32(best);
+            const uint32_t kv = wave::min_u32_all(best);
+            const uint64_t at = wave::ballot(best == kv);
+            const uint32_t kmin = wave::uniform_u(kv);
             if (kmin == 0xFFFFFFFFu || nV >= P.cap_v) {  // no run: impossible while P > M > 0
               status = SCHED_E_UNSUPPORTED;
               break;
             }
-            const int ln = __builtin_ctzll(wave::ballot(best == kmin));
+            const int ln = __builtin_ctzll(at);
             const int rr = wave::readlane(brow, ln);
             int32_t ek = 0, xk = 0, ck = 0;
             SK_AT_ROW(rr, ek = wave::readlane(r_end[r], ln); xk = wave::readlane(r_x[r], ln);

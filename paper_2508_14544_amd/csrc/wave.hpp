@@ -48,6 +48,9 @@ __device__ __forceinline__ uint32_t writelane_u(uint32_t v, uint32_t s, int lane
 }
 
 __device__ __forceinline__ int32_t uniform(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ uint32_t uniform_u(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int32_t>(v)));
+}
 
 // The same value, held in vector registers: the compiler treats the result
 // as varying per lane.  For wave-uniform state that is used rarely (array
@@ -111,6 +114,10 @@ __device__ __forceinline__ int32_t sum_i32(int32_t v) {
 __device__ __forceinline__ int32_t sum_i32_all(int32_t v) {
   return static_cast<int32_t>(fold_in_row(fold_rows(static_cast<uint32_t>(v), OpAddU32{}), OpAddU32{}));
 }
+
+// The minimum left in every lane, for locating it with a ballot without a
+// round trip through a scalar register.
+__device__ __forceinline__ uint32_t min_u32_all(uint32_t v) { return fold_in_row(fold_rows(v, OpMinU32{}), OpMinU32{}); }
 
 __device__ __forceinline__ uint32_t min_u32(uint32_t v) {
   const uint32_t r = fold_in_row(fold_rows(v, OpMinU32{}), OpMinU32{});
