@@ -120,7 +120,8 @@ def test_single_n200(B, algo):
 
 @pytest.mark.parametrize("cap", [384, 512, 1024])
 def test_launch_shape_independence(B, cap):
-    # 8 and 16 register rows per lane give the same bits (the default here is 16 rows)
+    # 6, 8 and 16 register rows give the same bits as the default launches (a
+    # 6-row kernel that re-runs outgrown instances with 8 rows, then 16)
     batch = W.generate("batch4096_n1000_m16384", 0, instance_ids=range(0, 4096, 97))
     ref = gpu_run(B, batch, O.AMIN)
     g = gpu_run(B, batch, O.AMIN, running_capacity=cap)
