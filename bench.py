@@ -6,7 +6,9 @@ its last completion) through the C ABI: the per-instance preparation kernel
 and the simulation kernel.  Inputs are resident in HBM before timing starts.
 
 Prints one JSON line.  Also reports the roofline of the simulation kernel
-(int32 VALU lane-operations; see the design doc for the per-request-step figure)
+(int32 VALU lane-operations: 6 per simulated request-step, the completion
+compare, the projected-memory add and the head test's compare, max, end
+compare and add for that run)
 and the CPU oracle timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -24,7 +26,8 @@ sys.path.insert(0, ROOT)
 # MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = int32 VALU lane-operations per second
 PEAK_INT32_LANE_OPS = 256 * 4 * 16 * 2.4e9
 PEAK_LDS_BYTES = 256 * 128 * 2.4e9
-# algorithmic int32 lane-operations per simulated request-step ("Roofline")
+# algorithmic int32 lane-operations per simulated request-step: completion compare,
+# projected-memory add, and the head test's planned-end compare, max, end compare, add
 OPS_PER_REQUEST_STEP = 6
 METRIC = "simulated request-steps/sec (A_min, 4096×n=1000) + % VALU/LDS roofline"
 SIM_KERNEL = "k_simulate"
@@ -159,7 +162,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only; the instances of a batch are "
-                                   "independent, and sharding them across GPUs is described in DESIGN.md"}))
+                                   "independent, so several GPUs would each simulate a contiguous share "
+                                   "of them and gather the per-instance outputs at the end"}))
         sys.exit(2)
 
     import numpy as np
