@@ -259,9 +259,6 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
 // Internal status of a first pass whose running set outgrew its register rows;
 // the retry pass (more rows) re-runs exactly those instances.
 constexpr int kRetry = -100;
-// Internal status of a body whose running set outgrew its rows when the same
-// wave re-runs the instance at once with a wider body.
-constexpr int kRetryInWave = -101;
 // r_end of an empty slot of the running set (below every planned end)
 constexpr int32_t kEmpty = INT32_MIN;
 // r_c of an empty slot (after every step)
@@ -277,11 +274,32 @@ __device__ __forceinline__ uint32_t uniform_u32(uint32_t v) {
   return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int32_t>(v)));
 }
 
+// The loop-carried state of one instance's simulation at an admission that
+// found no free register slot: a body with more rows continues from it (its
+// extra rows start empty); the LDS sets stay where they are.
+constexpr int kStateRows = 8;
+struct SimState {
+  int32_t r_end[kStateRows], r_x[kStateRows], r_c[kStateRows], r_h[kStateRows], r_u[kStateRows];
+  uint32_t r_key[kStateRows];
+  int fr_row;
+  uint64_t fr_mask;
+  int32_t N, X, t_r, next_c, aw_base, aw_a, aw_rank, arr_ptr, next_a, f_rank, fw_base, f_u, fw_u;
+  uint32_t f_key, f_so, fw_key, fw_so, v_key, v_so;
+  int32_t nV, nVe, v_pos, v_head, v_u, n_done, retry_at, t, DT;
+  int64_t rsteps, tot_ev;
+};
+// Status of a body that handed its state over (TO_STATE) instead of ending.
+constexpr int kResume = -102;
+
 // Simulates instance k (whose validation status is st0) with ROWS register
-// rows and writes its outputs; a running set that outgrows the rows ends the
-// simulation with `retry_status` (the per-request outputs are then reset).
-template <int ALGO, int ROWS>
-__device__ __forceinline__ int sim_instance(const Params& P, const int k, const int st0, const int retry_status) {
+// rows and writes its outputs.  A running set that outgrows the rows ends the
+// simulation with `retry_status` (the per-request outputs are then reset), or,
+// with TO_STATE, saves the state to *st and returns kResume at once.  With
+// FROM_STATE the body continues from *st instead of starting at step 0.
+template <int ALGO, int ROWS, bool FROM_STATE = false, bool TO_STATE = false>
+__device__ __forceinline__ int sim_instance(const Params& P, const int k, const int st0, const int retry_status,
+                                           SimState* st = nullptr) {
+  static_assert(!(FROM_STATE || TO_STATE) || ROWS <= kStateRows, "state holds at most kStateRows rows");
   extern __shared__ uint64_t lds64[];
   const int lane = threadIdx.x;
   const int64_t b = P.offsets[k];
@@ -290,7 +308,8 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
 
   int status = st0;
   // counters live in vector registers (see wave::in_vgpr)
-  int64_t rsteps = wave::in_vgpr<int64_t>(0), tot_ev = wave::in_vgpr<int64_t>(0);
+  int64_t rsteps = wave::in_vgpr<int64_t>(FROM_STATE ? st->rsteps : 0);
+  int64_t tot_ev = wave::in_vgpr<int64_t>(FROM_STATE ? st->tot_ev : 0);
 
   if (st0 == SCHED_OK && n > 0) {
     uint64_t* L0 = lds64;
@@ -301,13 +320,14 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     uint64_t* vent = L1 + P.nw1_max;
     const int nw = (n + 63) >> 6;
     const int nw1 = (nw + 63) >> 6;
-    for (int w = lane; w < nw; w += 64) L0[w] = 0;
-    for (int w = lane; w < nw1; w += 64) L1[w] = 0;
-    __syncthreads();
+    if (!FROM_STATE) {
+      for (int w = lane; w < nw; w += 64) L0[w] = 0;
+      for (int w = lane; w < nw1; w += 64) L1[w] = 0;
+      __syncthreads();
+    }
 
     const int32_t cap = P.cap[k];
-    // array bases in vector registers, except for A_l, whose extra register
-    // row leaves no room for them within four waves per SIMD
+    // array bases in vector registers
     auto base = [](auto* p) { return wave::in_vgpr(p); };
     const uint2* rec = base(P.rec + b);
     const int32_t* arrival = P.arrival ? base(P.arrival + b) : nullptr;
@@ -324,6 +344,10 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) {
       r_end[r] = kEmpty; r_x[r] = 0; r_c[r] = kNever; r_h[r] = 0; r_key[r] = 0xFFFFFFFFu; r_u[r] = 0;
+      if (FROM_STATE) {
+        r_end[r] = st->r_end[r]; r_x[r] = st->r_x[r]; r_c[r] = st->r_c[r];
+        r_h[r] = st->r_h[r]; r_key[r] = st->r_key[r]; r_u[r] = st->r_u[r];
+      }
     }
     int fr_row = 0;               // row that receives new runs ...
     uint64_t fr_mask = ~0ull;     // ... and its free lanes
@@ -343,6 +367,16 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     int32_t n_done = 0;
     // the head cannot start before retry_at; valid until the next event
     int32_t retry_at = 0;
+    int32_t t = 0;
+    int32_t DT = 0;               // memory held at t by the runs completing at t
+    if (FROM_STATE) {
+      fr_row = st->fr_row; fr_mask = st->fr_mask; N = st->N; X = st->X; t_r = st->t_r; next_c = st->next_c;
+      aw_base = st->aw_base; aw_a = st->aw_a; aw_rank = st->aw_rank; arr_ptr = st->arr_ptr; next_a = st->next_a;
+      f_rank = st->f_rank; fw_base = st->fw_base; f_key = st->f_key; f_so = st->f_so; fw_key = st->fw_key;
+      fw_so = st->fw_so; f_u = st->f_u; fw_u = st->fw_u;
+      nV = st->nV; nVe = st->nVe; v_pos = st->v_pos; v_head = st->v_head; v_key = st->v_key; v_so = st->v_so;
+      v_u = st->v_u; n_done = st->n_done; retry_at = st->retry_at; t = st->t; DT = st->DT;
+    }
 
 #define SK_LOAD_ARRIVALS()                                                           \
   do {                                                                               \
@@ -481,8 +515,9 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     }                                                                                \
   } while (0)
 
-    int32_t t = 0;
+    bool resuming = FROM_STATE;   // continue with the admissions of step t
     for (;;) {
+      if (!resuming) {
       if (t > cap) {
         status = SCHED_E_STEP_CAP;
         break;
@@ -529,7 +564,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       if (heads_changed) event = true;
 
       // ---- 2. completions at t; DT = memory they still hold at t (s + o each)
-      int32_t DT = 0;
+      DT = 0;
       if (t >= next_c) {
         int32_t sx = 0;
         int ndone = 0;
@@ -688,6 +723,8 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
         }
       }
       if (event) retry_at = 0;
+      }
+      resuming = false;
 
       // ---- 5. admission of the longest feasible prefix in key order
       bool stuck = true;          // the head cannot start before the next event
@@ -756,16 +793,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
         }
         const int32_t f = wave::uniform(fv);
         // admit: start at p = t; runs whose planned end is in (t+1, E] gain its share
-        const int32_t xw = s - t + t_r;
-        const int32_t hw = f + (xw + cE) + cE;
-        if (win) {
-          const uint32_t dh = static_cast<uint32_t>(xw) - static_cast<uint32_t>(t_r);
-#pragma unroll
-          for (int r = 0; r < ROWS; ++r) {
-            const uint32_t e = static_cast<uint32_t>(r_end[r]);
-            r_h[r] = static_cast<int32_t>(static_cast<uint32_t>(r_h[r]) + (e - lo2 <= span ? e + dh : 0u));
-          }
-        }
+        // a free slot first: without one nothing has changed for this candidate
         if (fr_mask == 0ull) {
           int rr = -1;
           uint64_t mm = 0ull;
@@ -776,11 +804,43 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
             mm = m ? m : mm;
           }
           if (rr < 0) {
-            status = retry_status;
+            if (TO_STATE) {
+              // hand the state at this admission to a body with more rows
+#pragma unroll
+              for (int r = 0; r < kStateRows; ++r) {
+                const bool have = r < ROWS;
+                st->r_end[r] = have ? r_end[r < ROWS ? r : 0] : kEmpty;
+                st->r_x[r] = have ? r_x[r < ROWS ? r : 0] : 0;
+                st->r_c[r] = have ? r_c[r < ROWS ? r : 0] : kNever;
+                st->r_h[r] = have ? r_h[r < ROWS ? r : 0] : 0;
+                st->r_key[r] = have ? r_key[r < ROWS ? r : 0] : 0xFFFFFFFFu;
+                st->r_u[r] = have ? r_u[r < ROWS ? r : 0] : 0;
+              }
+              st->fr_row = fr_row; st->fr_mask = fr_mask; st->N = N; st->X = X; st->t_r = t_r;
+              st->next_c = next_c; st->aw_base = aw_base; st->aw_a = aw_a; st->aw_rank = aw_rank;
+              st->arr_ptr = arr_ptr; st->next_a = next_a; st->f_rank = f_rank; st->fw_base = fw_base;
+              st->f_key = f_key; st->f_so = f_so; st->fw_key = fw_key; st->fw_so = fw_so; st->f_u = f_u;
+              st->fw_u = fw_u; st->nV = nV; st->nVe = nVe; st->v_pos = v_pos; st->v_head = v_head;
+              st->v_key = v_key; st->v_so = v_so; st->v_u = v_u; st->n_done = n_done;
+              st->retry_at = retry_at; st->t = t; st->DT = DT; st->rsteps = rsteps; st->tot_ev = tot_ev;
+              status = kResume;
+            } else {
+              status = retry_status;
+            }
             break;
           }
           fr_row = rr;
           fr_mask = mm;
+        }
+        const int32_t xw = s - t + t_r;
+        const int32_t hw = f + (xw + cE) + cE;
+        if (win) {
+          const uint32_t dh = static_cast<uint32_t>(xw) - static_cast<uint32_t>(t_r);
+#pragma unroll
+          for (int r = 0; r < ROWS; ++r) {
+            const uint32_t e = static_cast<uint32_t>(r_end[r]);
+            r_h[r] = static_cast<int32_t>(static_cast<uint32_t>(r_h[r]) + (e - lo2 <= span ? e + dh : 0u));
+          }
         }
         {
           const int ln = __builtin_ctzll(fr_mask);
@@ -854,6 +914,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       }
       t = tn;
     }
+    if (TO_STATE && status == kResume) return kResume;
   }
 
   // ---- epilogue: totals from the per-request outputs
@@ -911,18 +972,17 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
   sim_instance<ALGO, ROWS>(P, k, st0, P.retry_status);
 }
 
-// One wave per instance with 6 rows; an instance whose running set outgrows
-// them is simulated again at once by the same wave with 8 rows (its outputs
-// were reset; the fence orders that reset before the new run's writes and
-// atomics).  Held to 128 VGPRs so that four waves share a SIMD.
-template <int ALGO>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_simulate_6_8(Params P) {
+// One wave per instance with ROWS1 rows; when the running set of its instance
+// outgrows them, the wave continues the same simulation with 8 rows from the
+// admission that found no free slot (the state moves in registers, the LDS
+// sets stay).  Held to 128 VGPRs so that four waves share a SIMD.
+template <int ALGO, int ROWS1>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_simulate_grow(Params P) {
   const int k = blockIdx.x;
   if (P.algo_of && P.algo_of[k] != ALGO) return;
-  if (sim_instance<ALGO, 6>(P, k, P.status[k], kRetryInWave) == kRetryInWave) {
-    __threadfence();
-    sim_instance<ALGO, 8>(P, k, SCHED_OK, P.retry_status);
-  }
+  SimState st;
+  if (sim_instance<ALGO, ROWS1, false, true>(P, k, P.status[k], 0, &st) == kResume)
+    sim_instance<ALGO, 8, true, false>(P, k, SCHED_OK, P.retry_status, &st);
 }
 #undef SK_LOAD_ARRIVALS
 #undef SK_PICK
@@ -941,20 +1001,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
 // ---------------------------------------------------------------------------
 namespace {
 
-// Kernel variants by register rows.  First launch: `rows`, and with rows2 > 0
-// an in-wave re-run with rows2 rows for instances that outgrow `rows`.  Retry
-// launch (retry = true): the instances an earlier launch handed over.
+// Kernel variants by register rows.  First launch: `rows`, or with rows2 > 0
+// 5 rows growing to 8 in the same wave (k_simulate_grow).  Retry launch
+// (retry = true): the instances an earlier launch handed over.
 template <int ALGO>
 const void* sim_kernel(int rows, int rows2, bool retry) {
   if (retry)
     return rows <= 8 ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, true>)
                      : reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true>);
   if constexpr (ALGO != SCHED_AELL)
-    if (rows2 > 0) return reinterpret_cast<const void*>(&sk::k_simulate_6_8<ALGO>);
+    if (rows2 > 0) return reinterpret_cast<const void*>(&sk::k_simulate_grow<ALGO, 5>);
   switch (rows) {
     case 1: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 1, false>);
     case 2: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 2, false>);
     case 4: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 4, false>);
+    case 5: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 5, false>);
     case 6: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 6, false>);
     case 8: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, false>);
     default: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, false>);
@@ -964,7 +1025,7 @@ const void* sim_kernel(int rows, int rows2, bool retry) {
 // register rows that hold `want` runs
 int rows_for(int64_t want) {
   const int64_t r = (want + 63) / 64;
-  return r <= 1 ? 1 : r <= 2 ? 2 : r <= 4 ? 4 : r <= 6 ? 6 : r <= 8 ? 8 : 16;
+  return r <= 1 ? 1 : r <= 2 ? 2 : r <= 4 ? 4 : r <= 5 ? 5 : r <= 6 ? 6 : r <= 8 ? 8 : 16;
 }
 
 struct Tier {
@@ -1050,18 +1111,17 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   const int64_t nmax = in->max_requests;
   if (o.running_capacity > 1024) return SCHED_E_UNSUPPORTED;
   const bool forced = o.running_capacity > 0;
-  // launches per policy.  The first covers up to 384 runs (every run of most
-  // instances); an instance that outgrows them is simulated again with 512,
-  // then with 1024.  A_max, H-SF and A_random re-run it at once in the same
-  // wave; A_l, whose 6-row kernel already needs the registers of four waves
-  // per SIMD, starts with 512; A_min (whose combined kernel spills more
-  // scalar registers) hands it to a retry launch.
+  // launches per policy.  The first holds up to 320 runs (every run of most
+  // instances) and its wave continues with 512 when its instance outgrows
+  // them; A_l, which keeps one more register row and often holds more than
+  // 320 runs, starts with 512.  Instances beyond 512 runs are simulated again
+  // by a second launch with 1024.
   auto tiers_for = [&](int a, Tier* out) -> int {
     if (forced) {
       out[0] = Tier{rows_for(o.running_capacity), 0, false};
       return 1;
     }
-    if (nmax <= 384) {
+    if (nmax <= 320) {
       out[0] = Tier{rows_for(std::max<int64_t>(nmax, 1)), 0, false};
       return 1;
     }
@@ -1069,7 +1129,7 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
     if (a == SCHED_AELL) {
       out[m++] = Tier{8, 0, false};
     } else {
-      out[m++] = Tier{6, 8, false};
+      out[m++] = Tier{5, 8, false};
     }
     if (nmax > 512) out[m++] = Tier{16, 0, true};
     return m;

@@ -217,6 +217,35 @@ def test_default_passes_after_cancellations(B, algo):
     assert_parity(batch, g, ref)
 
 
+def _growth_instances():
+    # a first group of long runs is cancelled (A_min) from the first steps; a
+    # burst of tiny requests then lifts the running set past 320 while
+    # cancelled requests still wait, so the wave continues with more rows in
+    # the middle of the churn (and, for some, past 512)
+    insts = []
+    for seed, (n1, n2, t2, o1max) in [(1, (250, 500, 8, 20)), (1, (300, 600, 12, 30)), (0, (350, 500, 10, 25)),
+                                      (2, (250, 500, 8, 20)), (0, (200, 400, 6, 20))]:
+        rng = np.random.default_rng(seed)
+        o = np.r_[rng.integers(5, o1max + 1, n1), rng.integers(1, 4, n2)]
+        insts.append({"arrival": np.r_[np.zeros(n1, int), np.sort(rng.integers(t2, t2 + 4, n2))],
+                      "prompt": np.r_[np.ones(n1, int), np.zeros(n2, int)], "output": o,
+                      "lower": np.ones(n1 + n2, int), "upper": o + 2})
+    return W.from_lists(1600, insts, name="growth")
+
+
+@pytest.mark.parametrize("algo", ["amin", "hsf", "amax", "aell", "adaptive"])
+def test_growth_mid_simulation(B, algo):
+    batch = _growth_instances()
+    ref = oracle_run(batch, ALGOS[algo])
+    assert (ref["status"] == 0).all()
+    g = gpu_run(B, batch, ALGOS[algo])
+    assert_parity(batch, g, ref)
+    # the same bits from one launch that never runs out of rows
+    g1 = gpu_run(B, batch, ALGOS[algo], running_capacity=1024)
+    for f in ("status", "tel", "makespan", "request_steps", "total_evictions", "completion", "evictions"):
+        assert np.array_equal(g[f], g1[f]), f
+
+
 def test_determinism_and_chunking(B):
     batch = W.generate("batch4096_n1000_m16384", 0, instance_ids=range(1000, 1300))
     a = gpu_run(B, batch, O.AMIN)
