@@ -1009,8 +1009,7 @@ const void* sim_kernel(int rows, int rows2, bool retry) {
   if (retry)
     return rows <= 8 ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, true>)
                      : reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true>);
-  if constexpr (ALGO != SCHED_AELL)
-    if (rows2 > 0) return reinterpret_cast<const void*>(&sk::k_simulate_grow<ALGO, 5>);
+  if (rows2 > 0) return reinterpret_cast<const void*>(&sk::k_simulate_grow<ALGO, 5>);
   switch (rows) {
     case 1: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 1, false>);
     case 2: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 2, false>);
@@ -1111,12 +1110,10 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   const int64_t nmax = in->max_requests;
   if (o.running_capacity > 1024) return SCHED_E_UNSUPPORTED;
   const bool forced = o.running_capacity > 0;
-  // launches per policy.  The first holds up to 320 runs (every run of most
-  // instances) and its wave continues with 512 when its instance outgrows
-  // them; A_l, which keeps one more register row and often holds more than
-  // 320 runs, starts with 512.  Instances beyond 512 runs are simulated again
-  // by a second launch with 1024.
-  auto tiers_for = [&](int a, Tier* out) -> int {
+  // launches: the first holds up to 320 runs (every run of most instances)
+  // and its wave continues with 512 when its instance outgrows them;
+  // instances beyond 512 runs are simulated again by a second launch with 1024
+  auto tiers_for = [&](Tier* out) -> int {
     if (forced) {
       out[0] = Tier{rows_for(o.running_capacity), 0, false};
       return 1;
@@ -1126,11 +1123,7 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
       return 1;
     }
     int m = 0;
-    if (a == SCHED_AELL) {
-      out[m++] = Tier{8, 0, false};
-    } else {
-      out[m++] = Tier{5, 8, false};
-    }
+    out[m++] = Tier{5, 8, false};
     if (nmax > 512) out[m++] = Tier{16, 0, true};
     return m;
   };
@@ -1226,7 +1219,7 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   for (int a = 0; a < n_sim && err == hipSuccess; ++a) {
     const size_t lds = lds_for(sim_algos[a]);
     Tier tiers[3];
-    const int n_tiers = tiers_for(sim_algos[a], tiers);
+    const int n_tiers = tiers_for(tiers);
     for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass)
       if (lds > 65536) err = set_lds_limit_any(sim_algos[a], tiers[pass], static_cast<int>(lds));
   }
@@ -1235,7 +1228,7 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
     P.cap_v = cap_v_for(sim_algos[a]);
     const size_t lds = lds_for(sim_algos[a]);
     Tier tiers[3];
-    const int n_tiers = tiers_for(sim_algos[a], tiers);
+    const int n_tiers = tiers_for(tiers);
     for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass) {
       P.retry_status = pass + 1 < n_tiers ? sk::kRetry : SCHED_E_UNSUPPORTED;
       err = launch_sim_any(sim_algos[a], tiers[pass], P, lds, st);
