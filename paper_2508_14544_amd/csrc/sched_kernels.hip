@@ -9,27 +9,35 @@
 //   (8-bit digits, LDS histogram, ballot-based stable scatter).  The ranked
 //   records (key, s | o << 16) go to a workspace slice of the instance.
 //
-// k_simulate (per instance), state:
+// k_simulate (per instance), one body per policy (A_max, A_min, H-SF, A_l,
+// A_random; the adaptive policy runs the A_min and the A_l bodies, each on
+// its own instances), state:
 //   running set R    -- ROWS x 64 register slots, row r lane j holds one run:
 //                       planned end Rend = p + est, x = s - p + t_r, completion
 //                       C = p + o, key = est << 17 | index, and h = f(Rend) +
 //                       Rend - t_r, where f(c) is the planned memory at step c of
 //                       all runs whose planned end is >= c (equation (2) summed
 //                       over the planned set).  t_r is a base step that keeps the
-//                       int32 values small (rebased every 2^16 steps).
+//                       int32 values small (rebased every 2^16 steps).  The first
+//                       body has 5 rows; a wave whose instance outgrows them
+//                       hands its state to an 8-row body in the same kernel,
+//                       and instances beyond 512 runs are simulated again by a
+//                       16-row retry launch.
 //   fresh waiting F  -- two-level bitmap over key ranks in LDS; the smallest
 //                       waiting key is the first set bit.
-//   evicted waiting V-- (A_min) unsorted (key, s | o << 16) array in LDS; the
-//                       smallest key is found by a wave min-reduction.
-// Per step: arrivals set bits of F; runs with C == t complete; for A_min the
+//   cancelled V      -- A_min: unsorted (key, s | o << 16) array in LDS, the
+//                       smallest key found by a wave min-reduction; A_l: a FIFO
+//                       ring of promoted requests in LDS.
+// Per step: arrivals set bits of F; runs with C == t complete (A_l: runs still
+// present at their planned end are promoted to the back of V); for A_min the
 // projected memory P at t+1 is compared with M and runs are cancelled in
-// ascending key while P > M; then candidates (smallest key of F and V) are
-// admitted while equation (2) holds.  The admission test needs only O(1)
-// wave reductions because the planned set before the test is always feasible
-// (every checkpoint after the candidate's planned end was verified when its
-// runs were admitted), so it checks: step t (runs completing now hold s+o),
-// step t+1 when a run is already past its planned end, every existing planned
-// end <= the candidate's via max h, and the candidate's own planned end.
+// ascending key while P > M; then candidates (smallest key of F and V; A_l:
+// F first) are admitted while equation (2) holds.  The admission test needs
+// only O(1) wave reductions because the planned set before the test is always
+// feasible (every checkpoint after the candidate's planned end was verified
+// when its runs were admitted), so it checks: step t (runs completing now hold
+// s+o), step t+1 when a run is already past its planned end, every existing
+// planned end <= the candidate's via max h, and the candidate's own planned end.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
