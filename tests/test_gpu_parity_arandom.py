@@ -58,3 +58,17 @@ def test_batch4096_random_order_sampled(B):
     assert (g["status"] == 0).all()
     ks = list(range(0, 4096, 64)) + [1364, 1365, 2730, 4095]
     assert_parity(batch, g, oracle_run(batch, O.ARANDOM, instances=ks), instances=ks)
+
+
+def test_growth_mid_simulation_random_order(B):
+    # the running set outgrows the first register rows in the middle of the
+    # simulation (as in test_gpu_parity's growth test), under a random order
+    from test_gpu_parity import _growth_instances
+    batch = W.with_random_order(_growth_instances(), 5)
+    ref = oracle_run(batch, O.ARANDOM)
+    assert (ref["status"] == 0).all()
+    g = gpu_run(B, batch, O.ARANDOM)
+    assert_parity(batch, g, ref)
+    g1 = gpu_run(B, batch, O.ARANDOM, running_capacity=1024)
+    for f in ("status", "tel", "makespan", "request_steps", "completion"):
+        assert np.array_equal(g[f], g1[f]), f
