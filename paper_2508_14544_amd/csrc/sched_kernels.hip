@@ -981,16 +981,20 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
 }
 
 // One wave per instance with ROWS1 rows; when the running set of its instance
-// outgrows them, the wave continues the same simulation with 8 rows from the
-// admission that found no free slot (the state moves in registers, the LDS
-// sets stay).  Held to 128 VGPRs so that four waves share a SIMD.
+// outgrows them, the wave continues the same simulation with 6, then 8 rows
+// (A_l: 8) from the admission that found no free slot (the state moves in
+// registers, the LDS sets stay).  Held to 128 VGPRs so that four waves share
+// a SIMD.
 template <int ALGO, int ROWS1>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_simulate_grow(Params P) {
   const int k = blockIdx.x;
   if (P.algo_of && P.algo_of[k] != ALGO) return;
   SimState st;
-  if (sim_instance<ALGO, ROWS1, false, true>(P, k, P.status[k], 0, &st) == kResume)
-    sim_instance<ALGO, 8, true, false>(P, k, SCHED_OK, P.retry_status, &st);
+  int r = sim_instance<ALGO, ROWS1, false, true>(P, k, P.status[k], 0, &st);
+  // (A_l's extra register row leaves no room for a third body)
+  if constexpr (ALGO != SCHED_AELL)
+    if (r == kResume) r = sim_instance<ALGO, 6, true, true>(P, k, SCHED_OK, 0, &st);
+  if (r == kResume) sim_instance<ALGO, 8, true, false>(P, k, SCHED_OK, P.retry_status, &st);
 }
 #undef SK_LOAD_ARRIVALS
 #undef SK_PICK
