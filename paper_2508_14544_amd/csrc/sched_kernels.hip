@@ -878,11 +878,16 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
           --nV;
           SK_V_HEAD();
         } else {
-          // the last eligible entry moves into the hole; the last pending one fills its place
-          if (lane == 0) {
+          // the last eligible entry moves into the hole; the last pending one fills
+          // its place.  Lane 0 and lane 1 do the two moves with one read and one
+          // write (when the hole is the last eligible slot, only the second move
+          // is left, as in doing them one after the other)
+          if (lane < 2) {
             const int le = nVe - 1;
-            vent[v_pos] = vent[le];
-            if (nV > nVe) vent[le] = vent[nV - 1];
+            const int src = lane == 0 ? le : nV - 1;
+            const uint64_t mv = vent[src];
+            const bool act = lane == 0 ? v_pos != le : nV > nVe;
+            if (act) vent[lane == 0 ? v_pos : le] = mv;
           }
           --nVe;
           --nV;

@@ -246,6 +246,17 @@ def test_growth_mid_simulation(B, algo):
         assert np.array_equal(g[f], g1[f]), f
 
 
+@pytest.mark.parametrize("cap", [18, 30])
+def test_growth_then_step_cap(B, cap):
+    # the step cap ends the simulation after the running set has outgrown the
+    # first rows (crossings at steps 0, 14, 15, 22): partial outputs as the oracle's
+    batch = _growth_instances()
+    for algo in (O.AMIN, O.HSF):
+        ref = oracle_run(batch, algo, step_cap=cap)
+        assert (ref["status"] == O.E_STEP_CAP).any()
+        assert_parity(batch, gpu_run(B, batch, algo, step_cap=cap), ref)
+
+
 def test_determinism_and_chunking(B):
     batch = W.generate("batch4096_n1000_m16384", 0, instance_ids=range(1000, 1300))
     a = gpu_run(B, batch, O.AMIN)
