@@ -523,6 +523,23 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     }                                                                                \
   } while (0)
 
+    // Issue priority among the waves of a SIMD: the more requests an instance
+    // still has to complete, the higher (four levels by the unfinished
+    // fraction), so the instances that bound the launch are not slowed by
+    // their SIMD-mates.  Outputs do not depend on it.
+    int prio = -1;
+#define SK_SET_PRIORITY()                                                            \
+  do {                                                                               \
+    const int lv_ = (4 * (n - n_done) - 1) / n;                                      \
+    if (lv_ != prio) {                                                               \
+      prio = lv_;                                                                    \
+      if (lv_ >= 3) __builtin_amdgcn_s_setprio(3);                                   \
+      else if (lv_ == 2) __builtin_amdgcn_s_setprio(2);                              \
+      else if (lv_ == 1) __builtin_amdgcn_s_setprio(1);                              \
+      else __builtin_amdgcn_s_setprio(0);                                            \
+    }                                                                                \
+  } while (0)
+    SK_SET_PRIORITY();
     bool resuming = FROM_STATE;   // continue with the admissions of step t
     for (;;) {
       if (!resuming) {
@@ -606,6 +623,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
           N -= ndone;
           DT = sxw + ndone * (t - t_r);
           n_done += ndone;
+          SK_SET_PRIORITY();
         }
         // ---- 3. done?
         if (n_done == n) break;
@@ -1001,6 +1019,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
     if (r == kResume) r = sim_instance<ALGO, 6, true, true>(P, k, SCHED_OK, 0, &st);
   if (r == kResume) sim_instance<ALGO, 8, true, false>(P, k, SCHED_OK, P.retry_status, &st);
 }
+#undef SK_SET_PRIORITY
 #undef SK_LOAD_ARRIVALS
 #undef SK_PICK
 #undef SK_F_FIND
