@@ -136,7 +136,9 @@ def cpu_baseline(batch, algo, g_out, target_s: float, threads: int):
     w_ratio = work / max(1, int(st["request_steps"].sum()))
     return {
         "value": rs / wall, "unit": "request-steps/s", "cores": threads, "kind": "oracle",
-        "sample": f"{len(sample)} of {K} instances (every {stride}th), {rs} request-steps in {wall:.1f} s",
+        "sample": (f"{len(sample)} of {K} instances ("
+                   + (f"one in {stride}" if stride > 1 else "the first, in index order")
+                   + f"), {rs} request-steps in {wall:.1f} s on {threads} host threads"),
     }, bool(ok), (w_ratio, len(sub))
 
 
