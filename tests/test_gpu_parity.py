@@ -257,6 +257,41 @@ def test_growth_then_step_cap(B, cap):
         assert_parity(batch, gpu_run(B, batch, algo, step_cap=cap), ref)
 
 
+def _growth_sweep(seed, K=96):
+    # random instances whose running sets peak on both sides of 320, 384 and
+    # 512 runs: a first group that fills the memory (cancellations under
+    # A_min, promotions under A_l) and a burst of short requests a few steps
+    # later; every policy's priority input is a random order
+    rng = np.random.default_rng(seed)
+    insts = []
+    for _ in range(K):
+        n1, n2 = int(rng.integers(100, 350)), int(rng.integers(150, 550))
+        o = np.r_[rng.integers(3, int(rng.integers(8, 40)), n1), rng.integers(1, int(rng.integers(2, 6)), n2)]
+        t2 = int(rng.integers(0, 20))
+        a = np.r_[np.sort(rng.integers(0, 3, n1)), np.sort(rng.integers(t2, t2 + int(rng.integers(1, 6)), n2))]
+        order = np.argsort(a, kind="stable")
+        s = np.r_[rng.integers(0, 3, n1), rng.integers(0, 2, n2)]
+        l = np.maximum(1, (o * rng.uniform(0.2, 1.0, n1 + n2)).astype(int))
+        u = o + rng.integers(0, 4, n1 + n2)
+        insts.append({"arrival": a[order], "prompt": s[order], "output": o[order], "lower": l[order],
+                      "upper": u[order], "priority": rng.permutation(n1 + n2)})
+    return W.from_lists(1400, insts, name=f"growth_sweep{seed}")
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+@pytest.mark.parametrize("name", ["amin", "amax", "hsf", "aell", "adaptive", "arandom"])
+def test_growth_random_sweep(B, seed, name):
+    algo = O.ALGOS[name]
+    batch = _growth_sweep(seed)
+    ref = oracle_run(batch, algo)
+    assert (ref["status"] == 0).all()
+    g = gpu_run(B, batch, algo)
+    assert_parity(batch, g, ref)
+    g1 = gpu_run(B, batch, algo, running_capacity=1024)
+    for f in ("status", "tel", "makespan", "request_steps", "total_evictions", "completion", "evictions"):
+        assert np.array_equal(g[f], g1[f]), f
+
+
 def test_determinism_and_chunking(B):
     batch = W.generate("batch4096_n1000_m16384", 0, instance_ids=range(1000, 1300))
     a = gpu_run(B, batch, O.AMIN)
