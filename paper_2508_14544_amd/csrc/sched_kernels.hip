@@ -1043,8 +1043,9 @@ namespace {
 template <int ALGO>
 const void* sim_kernel(int rows, int rows2, bool retry) {
   if (retry)
-    return rows <= 8 ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, true>)
-                     : reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true>);
+    return rows <= 8    ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, true>)
+           : rows <= 10 ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 10, true>)
+                        : reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true>);
   if (rows2 > 0) return reinterpret_cast<const void*>(&sk::k_simulate_grow<ALGO, 5>);
   switch (rows) {
     case 1: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 1, false>);
@@ -1147,8 +1148,10 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   if (o.running_capacity > 1024) return SCHED_E_UNSUPPORTED;
   const bool forced = o.running_capacity > 0;
   // launches: the first holds up to 320 runs (every run of most instances)
-  // and its wave continues with 512 when its instance outgrows them;
-  // instances beyond 512 runs are simulated again by a second launch with 1024
+  // and its wave continues with 384, then 512 when its instance outgrows
+  // them; instances beyond 512 runs are simulated again by a launch with 640
+  // (fewer registers, so more waves per SIMD than with 1024), and beyond 640
+  // by one with 1024
   auto tiers_for = [&](Tier* out) -> int {
     if (forced) {
       out[0] = Tier{rows_for(o.running_capacity), 0, false};
@@ -1160,7 +1163,8 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
     }
     int m = 0;
     out[m++] = Tier{5, 8, false};
-    if (nmax > 512) out[m++] = Tier{16, 0, true};
+    if (nmax > 512) out[m++] = Tier{10, 0, true};
+    if (nmax > 640) out[m++] = Tier{16, 0, true};
     return m;
   };
 

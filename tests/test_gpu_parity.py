@@ -195,20 +195,21 @@ def test_capacity_overflow_reported(B):
 @pytest.mark.parametrize("algo", ["amin", "hsf", "amax", "aell", "adaptive"])
 def test_default_passes_after_cancellations(B, algo):
     # 140 long requests are cancelled (A_min, A_l) from step 1 on; a burst of
-    # tiny requests at step 3000 then lifts the running set past 384 (the
-    # 6-row body re-runs the instance with 8 rows in the same wave) or past
-    # 512 (a second launch with 16 rows).  The outputs, cancellation counts
-    # included, must be those of a run that never outgrew its rows.
+    # tiny requests at step 3000 then lifts the running set past 320 and 384
+    # (the wave continues with more rows), past 512 (a second launch with 640
+    # slots simulates the instance again) or past 640 (a third with 1024).
+    # The outputs, cancellation counts included, must be those of a run that
+    # never outgrew its rows.
     rng = np.random.default_rng(3)
     insts = []
-    for burst in (300, 450, 600, 0, 450, 600):
+    for burst in (300, 450, 600, 0, 450, 600, 900):
         g1 = 140
         o1 = rng.integers(10, 30, g1)
         o = np.r_[o1, np.ones(burst, int)]
         insts.append({"arrival": np.r_[np.zeros(g1, int), np.full(burst, 3000)],
                       "prompt": np.r_[np.full(g1, 4), np.zeros(burst, int)], "output": o,
                       "lower": np.ones(g1 + burst, int), "upper": o + 2})
-    batch = W.from_lists(700, insts, name="bursts")
+    batch = W.from_lists(1000, insts, name="bursts")
     g = gpu_run(B, batch, ALGOS[algo])
     ref = oracle_run(batch, ALGOS[algo])
     assert (ref["status"] == 0).all()
