@@ -122,12 +122,14 @@ typedef struct {
   int64_t step_cap;         /* last simulated step; <= 0: per instance
                                min(2^30, 4*(max a + sum(o+1)) + 64)                       */
   int32_t running_capacity; /* > 0 (<= 1024): hold at most this many concurrently running
-                               requests per instance, rounded up to 64, 128, 256, 384, 512
-                               or 1024; an instance that needs more gets
-                               SCHED_E_UNSUPPORTED.  0: as many as it needs, up to 1024 (the
-                               library starts with up to 384 and simulates an instance that
-                               outgrows them again with 512, then 1024; outputs do not
-                               depend on this)                                             */
+                               requests per instance, rounded up to 64, 128, 256, 320, 384,
+                               512 or 1024; an instance that needs more gets
+                               SCHED_E_UNSUPPORTED.  0: as many as it needs, up to 1024 (an
+                               instance of up to 320 requests gets room for all of them;
+                               a larger one starts with 320, grows to 384 and 512 within the
+                               same launch, and is simulated again from step 0 with 640,
+                               then 1024, if it outgrows that; outputs do not depend on
+                               this)                                                       */
   int32_t evicted_capacity; /* max cancelled requests waiting at once (A_min, A_l); 0: default */
   void* event_before;       /* hipEvent_t recorded just before the simulation kernel, or NULL */
   void* event_after;        /* hipEvent_t recorded just after it, or NULL                  */
