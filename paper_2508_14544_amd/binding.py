@@ -70,6 +70,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     if _lib is None:
         if not os.path.exists(path):
             raise OSError(f"{path} is not built; run __graft_entry__.build()")
+        # torch first: the library must bind to the HIP runtime that owns the
+        # device buffers and streams it is handed, not load a second one
+        import torch  # noqa: F401
         lib = ctypes.CDLL(path)
         lib.sched_simulate.restype = ctypes.c_int
         lib.sched_simulate.argtypes = [ctypes.POINTER(SchedInstances), ctypes.c_int, ctypes.c_int64,

@@ -20,9 +20,12 @@
 //                       over the planned set).  t_r is a base step that keeps the
 //                       int32 values small (rebased every 2^16 steps).  The first
 //                       body has 5 rows; a wave whose instance outgrows them
-//                       hands its state to an 8-row body in the same kernel,
-//                       and instances beyond 512 runs are simulated again by a
-//                       16-row retry launch.
+//                       hands its state to a 6-row, then an 8-row body in the
+//                       same kernel (A_l: straight to 8), and instances beyond
+//                       512 runs are simulated again by a 10-row, then a 16-row
+//                       retry launch.  Scans cover every row: a uniform branch
+//                       per row to stop at the last occupied one measured slower,
+//                       although runs occupy 2 or 3 of the 5 rows most of the time.
 //   fresh waiting F  -- two-level bitmap over key ranks in LDS; the smallest
 //                       waiting key is the first set bit.
 //   cancelled V      -- A_min: unsorted (key, s | o << 16) array in LDS, the
