@@ -27,7 +27,8 @@
 //                       per row to stop at the last occupied one measured slower,
 //                       although runs occupy 2 or 3 of the 5 rows most of the time.
 //   fresh waiting F  -- two-level bitmap over key ranks in LDS; the smallest
-//                       waiting key is the first set bit.
+//                       waiting key is the first set bit.  Its word is cached in
+//                       scalar registers until it empties.
 //   cancelled V      -- A_min: unsorted (key, s | o << 16) array in LDS, the
 //                       smallest key found by a wave min-reduction; A_l: a FIFO
 //                       ring of promoted requests in LDS.
@@ -296,6 +297,7 @@ struct SimState {
   uint64_t fr_mask;
   int32_t N, X, t_r, next_c, aw_base, aw_a, aw_rank, arr_ptr, next_a, f_rank, fw_base, f_u, fw_u;
   uint32_t f_key, f_so, fw_key, fw_so, v_key, v_so;
+  uint64_t f_word;
   int32_t nV, nVe, v_pos, v_head, v_u, n_done, retry_at, t, DT;
   int64_t rsteps, tot_ev;
 };
@@ -370,6 +372,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     int32_t aw_base = -64, aw_a = 0x7FFFFFFF, aw_rank = 0, arr_ptr = 0;
     int32_t next_a = 0;           // arrival step of request arr_ptr (0: look at step 0)
     int32_t f_rank = -1, fw_base = -1;
+    uint64_t f_word = 0ull;       // the bitmap word of f_rank (its LDS copy may still hold taken bits)
     uint32_t f_key = 0xFFFFFFFFu, f_so = 0, fw_key = 0xFFFFFFFFu, fw_so = 0;
     int32_t f_u = 0, fw_u = 0;
     int32_t nV = 0, nVe = 0, v_pos = -1, v_head = 0;
@@ -383,7 +386,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     if (FROM_STATE) {
       fr_row = st->fr_row; fr_mask = st->fr_mask; N = st->N; X = st->X; t_r = st->t_r; next_c = st->next_c;
       aw_base = st->aw_base; aw_a = st->aw_a; aw_rank = st->aw_rank; arr_ptr = st->arr_ptr; next_a = st->next_a;
-      f_rank = st->f_rank; fw_base = st->fw_base; f_key = st->f_key; f_so = st->f_so; fw_key = st->fw_key;
+      f_rank = st->f_rank; f_word = st->f_word; fw_base = st->fw_base; f_key = st->f_key; f_so = st->f_so; fw_key = st->fw_key;
       fw_so = st->fw_so; f_u = st->f_u; fw_u = st->fw_u;
       nV = st->nV; nVe = st->nVe; v_pos = st->v_pos; v_head = st->v_head; v_key = st->v_key; v_so = st->v_so;
       v_u = st->v_u; n_done = st->n_done; retry_at = st->retry_at; t = st->t; DT = st->DT;
@@ -400,7 +403,28 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       aw_rank = rank_of[i_];                                                         \
     }                                                                                \
   } while (0)
-    // smallest waiting fresh request: first set bit of the two-level bitmap
+    // the record of fresh rank f_rank from the 64-record window (reloaded when
+    // f_rank leaves it)
+#define SK_F_RECORD()                                                                \
+  do {                                                                               \
+    if (fw_base < 0 || f_rank < fw_base || f_rank >= fw_base + 64) {                 \
+      fw_base = f_rank;                                                              \
+      const int rr_ = fw_base + lane;                                                \
+      fw_key = 0xFFFFFFFFu;                                                          \
+      fw_so = 0u;                                                                    \
+      if (rr_ < n) {                                                                 \
+        const uint2 rv_ = rec[rr_];                                                  \
+        fw_key = rv_.x;                                                              \
+        fw_so = rv_.y;                                                               \
+        if (ALGO == SCHED_AELL) fw_u = upper_k[rr_];                                 \
+      }                                                                              \
+    }                                                                                \
+    f_key = wave::readlane_u(fw_key, f_rank - fw_base);                              \
+    f_so = wave::readlane_u(fw_so, f_rank - fw_base);                                \
+    if (ALGO == SCHED_AELL) f_u = wave::readlane(fw_u, f_rank - fw_base);            \
+  } while (0)
+    // smallest waiting fresh request: first set bit of the two-level bitmap in
+    // LDS; its word stays in scalar registers (f_word) while it has bits left
 #define SK_F_FIND()                                                                  \
   do {                                                                               \
     const uint64_t w1_ = lane < nw1 ? L1[lane] : 0ull;                               \
@@ -412,36 +436,51 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       const int j1_ = __builtin_ctzll(nz_);                                          \
       const uint64_t w1v_ = wave::readlane_u64(w1_, j1_);                            \
       const int j0_ = j1_ * 64 + __builtin_ctzll(w1v_);                              \
-      const uint64_t w0_ = uniform_u64(L0[j0_]);                                     \
-      f_rank = j0_ * 64 + __builtin_ctzll(w0_);                                      \
-      if (fw_base < 0 || f_rank < fw_base || f_rank >= fw_base + 64) {               \
-        fw_base = f_rank;                                                            \
-        const int rr_ = fw_base + lane;                                              \
-        fw_key = 0xFFFFFFFFu;                                                        \
-        fw_so = 0u;                                                                  \
-        if (rr_ < n) {                                                               \
-          const uint2 rv_ = rec[rr_];                                                \
-          fw_key = rv_.x;                                                            \
-          fw_so = rv_.y;                                                             \
-          if (ALGO == SCHED_AELL) fw_u = upper_k[rr_];                               \
-        }                                                                            \
-      }                                                                              \
-      f_key = wave::readlane_u(fw_key, f_rank - fw_base);                            \
-      f_so = wave::readlane_u(fw_so, f_rank - fw_base);                              \
-      if (ALGO == SCHED_AELL) f_u = wave::readlane(fw_u, f_rank - fw_base);          \
+      f_word = uniform_u64(L0[j0_]);                                                 \
+      f_rank = j0_ * 64 + __builtin_ctzll(f_word);                                   \
+      SK_F_RECORD();                                                                 \
     }                                                                                \
   } while (0)
-    // per-lane smallest cancelled entry over slots [FROM_, TO_): vb_k, vb_p, vb_s
+    // f_rank starts: it is the lowest bit of f_word.  The next one is the next
+    // bit of the same word (no LDS access); an emptied word is written back
+    // and leaves the summary level, and the search goes to the next word.
+#define SK_F_TAKE()                                                                  \
+  do {                                                                               \
+    f_word &= f_word - 1ull;                                                         \
+    if (f_word != 0ull) {                                                            \
+      f_rank = (f_rank & ~63) + __builtin_ctzll(f_word);                             \
+      SK_F_RECORD();                                                                 \
+    } else {                                                                         \
+      const int j0_ = f_rank >> 6;                                                   \
+      if (lane == 0) {                                                               \
+        L0[j0_] = 0ull;                                                              \
+        atomicAnd(reinterpret_cast<unsigned long long*>(&L1[j0_ >> 6]), ~(1ull << (j0_ & 63))); \
+      }                                                                              \
+      SK_F_FIND();                                                                   \
+    }                                                                                \
+  } while (0)
+    // per-lane smallest cancelled entry over slots [FROM_, TO_): vb_k, vb_p, vb_s.
+    // The loop runs over blocks of 128 slots with a uniform trip count (no
+    // per-lane exit), both loads of a block in flight at once; a slot past
+    // TO_ reads the last slot instead and counts as empty.
 #define SK_V_SCAN(FROM_, TO_)                                                        \
   uint32_t vb_k = 0xFFFFFFFFu, vb_s = 0u;                                            \
   int32_t vb_p = -1;                                                                 \
-  _Pragma("unroll 4") for (int j_ = (FROM_) + lane; j_ < (TO_); j_ += 64) {         \
-    const uint64_t ev_ = vent[j_];                                                   \
-    const uint32_t kk_ = static_cast<uint32_t>(ev_);                                 \
-    const bool lt_ = kk_ < vb_k;                                                     \
-    vb_k = lt_ ? kk_ : vb_k;                                                         \
-    vb_p = lt_ ? j_ : vb_p;                                                          \
-    vb_s = lt_ ? static_cast<uint32_t>(ev_ >> 32) : vb_s;                            \
+  for (int b_ = (FROM_); b_ < (TO_); b_ += 128) {                                    \
+    const int to_ = (TO_), last_ = to_ - 1;                                          \
+    const int j0_ = b_ + lane, j1_ = b_ + 64 + lane;                                 \
+    const uint64_t e0_ = vent[j0_ < last_ ? j0_ : last_];                            \
+    const uint64_t e1_ = vent[j1_ < last_ ? j1_ : last_];                            \
+    const uint32_t k0_ = j0_ < to_ ? static_cast<uint32_t>(e0_) : 0xFFFFFFFFu;       \
+    const uint32_t k1_ = j1_ < to_ ? static_cast<uint32_t>(e1_) : 0xFFFFFFFFu;       \
+    const bool l0_ = k0_ < vb_k;                                                     \
+    vb_k = l0_ ? k0_ : vb_k;                                                         \
+    vb_p = l0_ ? j0_ : vb_p;                                                         \
+    vb_s = l0_ ? static_cast<uint32_t>(e0_ >> 32) : vb_s;                            \
+    const bool l1_ = k1_ < vb_k;                                                     \
+    vb_k = l1_ ? k1_ : vb_k;                                                         \
+    vb_p = l1_ ? j1_ : vb_p;                                                         \
+    vb_s = l1_ ? static_cast<uint32_t>(e1_ >> 32) : vb_s;                            \
   }
     // smallest cancelled request that may start now (slots [0, nVe))
 #define SK_V_FIND()                                                                  \
@@ -564,6 +603,8 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       bool event = false;
       // ---- 1. arrivals; requests cancelled at the previous step become eligible
       if (t >= next_a) {
+        // the cached word goes back to LDS before arrivals set bits in it
+        if (f_rank >= 0 && lane == 0) L0[f_rank >> 6] = f_word;
         while (arr_ptr < n) {
           if (arr_ptr >= aw_base + 64) SK_LOAD_ARRIVALS();
           const bool take = (aw_base + lane >= arr_ptr) && aw_a <= t;
@@ -847,7 +888,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
               }
               st->fr_row = fr_row; st->fr_mask = fr_mask; st->N = N; st->X = X; st->t_r = t_r;
               st->next_c = next_c; st->aw_base = aw_base; st->aw_a = aw_a; st->aw_rank = aw_rank;
-              st->arr_ptr = arr_ptr; st->next_a = next_a; st->f_rank = f_rank; st->fw_base = fw_base;
+              st->arr_ptr = arr_ptr; st->next_a = next_a; st->f_rank = f_rank; st->f_word = f_word; st->fw_base = fw_base;
               st->f_key = f_key; st->f_so = f_so; st->fw_key = fw_key; st->fw_so = fw_so; st->f_u = f_u;
               st->fw_u = fw_u; st->nV = nV; st->nVe = nVe; st->v_pos = v_pos; st->v_head = v_head;
               st->v_key = v_key; st->v_so = v_so; st->v_u = v_u; st->n_done = n_done;
@@ -887,13 +928,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
         X += xw;
         N += 1;
         if (c_fromF) {
-          const int j0 = f_rank >> 6;
-          if (lane == 0) {
-            const uint64_t w = L0[j0] & ~(1ull << (f_rank & 63));
-            L0[j0] = w;
-            if (w == 0ull) L1[j0 >> 6] &= ~(1ull << (j0 & 63));
-          }
-          SK_F_FIND();
+          SK_F_TAKE();
         } else if (ALGO == SCHED_AELL) {
           v_head = v_head + 1 == P.cap_v ? 0 : v_head + 1;
           --nV;
@@ -1026,6 +1061,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
 #undef SK_LOAD_ARRIVALS
 #undef SK_PICK
 #undef SK_F_FIND
+#undef SK_F_RECORD
+#undef SK_F_TAKE
 #undef SK_V_FIND
 #undef SK_V_SCAN
 #undef SK_V_MERGE
