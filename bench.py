@@ -40,20 +40,39 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload: str, algo: str):
-    """HBM bytes per launch from the committed rocprofv3 --pmc summary, if it is
-    still current (same kernel source); otherwise None."""
+def load_profile(workload: str, algo: str) -> dict:
+    """The machine-readable figures of the committed rocprofv3 summary of this
+    kernel and workload, if it is still current (same kernel source); else {}."""
     path = os.path.join(ROOT, "profiles", f"{SIM_KERNEL}_{algo}_{workload}.md")
     if not os.path.exists(path):
-        return None
+        return {}
     text = open(path).read()
     if "```json" not in text:
-        return None
+        return {}
     block = text.split("```json", 1)[1].split("```", 1)[0]
     d = json.loads(block)
     if d.get("kernel_source_hash") != kernel_source_hash():
+        return {}
+    return d
+
+
+def load_traffic(workload: str, algo: str):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary (None if
+    absent or stale)."""
+    return load_profile(workload, algo).get("hbm_bytes_per_launch")
+
+
+def load_hardware_fraction(workload: str, algo: str):
+    """The chip's vector lane-cycle fraction over one launch, VALUBusy x
+    VALUUtilization from the committed rocprofv3 --pmc summary (None if absent
+    or stale): the issued-work counterpart of the algorithmic fraction."""
+    d = load_profile(workload, algo)
+    if "valu_busy_pct" not in d:
         return None
-    return d.get("hbm_bytes_per_launch")
+    return {"valu_lane_cycles": d["valu_busy_pct"] * d["valu_utilization_pct"] / 1e4,
+            "valu_busy_pct": d["valu_busy_pct"], "valu_utilization_pct": d["valu_utilization_pct"],
+            "lds_bank_conflict_pct": d.get("lds_bank_conflict_pct"),
+            "source": "rocprofv3 --pmc VALUBusy VALUUtilization (committed summary of this kernel source)"}
 
 
 def probe_peaks():
@@ -270,6 +289,7 @@ def main():
             "unit": "TOP/s",
             "frac": achieved / PEAK_INT32_LANE_OPS,
             "traffic": traffic,
+            "hardware_fraction": load_hardware_fraction(args.workload, args.algo),
             "kernel_ms": sim_avg_ms,
             "kernel_ms_median": float(np.median(sim_ms)),
             "ops_per_request_step": OPS_PER_REQUEST_STEP,

@@ -1,0 +1,53 @@
+"""Host-side pieces of bench.py: reading the committed rocprofv3 summaries.
+
+The roofline's `traffic` and `hardware_fraction` come from the machine-readable
+block of a profile only while its recorded kernel source hash matches the
+current source; a stale or missing summary gives None, never old figures."""
+import json
+import os
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+
+def _write_profile(tmp_path, fields):
+    d = tmp_path / "profiles"
+    d.mkdir(exist_ok=True)
+    body = "# summary\n\n```json\n" + json.dumps(fields, indent=1) + "\n```\n"
+    (d / "k_simulate_amin_wl.md").write_text(body)
+
+
+def test_current_profile_fields(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "x")
+    _write_profile(tmp_path, {"kernel_source_hash": "x", "hbm_bytes_per_launch": 123, "valu_busy_pct": 25.0,
+                              "valu_utilization_pct": 80.0, "lds_bank_conflict_pct": 0.05})
+    assert bench.load_traffic("wl", "amin") == 123
+    hw = bench.load_hardware_fraction("wl", "amin")
+    assert abs(hw["valu_lane_cycles"] - 0.2) < 1e-12
+    assert hw["lds_bank_conflict_pct"] == 0.05
+
+
+def test_stale_or_missing_profile_gives_none(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "current")
+    assert bench.load_traffic("wl", "amin") is None          # no file
+    _write_profile(tmp_path, {"kernel_source_hash": "older", "hbm_bytes_per_launch": 5,
+                              "valu_busy_pct": 1.0, "valu_utilization_pct": 1.0})
+    assert bench.load_traffic("wl", "amin") is None
+    assert bench.load_hardware_fraction("wl", "amin") is None
+
+
+def test_committed_profiles_parse():
+    # every committed summary carries a parseable block with the fields bench reads
+    d = os.path.join(ROOT, "profiles")
+    for name in os.listdir(d):
+        if not name.startswith("k_simulate_"):
+            continue
+        text = open(os.path.join(d, name)).read()
+        block = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+        assert isinstance(block["kernel_source_hash"], str)
+        assert block["hbm_bytes_per_launch"] > 0
