@@ -21,6 +21,10 @@ FLAGS = [
     "-Wall", "-Wno-unused-function",
     "-I" + os.path.join(ROOT, "include"),
 ]
+# The simulation kernels are latency-bound chains of dependent instructions on
+# one wave; LLVM's iterative ILP scheduling strategy measured 1-7% faster than
+# the default occupancy-first one on them (the probes keep the default).
+SIM_FLAGS = ["-mllvm", "--amdgpu-sched-strategy=iterative-ilp"]
 
 
 def _compile(sources, lib, verbose, extra):
@@ -34,7 +38,7 @@ def _compile(sources, lib, verbose, extra):
 
 def build(verbose: bool = True, extra=()) -> str:
     """Compile libschedsim.so and libschedprobe.so (always recompiles)."""
-    _compile(SOURCES, LIB, verbose, extra)
+    _compile(SOURCES, LIB, verbose, [*SIM_FLAGS, *extra])
     _compile(PROBE_SOURCES, PROBE_LIB, verbose, extra)
     return LIB
 
