@@ -293,6 +293,36 @@ def test_growth_random_sweep(B, seed, name):
         assert np.array_equal(g[f], g1[f]), f
 
 
+def _arrival_word_sweep(seed, K=128):
+    # fresh requests keep arriving while earlier ones wait: arrivals land in
+    # the bitmap word of the current smallest waiting rank (often below it:
+    # short outputs arriving late), words empty as their requests start and
+    # refill later; memory is tight so the waiting set stays long
+    rng = np.random.default_rng(1000 + seed)
+    M = int(rng.integers(80, 400))
+    insts = []
+    for _ in range(K):
+        n = int(rng.integers(60, 400))
+        o = rng.integers(1, int(rng.integers(4, 60)), n)
+        a = np.sort(rng.integers(0, int(rng.integers(1, 200)), n))
+        s = rng.integers(0, 6, n)
+        l = np.maximum(1, (o * rng.uniform(0.1, 1.0, n)).astype(int))
+        u = o + rng.integers(0, 10, n)
+        insts.append({"arrival": a, "prompt": s, "output": o, "lower": l, "upper": u,
+                      "priority": rng.permutation(n)})
+    return W.from_lists(M, insts, name=f"arrival_word_sweep{seed}")
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("name", ["amin", "amax", "hsf", "aell", "adaptive", "arandom"])
+def test_arrivals_into_waiting_words(B, seed, name):
+    algo = O.ALGOS[name]
+    batch = _arrival_word_sweep(seed)
+    ref = oracle_run(batch, algo)
+    assert (ref["status"] == 0).all()
+    assert_parity(batch, gpu_run(B, batch, algo), ref)
+
+
 def test_determinism_and_chunking(B):
     batch = W.generate("batch4096_n1000_m16384", 0, instance_ids=range(1000, 1300))
     a = gpu_run(B, batch, O.AMIN)
