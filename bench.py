@@ -96,6 +96,36 @@ def probe_peaks():
             "lds_read_TBs": l.value / 1e12, "lds_frac_of_published": l.value / PEAK_LDS_BYTES}
 
 
+def pipelined(db, algo, kw, ref_out, steps: int, nstreams: int = 3):
+    """Back-to-back batches with `nstreams` in flight (each on its own stream
+    with its own output buffers): the tail of one batch, where most SIMDs wait
+    for its slowest instances, overlaps the next batch.  Returns the time per
+    batch over `steps` batches and whether every stream's outputs equal the
+    serial run's."""
+    import torch
+    from paper_2508_14544_amd import binding as B
+    kw = {k: v for k, v in kw.items() if k != "stream"}
+    streams = [torch.cuda.Stream() for _ in range(nstreams)]
+    outs = [B.alloc_results(db) for _ in range(nstreams)]
+    for i in range(nstreams):   # warm-up: one batch per stream
+        B.simulate_into(db, algo, outs[i], stream=streams[i], **kw)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    main = torch.cuda.current_stream()
+    start.record(main)
+    for st in streams:
+        st.wait_event(start)
+    for i in range(steps):
+        B.simulate_into(db, algo, outs[i % nstreams], stream=streams[i % nstreams], **kw)
+    for st in streams:
+        main.wait_stream(st)
+    end.record(main)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    same = all(all(torch.equal(o[k], ref_out[k]) for k in o if o[k] is not None) for o in outs)
+    return ms, same
+
+
 def pinned_transfers(db, out, stream, reps: int = 3):
     """Median milliseconds of copying the batch's inputs from pinned host
     buffers into the resident device tensors, and the outputs back into pinned
@@ -206,6 +236,8 @@ def main():
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-peak-probe", action="store_true", help="skip the VALU/LDS throughput probes")
+    ap.add_argument("--pipeline-streams", type=int, default=3,
+                    help="batches in flight for the 'pipelined' figure (<= 1: skip it)")
     ap.add_argument("--instances", default="",
                     help="comma-separated instance ids: simulate only these (critical-path profiling)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -264,6 +296,8 @@ def main():
     sim_ms = [a.elapsed_ms(b) for a, b in ev]
     sim_avg_ms = sum(sim_ms) / len(sim_ms)
 
+    pipe_ms, pipe_same = (pipelined(db, algo, kw, out, args.steps, args.pipeline_streams)
+                          if args.pipeline_streams > 1 else (None, None))
     d0 = time.perf_counter()
     g = {k: (None if v is None else v.cpu().numpy()) for k, v in out.items()}
     d2h_ms = (time.perf_counter() - d0) * 1e3
@@ -337,6 +371,12 @@ def main():
             "pcie_inclusive_request_steps_per_s": rs / ((step_ms + pinned[0] + pinned[1]) / 1e3),
         },
         "wall_s_timed_region": wall,
+        "pipelined": (None if pipe_ms is None else {
+            "note": "the same batch simulated back to back with several batches in flight, one stream and "
+                    "one output set each: the tail of a batch overlaps the next; value and roofline above "
+                    "are one batch at a time",
+            "streams": args.pipeline_streams, "ms_per_step": pipe_ms,
+            "request_steps_per_s": rs / (pipe_ms / 1e3), "outputs_equal_serial": pipe_same}),
     }
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, os.cpu_count() or 1)
