@@ -139,7 +139,11 @@ typedef struct {
  * Returns SCHED_OK once the work is queued, or a call-level error code (then
  * nothing was queued).  Per-instance problems are reported in results.status;
  * other instances still run.  Scratch memory is allocated stream-ordered on
- * `stream` and released after the kernels (stream-ordered). */
+ * `stream` and released after the kernels (stream-ordered).  SCHED_ADAPTIVE
+ * runs its A_l instances on a second stream that the library creates once per
+ * device (default priority, kept until the process ends) and joins back into
+ * `stream` with events, so all of the call's work is ordered before whatever
+ * the caller queues on `stream` next. */
 int sched_simulate(const sched_instances_t* instances, sched_algo_t algo, int64_t M,
                    const sched_results_t* results, void* stream);
 

@@ -46,6 +46,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "schedsim.h"
 #include "wave.hpp"
@@ -1144,6 +1145,27 @@ hipError_t launch_sim_any(int algo, const Tier& tr, const sk::Params& P, size_t 
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+// A second stream per device (default priority, created on first use and kept
+// for the life of the process): the adaptive policy runs its A_l launches on
+// it while the A_min launches run on the caller's stream.  The two touch
+// disjoint instances.
+hipError_t side_stream(int dev, hipStream_t* out) {
+  constexpr int kMaxDev = 64;
+  static std::mutex mu;
+  static hipStream_t streams[kMaxDev] = {};
+  if (dev < 0 || dev >= kMaxDev) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!streams[dev]) {
+    const hipError_t e = hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking);
+    if (e != hipSuccess) {
+      streams[dev] = nullptr;
+      return e;
+    }
+  }
+  *out = streams[dev];
+  return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1304,16 +1326,38 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
       if (lds > 65536) err = set_lds_limit_any(sim_algos[a], tiers[pass], static_cast<int>(lds));
   }
   if (err == hipSuccess && o.event_before) err = hipEventRecord(static_cast<hipEvent_t>(o.event_before), st);
+  // adaptive: the A_l launches go to the side stream after the preparation,
+  // and the caller's stream waits for them before the end (fork and join)
+  hipStream_t side = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  if (err == hipSuccess && n_sim == 2) {
+    err = side_stream(dev, &side);
+    if (err == hipSuccess) err = hipEventCreateWithFlags(&fork, hipEventDisableTiming);
+    if (err == hipSuccess) err = hipEventCreateWithFlags(&join, hipEventDisableTiming);
+    if (err == hipSuccess) err = hipEventRecord(fork, st);
+    if (err == hipSuccess) err = hipStreamWaitEvent(side, fork, 0);
+  }
   for (int a = 0; a < n_sim && err == hipSuccess; ++a) {
     P.cap_v = cap_v_for(sim_algos[a]);
     const size_t lds = lds_for(sim_algos[a]);
+    const hipStream_t sa = a == 1 ? side : st;
     Tier tiers[3];
     const int n_tiers = tiers_for(tiers);
     for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass) {
       P.retry_status = pass + 1 < n_tiers ? sk::kRetry : SCHED_E_UNSUPPORTED;
-      err = launch_sim_any(sim_algos[a], tiers[pass], P, lds, st);
+      err = launch_sim_any(sim_algos[a], tiers[pass], P, lds, sa);
     }
   }
+  if (side) {
+    // join even after a failed launch, so that the workspace is not freed
+    // while work queued on the side stream may still use it
+    hipError_t je = join ? hipEventRecord(join, side) : hipErrorInvalidValue;
+    if (je == hipSuccess) je = hipStreamWaitEvent(st, join, 0);
+    if (je != hipSuccess) je = hipStreamSynchronize(side);
+    if (err == hipSuccess) err = je;
+  }
+  if (fork) (void)hipEventDestroy(fork);
+  if (join) (void)hipEventDestroy(join);
   if (err == hipSuccess && o.event_after) err = hipEventRecord(static_cast<hipEvent_t>(o.event_after), st);
   const hipError_t ferr = hipFreeAsync(ws, st);
   if (err != hipSuccess || ferr != hipSuccess) return SCHED_E_HIP;
