@@ -42,11 +42,13 @@ def test_stale_or_missing_profile_gives_none(tmp_path, monkeypatch):
 
 
 def test_committed_profiles_parse():
-    # every committed summary carries a parseable block with the fields bench reads
+    # the summaries bench reads (k_simulate_<policy>_<workload>.md) carry a
+    # parseable block with the fields it uses
     d = os.path.join(ROOT, "profiles")
-    for name in os.listdir(d):
-        if not name.startswith("k_simulate_"):
-            continue
+    policies = ("amin", "amax", "hsf", "aell", "adaptive", "arandom")
+    read = [n for n in os.listdir(d) if any(n.startswith(f"k_simulate_{a}_") for a in policies)]
+    assert "k_simulate_amin_batch4096_n1000_m16384.md" in read
+    for name in read:
         text = open(os.path.join(d, name)).read()
         block = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
         assert isinstance(block["kernel_source_hash"], str)
