@@ -164,10 +164,11 @@ int sched_simulate_opts(const sched_instances_t* instances, sched_algo_t algo, i
  * answer, since the search looks only for strictly better schedules).  Writes, per
  * instance, total_latency[K] and status[K] (SCHED_OK, SCHED_E_ARRIVAL,
  * SCHED_E_INTERVAL for o < 1 or s < 0, SCHED_E_TOO_BIG for s + o > M,
- * SCHED_E_INVAL for bad offsets, SCHED_E_STEP_CAP when the search exceeded
- * node_cap nodes (total_latency then holds the best schedule found, an upper
- * bound)), and, if nodes is not NULL, nodes[K] searched.  node_cap <= 0
- * selects 2^22.  Returns SCHED_E_UNSUPPORTED if max_requests > 8 (nothing
+ * SCHED_E_INVAL for bad offsets, SCHED_E_UNSUPPORTED when max a + sum(o + 1)
+ * reaches 2^27, SCHED_E_STEP_CAP when the search exceeded node_cap nodes
+ * (total_latency then holds the best schedule found, an upper bound)), and,
+ * if nodes is not NULL, nodes[K] searched.  node_cap <= 0 selects 2^22; larger
+ * budgets are clamped to 2^31 - 1.  Returns SCHED_E_UNSUPPORTED if max_requests > 8 (nothing
  * queued), SCHED_E_INVAL for NULL pointers or M outside (0, 2^30). */
 int sched_optimum(const sched_instances_t* instances, int64_t M, const int64_t* upper_bound,
                   int64_t* total_latency, int32_t* status, int64_t* nodes, int64_t node_cap, void* stream);

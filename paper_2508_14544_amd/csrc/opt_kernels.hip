@@ -9,7 +9,11 @@
 //   * a start is feasible iff the total stays <= M at the completion step of
 //     every placed run that overlaps the new one and at the new run's own
 //     completion (between two completions the set of present runs only grows
-//     and each run's memory grows, so the maximum is at a completion);
+//     and each run's memory grows, so the maximum is at a completion).  The
+//     memory at each placed run's completion is kept up to date as runs are
+//     placed and removed, so a test costs O(depth);
+//   * each depth is its own template instance, so every array index is a
+//     compile-time constant and the search state stays in registers;
 //   * the cost of a partial assignment plus the remaining requests' output
 //     lengths bounds any completion from below, and the cost grows with the
 //     start, so the first start that reaches the best total ends the level;
@@ -19,7 +23,8 @@
 //     request identical to the previous one never starts before it (swapping
 //     them gives the same schedule);
 //   * starts range over [a_i, max a + sum(o + 1) + 1], a horizon within which
-//     the sequential schedule already finishes every request.
+//     the sequential schedule already finishes every request (an instance
+//     whose horizon reaches 2^27 is not searched: SCHED_E_UNSUPPORTED).
 // A node budget per instance guarantees every lane reaches the exit.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -29,6 +34,9 @@
 namespace opt {
 
 constexpr int kMaxN = 8;
+// starts, ends and memory sums are int32: the horizon (max a + sum(o + 1) + 1)
+// must stay below this
+constexpr int64_t kHorizonLimit = int64_t(1) << 27;
 
 struct OptParams {
   int32_t K;
@@ -45,102 +53,166 @@ struct OptParams {
   int64_t* nodes;
 };
 
-__global__ __launch_bounds__(64) void k_optimum(OptParams P) {
+// One instance, sorted into search order.
+struct Inst {
+  int32_t a[kMaxN], s[kMaxN], o[kMaxN];
+  int32_t rem[kMaxN + 1];   // rem[i] = o[i] + ... + o[n-1]
+  uint32_t same;            // bit i: request i equals request i-1
+  int n;
+  int32_t M;
+  int32_t horizon;          // < kHorizonLimit
+};
+
+// The search state.  mem[q] is the memory at the completion step of placed
+// run q from every run placed so far (kept exact as runs are placed and
+// removed), so testing a start costs O(depth).  Runs are kept by completion
+// step (a start is c - o).
+struct Search {
+  int32_t c[kMaxN];         // completion step p + o of each placed run
+  int32_t mem[kMaxN];
+  int32_t best;             // below 8 * kHorizonLimit = 2^30
+  int32_t nodes, cap;       // the budget is clamped to 2^31 - 1
+  bool stop;
+};
+
+// Level D places request D, runs 0..D-1 being placed at total cost `cost`.
+// Every array index below is a compile-time constant, so the state stays in
+// registers.
+template <int D>
+__device__ __forceinline__ void place(const Inst& I, Search& S, int32_t cost) {
+  if constexpr (D < kMaxN) {
+    const int32_t lo = (D > 0 && ((I.same >> D) & 1u)) ? S.c[D > 0 ? D - 1 : 0] - I.o[D > 0 ? D - 1 : 0] : I.a[D];
+    for (int32_t pd = lo;; ++pd) {
+      // the placed runs are re-read every iteration rather than hoisted out of
+      // the loop: hoisted copies would stay live across every deeper level
+#pragma unroll
+      for (int q = 0; q < D; ++q) asm volatile("" : "+v"(S.c[q]), "+v"(S.mem[q]));
+      if (++S.nodes > S.cap) {
+        S.stop = true;
+        return;
+      }
+      const int32_t c = cost + (pd + I.o[D] - I.a[D]);
+      if (pd > I.horizon || c + I.rem[D + 1] >= S.best) return;  // later starts only cost more
+      const int32_t end = pd + I.o[D];
+      bool ok = true;
+      int32_t mend = I.s[D] + I.o[D];
+#pragma unroll
+      for (int q = 0; q < D; ++q) {
+        const int32_t cq = S.c[q], pq = cq - I.o[q];
+        if (cq >= pd && cq <= end) ok = ok && S.mem[q] + I.s[D] + (cq - pd) <= I.M;
+        if (pq <= end && end <= cq) mend += I.s[q] + (end - pq);
+      }
+      if (!ok || mend > I.M) continue;
+      if (D == I.n - 1) {
+        S.best = c;  // a complete schedule; later starts here cost more
+        return;
+      }
+      S.c[D] = end;
+#pragma unroll
+      for (int q = 0; q < D; ++q) {
+        const int32_t cq = S.c[q];
+        if (cq >= pd && cq <= end) S.mem[q] += I.s[D] + (cq - pd);
+      }
+      S.mem[D] = mend;
+      place<D + 1>(I, S, c);
+#pragma unroll
+      for (int q = 0; q < D; ++q) {
+        const int32_t cq = S.c[q];
+        if (cq >= pd && cq <= end) S.mem[q] -= I.s[D] + (cq - pd);
+      }
+      if (S.stop) return;
+    }
+  }
+}
+
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_optimum(OptParams P) {
   const int k = blockIdx.x * 64 + threadIdx.x;
   if (k >= P.K) return;
   const int64_t b = P.offsets[k];
   const int64_t e = P.offsets[k + 1];
   int status = SCHED_OK;
-  int64_t best = 0, nodes = 0;
+  Search S;
+  S.best = 0;
+  S.nodes = 0;
+  S.cap = static_cast<int32_t>(P.node_cap < 0x7FFFFFFF ? P.node_cap : 0x7FFFFFFF);
+  S.stop = false;
   if (b < 0 || e < b || e > P.N) status = SCHED_E_INVAL;
   const int n = status == SCHED_OK ? static_cast<int>(e - b) : 0;
   if (n > kMaxN) status = SCHED_E_UNSUPPORTED;
-  int32_t a[kMaxN], s[kMaxN], o[kMaxN], p[kMaxN];
-  int64_t cost[kMaxN + 1], rem[kMaxN + 1];
+  Inst I;
+  I.n = n;
+  I.M = P.M;
   if (status == SCHED_OK && n > 0) {
     bool arr_bad = false, int_bad = false, big_bad = false;
     int64_t amax = 0, span = 0;
 #pragma unroll
     for (int i = 0; i < kMaxN; ++i) {
-      a[i] = 0; s[i] = 0; o[i] = 1;
+      I.a[i] = 0; I.s[i] = 0; I.o[i] = 1;
       if (i < n) {
-        a[i] = P.arrival ? P.arrival[b + i] : 0;
-        s[i] = P.prompt[b + i];
-        o[i] = P.output[b + i];
-        if (a[i] < 0 || (i > 0 && a[i] < a[i - 1])) arr_bad = true;
-        if (o[i] < 1 || s[i] < 0) int_bad = true;
-        if (static_cast<int64_t>(s[i]) + o[i] > P.M) big_bad = true;
-        amax = a[i] > amax ? a[i] : amax;
-        span += static_cast<int64_t>(o[i]) + 1;
+        I.a[i] = P.arrival ? P.arrival[b + i] : 0;
+        I.s[i] = P.prompt[b + i];
+        I.o[i] = P.output[b + i];
+        if (I.a[i] < 0 || (i > 0 && I.a[i] < I.a[i > 0 ? i - 1 : 0])) arr_bad = true;
+        if (I.o[i] < 1 || I.s[i] < 0) int_bad = true;
+        if (static_cast<int64_t>(I.s[i]) + I.o[i] > P.M) big_bad = true;
+        amax = I.a[i] > amax ? I.a[i] : amax;
+        span += static_cast<int64_t>(I.o[i]) + 1;
       }
     }
     status = arr_bad ? SCHED_E_ARRIVAL : int_bad ? SCHED_E_INTERVAL : big_bad ? SCHED_E_TOO_BIG : SCHED_OK;
+    if (status == SCHED_OK && amax + span + 1 >= kHorizonLimit) status = SCHED_E_UNSUPPORTED;
     if (status == SCHED_OK) {
-      const int64_t horizon = amax + span + 1;
+      I.horizon = static_cast<int32_t>(amax + span + 1);
       // first bound: one request at a time, each after the previous completes
-      int64_t t = 0;
-      for (int i = 0; i < n; ++i) {
-        const int64_t start = t > a[i] ? t : a[i];
-        best += start + o[i] - a[i];
-        t = start + o[i] + 1;
-      }
-      if (P.upper_bound && P.upper_bound[k] > 0 && P.upper_bound[k] < best) best = P.upper_bound[k];
+      int32_t t = 0;
+#pragma unroll
+      for (int i = 0; i < kMaxN; ++i)
+        if (i < n) {
+          const int32_t start = t > I.a[i] ? t : I.a[i];
+          S.best += start + I.o[i] - I.a[i];
+          t = start + I.o[i] + 1;
+        }
+      if (P.upper_bound && P.upper_bound[k] > 0 && P.upper_bound[k] < S.best)
+        S.best = static_cast<int32_t>(P.upper_bound[k]);
       // search order: arrival, then the largest s + o, then the longest o
       // first (big runs placed early prune the most); the optimum does not
-      // depend on it, and equal keys mean identical requests
-      for (int i = 1; i < n; ++i)
-        for (int j = i; j > 0; --j) {
-          const int32_t wj = s[j] + o[j], wp = s[j - 1] + o[j - 1];
-          const bool gt = a[j - 1] > a[j] || (a[j - 1] == a[j] && (wp < wj || (wp == wj && o[j - 1] < o[j])));
-          if (!gt) break;
-          const int32_t ta = a[j], ts = s[j], to = o[j];
-          a[j] = a[j - 1]; s[j] = s[j - 1]; o[j] = o[j - 1];
-          a[j - 1] = ta; s[j - 1] = ts; o[j - 1] = to;
-        }
-      rem[n] = 0;
-      for (int i = n - 1; i >= 0; --i) rem[i] = rem[i + 1] + o[i];
-      int d = 0;
-      cost[0] = 0;
-      p[0] = a[0] - 1;
-      while (d >= 0) {
-        if (++nodes > P.node_cap) {
-          status = SCHED_E_STEP_CAP;
-          break;
-        }
-        const int64_t pd = ++p[d];
-        const int64_t c = cost[d] + pd + o[d] - a[d];
-        if (pd > horizon || c + rem[d + 1] >= best) {
-          --d;  // later starts at this level only cost more
-          continue;
-        }
-        // feasibility of run d starting at pd against runs 0..d-1
-        const int64_t end = pd + o[d];
-        bool ok = true;
-        for (int q = 0; q <= d && ok; ++q) {
-          const int64_t cq = q < d ? static_cast<int64_t>(p[q]) + o[q] : end;
-          if (cq < pd || cq > end) continue;
-          int64_t mem = s[d] + cq - pd;
-          for (int j = 0; j < d; ++j)
-            if (p[j] <= cq && cq <= static_cast<int64_t>(p[j]) + o[j]) mem += s[j] + cq - p[j];
-          ok = mem <= P.M;
-        }
-        if (!ok) continue;
-        if (d == n - 1) {
-          best = c;  // a complete schedule; larger starts here cost more
-          --d;
-          continue;
-        }
-        cost[d + 1] = c;
-        ++d;
-        const bool same = a[d] == a[d - 1] && s[d] == s[d - 1] && o[d] == o[d - 1];
-        p[d] = (same ? p[d - 1] : a[d]) - 1;
+      // depend on it, and equal keys mean identical requests.  A fixed
+      // compare-exchange network over the first n slots (odd-even
+      // transposition, n passes) keeps every index static.
+#pragma unroll
+      for (int pass = 0; pass < kMaxN; ++pass)
+#pragma unroll
+        for (int j = pass & 1; j + 1 < kMaxN; j += 2)
+          if (j + 1 < n) {
+            const int32_t wj = I.s[j + 1] + I.o[j + 1], wp = I.s[j] + I.o[j];
+            const bool gt = I.a[j] > I.a[j + 1] ||
+                            (I.a[j] == I.a[j + 1] && (wp < wj || (wp == wj && I.o[j] < I.o[j + 1])));
+            if (gt) {
+              const int32_t ta = I.a[j + 1], ts = I.s[j + 1], to = I.o[j + 1];
+              I.a[j + 1] = I.a[j]; I.s[j + 1] = I.s[j]; I.o[j + 1] = I.o[j];
+              I.a[j] = ta; I.s[j] = ts; I.o[j] = to;
+            }
+          }
+      I.rem[kMaxN] = 0;
+#pragma unroll
+      for (int i = kMaxN - 1; i >= 0; --i) I.rem[i] = I.rem[i + 1] + (i < n ? I.o[i] : 0);
+      I.same = 0u;
+#pragma unroll
+      for (int i = 1; i < kMaxN; ++i)
+        if (i < n && I.a[i] == I.a[i - 1] && I.s[i] == I.s[i - 1] && I.o[i] == I.o[i - 1]) I.same |= 1u << i;
+#pragma unroll
+      for (int i = 0; i < kMaxN; ++i) {
+        S.c[i] = 0;
+        S.mem[i] = 0;
       }
+      place<0>(I, S, 0);
+      if (S.stop) status = SCHED_E_STEP_CAP;
     }
   }
-  if (status != SCHED_OK && status != SCHED_E_STEP_CAP) best = 0;
-  P.total_latency[k] = best;
+  if (status != SCHED_OK && status != SCHED_E_STEP_CAP) S.best = 0;
+  P.total_latency[k] = S.best;
   P.status[k] = status;
-  if (P.nodes) P.nodes[k] = nodes;
+  if (P.nodes) P.nodes[k] = S.nodes;
 }
 
 }  // namespace opt

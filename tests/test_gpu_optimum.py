@@ -72,10 +72,11 @@ def test_closed_forms(B):
 
 def test_statuses_and_node_cap(B):
     good = {"arrival": [0, 0, 1], "prompt": [1, 2, 1], "output": [3, 2, 4]}
+    # the last one: a search horizon (max a + sum(o + 1) + 1) of 2^27 is not searched
     insts = [good, dict(good, arrival=[1, 0, 1]), dict(good, output=[0, 2, 4]), dict(good, prompt=[1, 2, 9]),
-             {"arrival": [], "prompt": [], "output": []}]
+             {"arrival": [], "prompt": [], "output": []}, dict(good, arrival=[(1 << 27) - 10] * 3)]
     r = gpu_opt(B, W.from_lists(10, insts, name="opt_status"))
-    assert r["status"].tolist() == [0, O.E_ARRIVAL, O.E_INTERVAL, O.E_TOO_BIG, 0]
+    assert r["status"].tolist() == [0, O.E_ARRIVAL, O.E_INTERVAL, O.E_TOO_BIG, 0, B.E_UNSUPPORTED]
     assert r["tel"][0] == O.opt_tel(good, 10) and r["tel"][4] == 0
     b = W.random_small(3, 20, 8, s_max=2, o_max=8, M=14, arrivals=False)
     capped = gpu_opt(B, b, node_cap=5)
