@@ -314,6 +314,10 @@ template <int ALGO, int ROWS, bool FROM_STATE = false, bool TO_STATE = false>
 __device__ __forceinline__ int sim_instance(const Params& P, const int k, const int st0, const int retry_status,
                                            SimState* st = nullptr) {
   static_assert(!(FROM_STATE || TO_STATE) || ROWS <= kStateRows, "state holds at most kStateRows rows");
+  // only A_min and A_l have cancelled (or promoted) requests waiting: for the
+  // other policies every head is fresh, and the code of the cancelled set is
+  // left out of their kernels
+  constexpr bool kHasV = ALGO == SCHED_AMIN || ALGO == SCHED_AELL;
   extern __shared__ uint64_t lds64[];
   const int lane = threadIdx.x;
   const int64_t b = P.offsets[k];
@@ -534,8 +538,8 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     // (A_l: every fresh request comes before the promoted ones); derived where
     // it is used rather than carried through the loop
 #define SK_PICK()                                                                    \
-  const bool c_any = f_rank >= 0 || v_pos >= 0;                                      \
-  const bool c_fromF = f_rank >= 0 && (ALGO == SCHED_AELL || f_key < v_key);         \
+  const bool c_any = f_rank >= 0 || (kHasV && v_pos >= 0);                           \
+  const bool c_fromF = !kHasV || (f_rank >= 0 && (ALGO == SCHED_AELL || f_key < v_key)); \
   const uint32_t c_key = c_fromF ? f_key : v_key;                                    \
   const uint32_t c_so = c_fromF ? f_so : v_so;                                       \
   const int32_t c_s = static_cast<int32_t>(c_so & 0xFFFFu);                          \
