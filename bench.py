@@ -236,8 +236,10 @@ def main():
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-peak-probe", action="store_true", help="skip the VALU/LDS throughput probes")
-    ap.add_argument("--pipeline-streams", type=int, default=3,
-                    help="batches in flight for the 'pipelined' figure (<= 1: skip it)")
+    # off by default, so that every launch of the default run is one batch at a
+    # time and a kernel trace of it averages the same launches as `roofline`
+    ap.add_argument("--pipeline-streams", type=int, default=0,
+                    help="batches in flight for the 'pipelined' figure (<= 1: skip it; e.g. 3)")
     ap.add_argument("--instances", default="",
                     help="comma-separated instance ids: simulate only these (critical-path profiling)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
