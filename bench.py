@@ -26,6 +26,8 @@ sys.path.insert(0, ROOT)
 # MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = int32 VALU lane-operations per second
 PEAK_INT32_LANE_OPS = 256 * 4 * 16 * 2.4e9
 PEAK_LDS_BYTES = 256 * 128 * 2.4e9
+# widest LDS access of the simulation kernel: ds_read_b64 over 64 lanes
+LDS_BYTES_PER_INST_MAX = 64 * 8
 # algorithmic int32 lane-operations per simulated request-step: completion compare,
 # projected-memory add, and the head test's planned-end compare, max, end compare, add
 OPS_PER_REQUEST_STEP = 6
@@ -64,17 +66,25 @@ def load_traffic(workload: str, algo: str):
     return load_profile(workload, algo).get("hbm_bytes_per_launch")
 
 
-def load_hardware_fraction(workload: str, algo: str):
+def load_hardware_fraction(workload: str, algo: str, kernel_ms: float = 0.0):
     """The chip's vector lane-cycle fraction over one launch, VALUBusy x
     VALUUtilization from the committed rocprofv3 --pmc summary (None if absent
-    or stale): the issued-work counterpart of the algorithmic fraction."""
+    or stale): the issued-work counterpart of the algorithmic fraction.  With
+    the launch's duration, also an upper bound on its LDS bandwidth: every LDS
+    instruction of the kernel (SQ_INSTS_LDS) moves at most 8 B per lane of a
+    wave64 (ds_read_b64 is its widest), against the LDS peak."""
     d = load_profile(workload, algo)
     if "valu_busy_pct" not in d:
         return None
-    return {"valu_lane_cycles": d["valu_busy_pct"] * d["valu_utilization_pct"] / 1e4,
-            "valu_busy_pct": d["valu_busy_pct"], "valu_utilization_pct": d["valu_utilization_pct"],
-            "lds_bank_conflict_pct": d.get("lds_bank_conflict_pct"),
-            "source": "rocprofv3 --pmc VALUBusy VALUUtilization (committed summary of this kernel source)"}
+    out = {"valu_lane_cycles": d["valu_busy_pct"] * d["valu_utilization_pct"] / 1e4,
+           "valu_busy_pct": d["valu_busy_pct"], "valu_utilization_pct": d["valu_utilization_pct"],
+           "lds_bank_conflict_pct": d.get("lds_bank_conflict_pct"),
+           "source": "rocprofv3 --pmc VALUBusy VALUUtilization (committed summary of this kernel source)"}
+    if "lds_insts_per_launch" in d and kernel_ms > 0:
+        lds_bytes = d["lds_insts_per_launch"] * LDS_BYTES_PER_INST_MAX
+        out["lds_bytes_per_launch_max"] = lds_bytes
+        out["lds_frac_max"] = lds_bytes / (kernel_ms * 1e-3) / PEAK_LDS_BYTES
+    return out
 
 
 def probe_peaks():
@@ -358,7 +368,7 @@ def main():
             "unit": "TOP/s",
             "frac": achieved / PEAK_INT32_LANE_OPS,
             "traffic": traffic,
-            "hardware_fraction": load_hardware_fraction(args.workload, args.algo),
+            "hardware_fraction": load_hardware_fraction(args.workload, args.algo, sim_avg_ms),
             "kernel_ms": sim_avg_ms,
             "kernel_ms_median": float(np.median(sim_ms)),
             "ops_per_request_step": OPS_PER_REQUEST_STEP,

@@ -29,6 +29,18 @@ def test_current_profile_fields(tmp_path, monkeypatch):
     hw = bench.load_hardware_fraction("wl", "amin")
     assert abs(hw["valu_lane_cycles"] - 0.2) < 1e-12
     assert hw["lds_bank_conflict_pct"] == 0.05
+    assert "lds_frac_max" not in hw           # no LDS instruction count in this summary
+
+
+def test_lds_bound_from_instruction_count(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "x")
+    _write_profile(tmp_path, {"kernel_source_hash": "x", "hbm_bytes_per_launch": 1, "valu_busy_pct": 10.0,
+                              "valu_utilization_pct": 50.0, "lds_insts_per_launch": 1e6})
+    hw = bench.load_hardware_fraction("wl", "amin", kernel_ms=2.0)
+    # 1e6 wave64 instructions x 8 B x 64 lanes over 2 ms, against 256 CUs x 128 B x 2.4 GHz
+    assert hw["lds_bytes_per_launch_max"] == 1e6 * 512
+    assert abs(hw["lds_frac_max"] - (512e6 / 2e-3) / (256 * 128 * 2.4e9)) < 1e-15
 
 
 def test_stale_or_missing_profile_gives_none(tmp_path, monkeypatch):
