@@ -338,6 +338,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": step_ms,
+        # the same step counted in instances advanced by one step (sum of makespans)
+        "instance_steps_per_s": int(g["makespan"].astype(np.int64).sum()) / (step_ms / 1e3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
