@@ -60,7 +60,7 @@ def _load():
             P32 = ctypes.POINTER(ctypes.c_int32)
             P64 = ctypes.POINTER(ctypes.c_int64)
             lib.orc_simulate.restype = ctypes.c_int
-            lib.orc_simulate.argtypes = [ctypes.c_int32, P32, P32, P32, P32, P32, P32, ctypes.c_int32,
+            lib.orc_simulate.argtypes = [ctypes.c_int32, P32, P32, P32, P32, P32, P32, P32, ctypes.c_int32,
                                          ctypes.c_int64, ctypes.c_int64, P32, P32, P64, P64, P64,
                                          P64, P64, ctypes.POINTER(_Event), ctypes.c_int64, P64]
             lib.orc_default_step_cap.restype = ctypes.c_int64
@@ -93,6 +93,7 @@ def simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap: int = 
     lo = _c32(inst.get("lower"))
     up = _c32(inst.get("upper"))
     pr = _c32(inst.get("priority"))
+    tk = _c32(inst.get("tie_key"))
     comp = np.empty(n, np.int32)
     ev = np.empty(n, np.int32)
     tel, mk, rs, te, nev = (ctypes.c_int64() for _ in range(5))
@@ -103,13 +104,13 @@ def simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap: int = 
         cap_ev = 1 << 16
         evbuf = (_Event * cap_ev)()
     P64 = ctypes.POINTER(ctypes.c_int64)
-    status = lib.orc_simulate(n, _p32(a), _p32(s), _p32(o), _p32(lo), _p32(up), _p32(pr), int(algo), int(M),
+    status = lib.orc_simulate(n, _p32(a), _p32(s), _p32(o), _p32(lo), _p32(up), _p32(pr), _p32(tk), int(algo), int(M),
                               int(step_cap), _p32(comp), _p32(ev), ctypes.byref(tel), ctypes.byref(mk),
                               ctypes.byref(rs), ctypes.byref(te), st_arr.ctypes.data_as(P64),
                               evbuf if events else ctypes.POINTER(_Event)(), cap_ev, ctypes.byref(nev))
     if events and nev.value > cap_ev:
         evbuf = (_Event * nev.value)()
-        status = lib.orc_simulate(n, _p32(a), _p32(s), _p32(o), _p32(lo), _p32(up), _p32(pr), int(algo), int(M),
+        status = lib.orc_simulate(n, _p32(a), _p32(s), _p32(o), _p32(lo), _p32(up), _p32(pr), _p32(tk), int(algo), int(M),
                                   int(step_cap), _p32(comp), _p32(ev), ctypes.byref(tel), ctypes.byref(mk),
                                   ctypes.byref(rs), ctypes.byref(te), st_arr.ctypes.data_as(P64),
                                   evbuf, nev.value, ctypes.byref(nev))
@@ -146,7 +147,13 @@ def simulate_batch(batch, algo: int, *, instances: Optional[Sequence[int]] = Non
     per-instance arrays.
     """
     ks = list(range(batch.num_instances)) if instances is None else list(instances)
-    threads = threads or min(16, os.cpu_count() or 1)
+    if not threads:
+        # every CPU this process may use, capped by OMP_NUM_THREADS where the
+        # host sets one (a share of a larger machine)
+        threads = len(os.sched_getaffinity(0))
+        env = os.environ.get("OMP_NUM_THREADS", "")
+        if env.isdigit() and int(env) > 0:
+            threads = min(threads, int(env))
 
     def one(k):
         return simulate(batch.instance(k), algo, batch.M, step_cap=step_cap, stats=stats)
@@ -180,10 +187,10 @@ def literal_simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap
     rising to the tokens it had generated; for A_l a run that has generated l
     tokens without finishing is removed, plans with u from then on and goes to
     the back of the queue (fresh requests first, promoted ones in promotion
-    order, same step by index) and may restart at once; then waiting requests
-    are taken in (planning length, index) order (A_l: queue order) while
-    equation (2) keeps holding.  ADAPTIVE runs the algorithm adaptive_choice
-    picks.
+    order, same step by fresh-queue position) and may restart at once; then
+    waiting requests are taken in (planning length, tie key, index) order (A_l:
+    queue order) while equation (2) keeps holding.  ADAPTIVE runs the
+    algorithm adaptive_choice picks.  Without a tie key, ties go by index.
     """
     if algo == ADAPTIVE:
         algo = adaptive_choice(inst)
@@ -199,7 +206,12 @@ def literal_simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap
         plan = [int(x) for x in inst["lower"]]
     upper = [int(x) for x in inst["upper"]] if inst.get("upper") is not None else None
     cap = step_cap if step_cap > 0 else default_step_cap(inst)
-    queue_pos = list(range(n))   # A_l order: fresh by index, then promotion order
+    # equal planning lengths: by the caller's tie key, then by index
+    tie = [int(x) for x in inst["tie_key"]] if inst.get("tie_key") is not None else [0] * n
+    # A_l order: fresh requests by (arrival, tie, index), then promotion order
+    queue_pos = [0] * n
+    for pos, i in enumerate(sorted(range(n), key=lambda r: (arr[r], tie[r], r))):
+        queue_pos[i] = pos
     promotions = 0
 
     start = {}                  # request -> current start step (running only)
@@ -227,7 +239,7 @@ def literal_simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap
             break
         if algo == AMIN:
             proj = sum(s[i] + (t + 1) - start[i] for i in start)
-            for i in sorted(start, key=lambda r: (plan[r], r)):
+            for i in sorted(start, key=lambda r: (plan[r], tie[r], r)):
                 if proj <= M:
                     break
                 proj -= s[i] + (t + 1) - start[i]
@@ -237,7 +249,8 @@ def literal_simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap
                 waiting.append(i)
                 eligible_from[i] = t + 1
         if algo == AELL:
-            for i in sorted(r for r in start if start[r] + plan[r] == t):
+            # same-step promotions in fresh-queue order (each request is promoted once)
+            for i in sorted((r for r in start if start[r] + plan[r] == t), key=lambda r: queue_pos[r]):
                 plan[i] = upper[i]
                 queue_pos[i] = n + promotions
                 promotions += 1
@@ -252,9 +265,9 @@ def literal_simulate(inst: Dict[str, Sequence[int]], algo: int, M: int, step_cap
         if algo == AELL:
             order_key = lambda r: (queue_pos[r], r)
         elif algo == ARANDOM:
-            order_key = lambda r: (int(inst["priority"][r]), r)
+            order_key = lambda r: (int(inst["priority"][r]), tie[r], r)
         else:
-            order_key = lambda r: (plan[r], r)
+            order_key = lambda r: (plan[r], tie[r], r)
         order = sorted((w for w in waiting if eligible_from[w] <= t), key=order_key)
         chosen: List[int] = []
         for w in order:

@@ -29,7 +29,9 @@
  *   memory of a run counts at both its start and its completion step; a
  *   request completing at t still occupies s+o at t; the admitted set is the
  *   longest feasible prefix of the waiting requests in key order; ties break by
- *   ascending request index; an evicted request waits and may restart from
+ *   the caller's tie key if one is given, then by ascending request index (the
+ *   paper breaks them uniformly at random; a random tie key is such an order);
+ *   an evicted request waits and may restart from
  *   t+1; o~ <- max(o~, tokens generated); online arrivals join the waiting set
  *   at their arrival step and latency is measured from arrival.
  */
@@ -41,9 +43,9 @@
 enum { NOT_ARRIVED = 0, WAITING = 1, RUNNING = 2, DONE = 3 };
 
 /* ---------------------------------------------------------------------------
- * Waiting set: binary min-heap of request indices ordered by (key, index), where
- * key is the planning length (A_max, A_min, H-SF), the queue position (A_l) or
- * the priority (A_random).
+ * Waiting set: binary min-heap of request indices ordered by (key, tie, index),
+ * where key is the planning length (A_max, A_min, H-SF), the queue position
+ * (A_l) or the priority (A_random), and tie the caller's tie key (if any).
  * Only "peek the smallest" and "remove the smallest" are needed, because the
  * admission walk stops at the first request that does not fit.
  * ------------------------------------------------------------------------- */
@@ -51,10 +53,12 @@ typedef struct {
   int32_t* idx;
   int64_t size;
   const int64_t* key;
+  const int32_t* tie; /* tie-break before the index; NULL = index only */
 } heap_t;
 
 static int key_less(const heap_t* h, int32_t x, int32_t y) {
   if (h->key[x] != h->key[y]) return h->key[x] < h->key[y];
+  if (h->tie && h->tie[x] != h->tie[y]) return h->tie[x] < h->tie[y];
   return x < y;
 }
 
@@ -106,8 +110,12 @@ static int feasible(int64_t nq, const int64_t* qp, const int64_t* qs, const int6
   return 1;
 }
 
+/* Sort record: the eviction order (o~, tie, index) of A_min, A_l's fresh-queue
+ * order (arrival, tie, index) and its same-step promotion order (queue
+ * position) all sort (key, tie, i) triples. */
 typedef struct {
   int32_t i;
+  int32_t tie;
   int64_t key_est;
 } evict_key_t;
 
@@ -115,12 +123,8 @@ static int cmp_evict(const void* x, const void* y) {
   const evict_key_t* a = (const evict_key_t*)x;
   const evict_key_t* b = (const evict_key_t*)y;
   if (a->key_est != b->key_est) return a->key_est < b->key_est ? -1 : 1;
+  if (a->tie != b->tie) return a->tie < b->tie ? -1 : 1;
   return a->i < b->i ? -1 : (a->i > b->i);
-}
-
-static int cmp_index(const void* x, const void* y) {
-  const int32_t a = *(const int32_t*)x, b = *(const int32_t*)y;
-  return a < b ? -1 : (a > b);
 }
 
 int64_t orc_default_step_cap(int32_t n, const int32_t* a, const int32_t* o) {
@@ -180,7 +184,8 @@ int32_t orc_adaptive_choice(int32_t n, const int32_t* l, const int32_t* u) {
 }
 
 int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o,
-                 const int32_t* l, const int32_t* u, const int32_t* prio, int32_t algo, int64_t M,
+                 const int32_t* l, const int32_t* u, const int32_t* prio, const int32_t* tie,
+                 int32_t algo, int64_t M,
                  int64_t step_cap, int32_t* completion, int32_t* evictions,
                  int64_t* tel, int64_t* makespan, int64_t* request_steps,
                  int64_t* total_evictions, int64_t* stats, orc_event_t* events,
@@ -223,13 +228,23 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
   int64_t* qpos = (int64_t*)malloc(sizeof(int64_t) * n);
   int32_t* promoted = (int32_t*)malloc(sizeof(int32_t) * n);
   int64_t n_promotions = 0;
-  heap_t waiting = {heap_mem, 0, algo == ORC_AELL || algo == ORC_ARANDOM ? qpos : est};
+  heap_t waiting = {heap_mem, 0, algo == ORC_AELL || algo == ORC_ARANDOM ? qpos : est, tie};
 
   /* Planning length: u (A_max, Alg. 1), o (H-SF, Alg. 3), o~ initialised to l
    * (A_min, Alg. 2 and Alg. 4; A_l, Alg. 5). */
   for (int32_t i = 0; i < n; i++) {
     est[i] = (algo == ORC_AMAX) ? u[i] : (algo == ORC_HSF || algo == ORC_ARANDOM) ? o[i] : l[i];
     qpos[i] = algo == ORC_ARANDOM ? prio[i] : i;
+  }
+  /* A_l's fresh queue: by arrival, equal arrivals by (tie, index) */
+  if (algo == ORC_AELL && tie) {
+    for (int32_t i = 0; i < n; i++) {
+      ek[i].i = i;
+      ek[i].tie = tie[i];
+      ek[i].key_est = a ? a[i] : 0;
+    }
+    qsort(ek, n, sizeof(evict_key_t), cmp_evict);
+    for (int32_t r = 0; r < n; r++) qpos[ek[r].i] = r;
   }
 
   int32_t n_running = 0, n_deferred = 0, n_done = 0, next_arrival = 0;
@@ -281,6 +296,7 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
       if (P > M) {
         for (int32_t k = 0; k < n_running; k++) {
           ek[k].i = running[k];
+          ek[k].tie = tie ? tie[running[k]] : 0;
           ek[k].key_est = est[running[k]];
         }
         qsort(ek, n_running, sizeof(evict_key_t), cmp_evict);
@@ -313,8 +329,9 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
 
     /* 4'. A_l: a run that has generated o~ = l tokens without finishing has
      *     o > l; it leaves the running set, plans with u from now on and joins
-     *     the back of the queue (same-step promotions in index order), where it
-     *     may be admitted again at this step (Alg. 5). */
+     *     the back of the queue (same-step promotions in the order of their
+     *     fresh-queue positions: index order without tie keys), where it may
+     *     be admitted again at this step (Alg. 5). */
     if (algo == ORC_AELL) {
       int32_t n_prom = 0;
       kept = 0;
@@ -329,9 +346,15 @@ int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o
           stats[ORC_STAT_WORK] += n_running;
         }
         n_running = kept;
-        qsort(promoted, n_prom, sizeof(int32_t), cmp_index);
+        /* a request is promoted at most once, so qpos still holds its fresh position */
         for (int32_t x = 0; x < n_prom; x++) {
-          int32_t i = promoted[x];
+          ek[x].i = promoted[x];
+          ek[x].tie = 0;
+          ek[x].key_est = qpos[promoted[x]];
+        }
+        qsort(ek, n_prom, sizeof(evict_key_t), cmp_evict);
+        for (int32_t x = 0; x < n_prom; x++) {
+          int32_t i = ek[x].i;
           est[i] = u[i];
           qpos[i] = (int64_t)n + n_promotions++;
           evc[i]++;

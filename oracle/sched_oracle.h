@@ -66,6 +66,13 @@ enum {
  *             algorithm does not read it).
  *   prio    : per-request priorities (the random order of A_random); needed
  *             only for ORC_ARANDOM (NULL otherwise).
+ *   tie     : per-request tie keys, or NULL.  The paper breaks ties among
+ *             equal planning lengths uniformly at random (Algorithm 2's
+ *             eviction and admission sorts, Algorithm 1's random sample); the
+ *             oracle orders equal keys by (tie, index), so a random tie key is
+ *             such a random order and NULL means index order.  A_l's fresh
+ *             queue is ordered by (arrival, tie, index), and its same-step
+ *             promotions by their fresh-queue positions.
  *   algo    : ORC_AMAX, ORC_AMIN, ORC_HSF, ORC_AELL, ORC_ADAPTIVE (which
  *             simulates orc_adaptive_choice's algorithm) or ORC_ARANDOM.
  *   M       : KV-cache budget in tokens (> 0).
@@ -79,7 +86,8 @@ enum {
  * Returns the instance status (ORC_OK or a negative code).
  */
 int orc_simulate(int32_t n, const int32_t* a, const int32_t* s, const int32_t* o,
-                 const int32_t* l, const int32_t* u, const int32_t* prio, int32_t algo, int64_t M,
+                 const int32_t* l, const int32_t* u, const int32_t* prio, const int32_t* tie,
+                 int32_t algo, int64_t M,
                  int64_t step_cap, int32_t* completion, int32_t* evictions,
                  int64_t* tel, int64_t* makespan, int64_t* request_steps,
                  int64_t* total_evictions, int64_t* stats, orc_event_t* events,

@@ -115,6 +115,7 @@ class Instances:
     instance_ids: np.ndarray      # int64 [K] ids within the full workload
     meta: Dict[str, object] = field(default_factory=dict)
     priority: Optional[np.ndarray] = None   # int32 [N]: the random order of A_random
+    tie_key: Optional[np.ndarray] = None    # int32 [N]: order among equal planning lengths
 
     @property
     def num_instances(self) -> int:
@@ -136,11 +137,12 @@ class Instances:
         d["lower"] = None if self.lower is None else self.lower[b:e]
         d["upper"] = None if self.upper is None else self.upper[b:e]
         d["priority"] = None if self.priority is None else self.priority[b:e]
+        d["tie_key"] = None if self.tie_key is None else self.tie_key[b:e]
         return d
 
     def subset(self, ks: Sequence[int]) -> "Instances":
         ks = list(ks)
-        parts = {f: [] for f in ("arrival", "prompt", "output", "lower", "upper", "priority")}
+        parts = {f: [] for f in ("arrival", "prompt", "output", "lower", "upper", "priority", "tie_key")}
         offs = [0]
         for k in ks:
             d = self.instance(k)
@@ -153,7 +155,8 @@ class Instances:
                          cat("output"), None if self.lower is None else cat("lower"),
                          None if self.upper is None else cat("upper"),
                          self.instance_ids[ks].copy(), dict(self.meta),
-                         None if self.priority is None else cat("priority"))
+                         None if self.priority is None else cat("priority"),
+                         None if self.tie_key is None else cat("tie_key"))
 
 
 # ---------------------------------------------------------------------------
@@ -295,9 +298,11 @@ def generate(name: str, seed: int = 0, instance_ids: Optional[Sequence[int]] = N
 
 
 def from_lists(M: int, instances: List[Dict[str, Sequence[int]]], name: str = "custom") -> Instances:
-    """Pack hand-written instances (dicts with keys arrival/prompt/output/lower/upper) into CSR."""
+    """Pack hand-written instances (dicts with keys arrival/prompt/output/lower/upper and
+    optionally priority/tie_key) into CSR."""
     offs = [0]
-    cols: Dict[str, list] = {f: [] for f in ("arrival", "prompt", "output", "lower", "upper", "priority")}
+    cols: Dict[str, list] = {f: [] for f in ("arrival", "prompt", "output", "lower", "upper", "priority",
+                                             "tie_key")}
     has = {f: True for f in cols}
     for d in instances:
         n = len(d["output"])
@@ -317,7 +322,7 @@ def from_lists(M: int, instances: List[Dict[str, Sequence[int]]], name: str = "c
     K = len(instances)
     return Instances(name, int(M), np.array(offs, dtype=np.int64), arr("arrival"), arr("prompt"),
                      arr("output"), arr("lower"), arr("upper"), np.arange(K, dtype=np.int64),
-                     priority=arr("priority"))
+                     priority=arr("priority"), tie_key=arr("tie_key"))
 
 
 def random_small(seed: int, num_instances: int, n_max: int, *, s_max: int = 6, o_max: int = 8,
@@ -428,6 +433,20 @@ def with_random_order(batch: Instances, seed: int = 0) -> Instances:
         r = raw64(seed, 200, 0, np.array([batch.instance_ids[k]], np.int64), e - b)[0]
         pr[b:e] = np.argsort(np.argsort(r, kind="stable"), kind="stable").astype(np.int32)
     return dataclasses.replace(batch, priority=pr)
+
+
+def with_tie_keys(batch: Instances, seed: int = 0) -> Instances:
+    """A copy of `batch` with random tie keys: per instance a uniformly random
+    permutation of 0..n-1 (ranks of i.i.d. 64-bit draws from a stream of its
+    own), so that requests with equal planning lengths are ordered uniformly at
+    random, as the paper's policies break ties."""
+    import dataclasses
+    tk = np.empty(batch.total_requests, np.int32)
+    for k in range(batch.num_instances):
+        b, e = int(batch.offsets[k]), int(batch.offsets[k + 1])
+        r = raw64(seed, 201, 0, np.array([batch.instance_ids[k]], np.int64), e - b)[0]
+        tk[b:e] = np.argsort(np.argsort(r, kind="stable"), kind="stable").astype(np.int32)
+    return dataclasses.replace(batch, tie_key=tk)
 
 
 def tiny(seed: int, num_instances: int, n: int, *, s_max: int = 3, o_max: int = 6, M: int = 12,

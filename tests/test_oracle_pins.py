@@ -425,3 +425,70 @@ def test_arandom_c_oracle_equals_literal(seed):
         r = O.simulate(inst, O.ARANDOM, b.M, events=True)
         assert same(r, O.literal_simulate(inst, O.ARANDOM, b.M))
         O.audit(inst, O.ARANDOM, b.M, r)
+
+
+# ---------------------------------------------------------------------------
+# Tie keys: the paper breaks ties among equal planning lengths uniformly at
+# random (Algorithm 1's random sample; Algorithm 2's eviction and admission
+# sorts); a caller-given tie key is that order, index order without one.
+# ---------------------------------------------------------------------------
+
+def _relabel(inst, perm):
+    """Instance j of the result is request perm[j] of `inst`."""
+    out = {}
+    for f, v in inst.items():
+        out[f] = None if v is None else np.asarray(v)[perm]
+    return out
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_tie_key_relabelling(seed):
+    # Renumber the requests (inside each group of equal arrivals, so arrivals
+    # stay sorted) and give each its old index as tie key: every policy must
+    # produce the old outputs, renumbered.  A tie decided by the new index
+    # anywhere (admission, cancellation, A_l's queue) breaks this.
+    rng = np.random.default_rng(40 + seed)
+    b = W.random_small(seed + 40, 40, 10, s_max=4, o_max=8, M=22, arrivals=(seed == 2), alpha=1.0)
+    b = W.with_random_order(b, seed)
+    n_ev = 0
+    for k in range(b.num_instances):
+        inst = dict(b.instance(k))
+        inst.pop("tie_key", None)
+        a = np.asarray(inst["arrival"])
+        perm = np.concatenate([rng.permutation(np.flatnonzero(a == v)) for v in np.unique(a)]).astype(np.int64)
+        new = _relabel(inst, perm)
+        new["tie_key"] = perm.astype(np.int32)
+        for algo in (O.AMAX, O.AMIN, O.HSF, O.AELL, O.ADAPTIVE, O.ARANDOM):
+            r0 = O.simulate(inst, algo, b.M)
+            r1 = O.simulate(new, algo, b.M)
+            assert all(r0[f] == r1[f] for f in FIELDS_I), (k, algo)
+            assert np.array_equal(r0["completion"][perm], r1["completion"]), (k, algo)
+            assert np.array_equal(r0["evictions"][perm], r1["evictions"]), (k, algo)
+            n_ev += r0["total_evictions"]
+    assert n_ev > 0
+
+
+def test_tie_key_neutral_forms():
+    # the identity and a constant tie key both leave index order
+    b = W.random_small(50, 40, 9, s_max=4, o_max=8, M=22, alpha=1.0)
+    for k in range(b.num_instances):
+        inst = dict(b.instance(k))
+        n = len(inst["output"])
+        for algo in (O.AMAX, O.AMIN, O.HSF, O.AELL):
+            r = O.simulate(inst, algo, b.M)
+            assert same(r, O.simulate(dict(inst, tie_key=np.arange(n, dtype=np.int32)), algo, b.M))
+            assert same(r, O.simulate(dict(inst, tie_key=np.full(n, 7, np.int32)), algo, b.M))
+
+
+@pytest.mark.parametrize("seed", range(2))
+def test_tie_key_c_oracle_equals_literal_and_audit(seed):
+    # random tie keys with repeats (ties among tie keys fall back to the index)
+    b = W.random_small(seed + 60, 60, 8, s_max=5, o_max=9, M=24, arrivals=(seed == 1), alpha=1.0)
+    rng = np.random.default_rng(seed)
+    for k in range(b.num_instances):
+        inst = dict(b.instance(k))
+        inst["tie_key"] = rng.integers(0, 4, len(inst["output"])).astype(np.int32)
+        for algo in (O.AMAX, O.AMIN, O.HSF, O.AELL):
+            r = O.simulate(inst, algo, b.M, events=True)
+            assert same(r, O.literal_simulate(inst, algo, b.M)), (k, algo)
+            O.audit(inst, algo, b.M, r)
