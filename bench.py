@@ -197,6 +197,24 @@ class HipEvent:
             pass
 
 
+def host_cpus():
+    """Logical CPUs this process may run on, the oracle pool size (that count,
+    capped by OMP_NUM_THREADS where the host sets one: a share of a larger
+    machine), and the CPU model from /proc/cpuinfo."""
+    avail = len(os.sched_getaffinity(0))
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    threads = min(avail, int(env)) if env.isdigit() and int(env) > 0 else avail
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return avail, threads, model
+
+
 def cpu_baseline(batch, algo, g_out, target_s: float, threads: int):
     """Time the oracle on a bounded sample of instances; check parity on it."""
     import numpy as np
@@ -225,8 +243,10 @@ def cpu_baseline(batch, algo, g_out, target_s: float, threads: int):
     st = O.simulate_batch(batch, algo, instances=sub, threads=threads, stats=True)
     work = sum(x["work"] for x in st["stats"])
     w_ratio = work / max(1, int(st["request_steps"].sum()))
+    avail, _, model = host_cpus()
     return {
         "value": rs / wall, "unit": "request-steps/s", "cores": threads, "kind": "oracle",
+        "threads": threads, "cpus_available": avail, "cpu_model": model,
         "sample": (f"{len(sample)} of {K} instances ("
                    + (f"one in {stride}" if stride > 1 else "the first, in index order")
                    + f"), {rs} request-steps in {wall:.1f} s on {threads} host threads"),
@@ -393,7 +413,7 @@ def main():
             "request_steps_per_s": rs / (pipe_ms / 1e3), "outputs_equal_serial": pipe_same}),
     }
     if not args.no_cpu_baseline:
-        threads = args.cpu_threads or min(16, os.cpu_count() or 1)
+        threads = args.cpu_threads or host_cpus()[1]
         cb, parity, (w_ratio, w_n) = cpu_baseline(batch, algo, g, args.cpu_seconds, threads)
         result["cpu_baseline"] = cb
         result["parity_on_cpu_sample"] = parity

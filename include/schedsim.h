@@ -36,9 +36,11 @@
  *               (ascending; ties by index) drawn by the caller.
  * Each step, waiting requests are tried in ascending (planning length, index)
  * order (A_l: the queue order above) and the longest prefix that keeps
- * equation (2) is started.  Ties break by ascending request index.  Requests
- * arriving at step a_i join the waiting set at that step (the paper has every
- * a_i = 0).
+ * equation (2) is started.  Ties break by ascending request index, or by an
+ * optional per-request tie key first (the paper breaks ties uniformly at
+ * random, Algorithms 1, 2 and 4; a random tie key is such a random order).
+ * Requests arriving at step a_i join the waiting set at that step (the paper
+ * has every a_i = 0).
  *
  * All pointers in sched_instances_t and sched_results_t are DEVICE pointers
  * (e.g. torch tensors on the GPU), allocated and owned by the caller; the
@@ -78,8 +80,8 @@ enum {
   SCHED_E_HIP = -5,         /* call: a HIP runtime call failed                                  */
   SCHED_E_UNSUPPORTED = -6, /* call: capacity request beyond what the kernels hold.
                                status: o, u or l >= 2^15, s >= 2^16, n >= 2^17, a priority
-                               outside [0, 2^15), or the running or evicted set outgrew its
-                               capacity                                                          */
+                               outside [0, 2^15), or more than 1024 requests (or a forced
+                               running_capacity) would run at once                              */
   SCHED_E_ARRIVAL = -7      /* status: an arrival < 0 or arrivals not non-decreasing in index  */
 };
 
@@ -97,6 +99,14 @@ typedef struct {
   const int32_t* upper;     /* [N] u_i; required for SCHED_AMAX, SCHED_AELL, SCHED_ADAPTIVE */
   const int32_t* priority;  /* [N] A_random's order (ascending, ties by index); required for
                                SCHED_ARANDOM, unused otherwise                              */
+  const int32_t* tie_key;   /* [N] or NULL.  Order among requests whose planning keys are
+                               equal: by (tie_key, index) instead of index, in every policy's
+                               admission order and in A_min's cancellation order (A_random:
+                               equal priorities).  A_l's queue of fresh requests is ordered by
+                               (arrival, tie_key, index) and its same-step cancellations by
+                               that queue order.  Any int32 values; equal tie keys fall back
+                               to the index.  The library sorts them once per call (8 bytes of
+                               workspace and 8 of staging per request).                    */
 } sched_instances_t;
 
 /* Outputs.  Per request: completion step C_i (-1 if it never completed) and
@@ -118,6 +128,12 @@ typedef struct {
   int32_t* algo_used;       /* [K] or NULL      */
 } sched_results_t;
 
+/* Capacities.  Outputs never depend on any of the sizes below, nor on which
+ * other instances share a batch: an instance whose running set or cancelled
+ * set outgrows the room of one launch is simulated again from step 0 by a
+ * later launch with more room.  Only an instance that needs more than 1024
+ * concurrently running requests (or more than a forced running_capacity)
+ * ends with status SCHED_E_UNSUPPORTED. */
 typedef struct {
   int64_t step_cap;         /* last simulated step; <= 0: per instance
                                min(2^30, 4*(max a + sum(o+1)) + 64)                       */
@@ -128,11 +144,20 @@ typedef struct {
                                instance of up to 320 requests gets room for all of them;
                                a larger one starts with 320, grows to 384 and 512 within the
                                same launch, and is simulated again from step 0 with 640,
-                               then 1024, if it outgrows that; outputs do not depend on
-                               this)                                                       */
-  int32_t evicted_capacity; /* max cancelled requests waiting at once (A_min, A_l); 0: default */
+                               then 1024, if it outgrows that)                             */
+  int32_t evicted_capacity; /* LDS slots of the cancelled set (A_min, A_l) in the first launch;
+                               0: default (A_min: min(n_max, 16384) for batches of at most 64
+                               instances, else min(n_max, 1024); A_l: n_max; both clipped to
+                               what a workgroup's LDS holds).  An instance that outgrows them
+                               is simulated again with as many slots as the LDS holds, and
+                               one that outgrows those with a set of n slots in global memory
+                               (8 bytes of workspace per request when n_max exceeds the LDS
+                               room).                                                       */
   void* event_before;       /* hipEvent_t recorded just before the simulation kernel, or NULL */
   void* event_after;        /* hipEvent_t recorded just after it, or NULL                  */
+  int32_t evicted_lds_limit;/* > 0: at most this many LDS slots for the cancelled set in any
+                               launch (beyond them the global-memory set); 0: as many as fit.
+                               For tests of the global-memory set on small instances.      */
 } sched_options_t;
 
 /* Simulate every instance with the given policy and budget M (0 < M < 2^30).
@@ -151,6 +176,17 @@ int sched_simulate(const sched_instances_t* instances, sched_algo_t algo, int64_
 int sched_simulate_opts(const sched_instances_t* instances, sched_algo_t algo, int64_t M,
                         const sched_results_t* results, void* stream,
                         const sched_options_t* opts);
+
+/* Validation only: writes to status[K] (device) the per-instance status that
+ * sched_simulate would give each instance before simulating it (SCHED_OK,
+ * SCHED_E_INVAL for bad offsets, SCHED_E_ARRIVAL, SCHED_E_INTERVAL,
+ * SCHED_E_TOO_BIG or SCHED_E_UNSUPPORTED for field values beyond the
+ * kernels' widths), reading the same request fields as sched_simulate with
+ * `algo` (the adaptive policy validates with the policy it picks).  No
+ * workspace; asynchronous on `stream`.  Returns a call-level code like
+ * sched_simulate (SCHED_E_INVAL for NULL pointers or M outside (0, 2^30)). */
+int sched_validate(const sched_instances_t* instances, sched_algo_t algo, int64_t M, int32_t* status,
+                   void* stream);
 
 /* The hindsight optimum of tiny instances (n_k <= 8): the minimum total
  * latency (equation (3)) over every non-preemptive schedule that knows the

@@ -20,7 +20,8 @@ ALGOS = {"amax": AMAX, "amin": AMIN, "hsf": HSF, "aell": AELL, "adaptive": ADAPT
 OK, E_INVAL, E_INTERVAL, E_TOO_BIG, E_STEP_CAP, E_HIP, E_UNSUPPORTED, E_ARRIVAL = 0, -1, -2, -3, -4, -5, -6, -7
 
 # every symbol include/schedsim.h declares
-EXPORTED = ("sched_optimum", "sched_simulate", "sched_simulate_opts", "sched_strerror", "sched_version")
+EXPORTED = ("sched_optimum", "sched_simulate", "sched_simulate_opts", "sched_strerror", "sched_validate",
+            "sched_version")
 
 
 class SchedInstances(ctypes.Structure):
@@ -35,6 +36,7 @@ class SchedInstances(ctypes.Structure):
         ("lower", ctypes.c_void_p),
         ("upper", ctypes.c_void_p),
         ("priority", ctypes.c_void_p),
+        ("tie_key", ctypes.c_void_p),
     ]
 
 
@@ -58,6 +60,7 @@ class SchedOptions(ctypes.Structure):
         ("evicted_capacity", ctypes.c_int32),
         ("event_before", ctypes.c_void_p),
         ("event_after", ctypes.c_void_p),
+        ("evicted_lds_limit", ctypes.c_int32),
     ]
 
 
@@ -81,6 +84,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.sched_simulate_opts.argtypes = [ctypes.POINTER(SchedInstances), ctypes.c_int, ctypes.c_int64,
                                             ctypes.POINTER(SchedResults), ctypes.c_void_p,
                                             ctypes.POINTER(SchedOptions)]
+        lib.sched_validate.restype = ctypes.c_int
+        lib.sched_validate.argtypes = [ctypes.POINTER(SchedInstances), ctypes.c_int, ctypes.c_int64, ctypes.c_void_p,
+                                       ctypes.c_void_p]
         lib.sched_strerror.restype = ctypes.c_char_p
         lib.sched_strerror.argtypes = [ctypes.c_int]
         lib.sched_version.restype = ctypes.c_int
@@ -118,6 +124,7 @@ class DeviceBatch:
     lower: object
     upper: object
     priority: object = None
+    tie_key: object = None
 
     @property
     def num_instances(self) -> int:
@@ -137,7 +144,8 @@ def to_device(batch, device="cuda") -> DeviceBatch:
 
     return DeviceBatch(batch.M, batch.max_requests, t(batch.offsets, torch.int64), t(batch.arrival, torch.int32),
                        t(batch.prompt, torch.int32), t(batch.output, torch.int32), t(batch.lower, torch.int32),
-                       t(batch.upper, torch.int32), t(getattr(batch, "priority", None), torch.int32))
+                       t(batch.upper, torch.int32), t(getattr(batch, "priority", None), torch.int32),
+                       t(getattr(batch, "tie_key", None), torch.int32))
 
 
 def alloc_results(db: DeviceBatch, evictions: bool = True):
@@ -156,27 +164,47 @@ def alloc_results(db: DeviceBatch, evictions: bool = True):
     }
 
 
+def _instances(db: DeviceBatch, pass_lower: bool = True, pass_upper: bool = True) -> SchedInstances:
+    return SchedInstances(db.num_instances, db.max_requests, db.total_requests, _ptr(db.offsets), _ptr(db.arrival),
+                          _ptr(db.prompt), _ptr(db.output), _ptr(db.lower) if pass_lower else None,
+                          _ptr(db.upper) if pass_upper else None, _ptr(db.priority), _ptr(db.tie_key))
+
+
 def simulate_into(db: DeviceBatch, algo: int, out: Dict[str, object], *, M: Optional[int] = None, stream=None,
                   step_cap: int = 0, running_capacity: int = 0, evicted_capacity: int = 0,
-                  event_before=None, event_after=None, pass_lower: bool = True, pass_upper: bool = True) -> None:
+                  evicted_lds_limit: int = 0, event_before=None, event_after=None, pass_lower: bool = True,
+                  pass_upper: bool = True) -> None:
     """Queue ``sched_simulate_opts`` on ``stream`` (default: torch's current stream)."""
     import torch
     lib = load_library()
     if stream is None:
         stream = torch.cuda.current_stream(db.output.device)
-    inst = SchedInstances(db.num_instances, db.max_requests, db.total_requests, _ptr(db.offsets), _ptr(db.arrival),
-                          _ptr(db.prompt), _ptr(db.output), _ptr(db.lower) if pass_lower else None,
-                          _ptr(db.upper) if pass_upper else None, _ptr(db.priority))
+    inst = _instances(db, pass_lower, pass_upper)
     res = SchedResults(_ptr(out["completion"]), _ptr(out.get("evictions")), _ptr(out["tel"]),
                        _ptr(out.get("makespan")), _ptr(out.get("request_steps")), _ptr(out.get("total_evictions")),
                        _ptr(out["status"]), _ptr(out.get("algo_used")))
     opts = SchedOptions(int(step_cap), int(running_capacity), int(evicted_capacity),
                         None if event_before is None else int(event_before.cuda_event),
-                        None if event_after is None else int(event_after.cuda_event))
+                        None if event_after is None else int(event_after.cuda_event), int(evicted_lds_limit))
     code = lib.sched_simulate_opts(ctypes.byref(inst), int(algo), int(db.M if M is None else M), ctypes.byref(res),
                                    ctypes.c_void_p(stream.cuda_stream), ctypes.byref(opts))
     if code != OK:
         raise SchedError(code)
+
+
+def validate(db: DeviceBatch, algo: int, *, M: Optional[int] = None, stream=None, pass_lower: bool = True,
+             pass_upper: bool = True):
+    """Queue ``sched_validate``; returns the int32 device tensor of per-instance statuses (not synchronised)."""
+    import torch
+    lib = load_library()
+    if stream is None:
+        stream = torch.cuda.current_stream(db.output.device)
+    status = torch.empty(db.num_instances, dtype=torch.int32, device=db.output.device)
+    code = lib.sched_validate(ctypes.byref(_instances(db, pass_lower, pass_upper)), int(algo),
+                              int(db.M if M is None else M), _ptr(status), ctypes.c_void_p(stream.cuda_stream))
+    if code != OK:
+        raise SchedError(code)
+    return status
 
 
 def simulate(db: DeviceBatch, algo: int, **kw) -> Dict[str, object]:
@@ -200,7 +228,7 @@ def optimum(db: DeviceBatch, *, M: Optional[int] = None, node_cap: int = 0, uppe
     out = {"tel": torch.empty(K, dtype=torch.int64, device=dev), "status": torch.empty(K, dtype=torch.int32, device=dev),
            "nodes": torch.empty(K, dtype=torch.int64, device=dev)}
     inst = SchedInstances(K, db.max_requests, db.total_requests, _ptr(db.offsets), _ptr(db.arrival),
-                          _ptr(db.prompt), _ptr(db.output), None, None, None)
+                          _ptr(db.prompt), _ptr(db.output), None, None, None, None)
     code = lib.sched_optimum(ctypes.byref(inst), int(db.M if M is None else M), _ptr(upper_bound), _ptr(out["tel"]),
                              _ptr(out["status"]), _ptr(out["nodes"]), int(node_cap),
                              ctypes.c_void_p(stream.cuda_stream))

@@ -71,6 +71,7 @@ struct Params {
   const int32_t* lower;
   const int32_t* upper;
   const int32_t* priority;
+  const int32_t* tie_key;   // NULL: equal keys by index; else by (tie key, index)
   int32_t* completion;
   int32_t* evictions;
   int64_t* total_latency;
@@ -86,22 +87,125 @@ struct Params {
   uint32_t* sort_b;
   uint2* rec;
   int32_t* rank_of;
+  int32_t* u_of_rank;    // A_l: u of the request at each rank (the workspace of the second sort buffer)
   int32_t* cap;
   int32_t* algo_of;      // adaptive runs: the policy each instance runs (else NULL)
+  // with tie keys: each request's rank in tie order (its identity inside the
+  // kernels, in place of the index), the inverse map, and staging arrays of
+  // the per-request outputs indexed by that rank (copied out in index order
+  // at the end)
+  int32_t* tr_of;
+  int32_t* idx_of;
+  int32_t* comp_st;
+  int32_t* ev_st;
+  // cancelled set in global memory (the last retry pass): n entries per instance
+  uint64_t* vglob;
   // LDS layout of k_simulate
   int32_t nw_max;        // 64-bit words of the level-0 bitmap
   int32_t nw1_max;       // 64-bit words of the level-1 bitmap
-  int32_t cap_v;         // evicted-set capacity
-  int32_t retry_status;  // status for an outgrown running set: next pass (kRetry) or SCHED_E_UNSUPPORTED
+  int32_t cap_v;         // evicted-set capacity (LDS passes)
+  int32_t retry_status;  // status for an outgrown running set: a later pass (kRetryRows) or SCHED_E_UNSUPPORTED
+  int32_t retry_v_status;// status for an outgrown evicted set: a later pass (kRetryV) or SCHED_E_UNSUPPORTED
+  int32_t run_mask;      // retry passes: bit 0 runs kRetryRows instances, bit 1 kRetryV ones
+  int32_t run_cap;       // retry passes: most runs at once (a caller's forced capacity), else INT32_MAX
 };
+
+// Internal statuses of an instance handed to a later pass: its running set
+// outgrew the register rows, or its cancelled set outgrew its slots.  The
+// later pass simulates it again from step 0 with more room.
+constexpr int kRetryRows = -100;
+constexpr int kRetryV = -101;
 
 // ---------------------------------------------------------------------------
 // k_prepare
 // ---------------------------------------------------------------------------
+// One stable LSD radix pass of a wave over the n elements src[0..n) -> dst,
+// by the 8-bit digit dig(element): LDS histogram, wave scan of the bucket
+// starts, and a stable scatter that ranks equal digits inside each 64-element
+// chunk with 8 ballots.
+template <typename DigitFn>
+__device__ __forceinline__ void radix_pass(uint32_t* hist, const uint32_t* src, uint32_t* dst, int n, DigitFn dig) {
+  const int lane = threadIdx.x;
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int j = lane; j < 256; j += 64) hist[j] = 0;
+  __syncthreads();
+  for (int c = 0; c < n; c += 64) {
+    const int i = c + lane;
+    if (i < n) atomicAdd(&hist[dig(src[i])], 1u);
+  }
+  __syncthreads();
+  {
+    uint32_t h0 = hist[4 * lane], h1 = hist[4 * lane + 1], h2 = hist[4 * lane + 2], h3 = hist[4 * lane + 3];
+    int32_t tot = static_cast<int32_t>(h0 + h1 + h2 + h3);
+    int32_t ex = wave::inclusive_scan_i32(tot) - tot;
+    __syncthreads();
+    hist[4 * lane] = ex;
+    hist[4 * lane + 1] = ex + h0;
+    hist[4 * lane + 2] = ex + h0 + h1;
+    hist[4 * lane + 3] = ex + h0 + h1 + h2;
+  }
+  __syncthreads();
+  for (int c = 0; c < n; c += 64) {
+    const int i = c + lane;
+    const bool act = i < n;
+    const uint32_t key = act ? src[i] : 0u;
+    const uint32_t d = act ? dig(key) : 0u;
+    uint64_t eq = wave::ballot(act);
+    for (int bit = 0; bit < 8; ++bit) {
+      const uint64_t bal = wave::ballot(act && ((d >> bit) & 1u));
+      eq &= ((d >> bit) & 1u) ? bal : ~bal;
+    }
+    const int rank = __builtin_popcountll(eq & lt_mask);
+    const uint32_t base = act ? hist[d] : 0u;
+    __syncthreads();
+    if (act) {
+      dst[base + rank] = key;
+      if (rank == 0) hist[d] = base + static_cast<uint32_t>(__builtin_popcountll(eq));
+    }
+    __syncthreads();
+  }
+  __syncthreads();
+}
+
+// Stable sort of the request indices 0..n-1 by the 32-bit key key(i) (four
+// radix passes; a byte on which every key agrees is skipped).  Returns the
+// buffer holding the sorted indices (a or b).
+template <typename KeyFn>
+__device__ __forceinline__ uint32_t* sort_indices_by(uint32_t* hist, uint32_t* a, uint32_t* b, int n, KeyFn key,
+                                                     bool init) {
+  const int lane = threadIdx.x;
+  uint32_t kand = 0xFFFFFFFFu, kor = 0u;
+  for (int c = 0; c < n; c += 64) {
+    const int i = c + lane;
+    if (i < n) {
+      if (init) a[i] = static_cast<uint32_t>(i);
+      const uint32_t k = key(static_cast<uint32_t>(i));
+      kand &= k;
+      kor |= k;
+    }
+  }
+  for (int off = 32; off >= 1; off >>= 1) {
+    kand &= static_cast<uint32_t>(__shfl_xor(static_cast<int>(kand), off, 64));
+    kor |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(kor), off, 64));
+  }
+  const uint32_t varies = kand ^ kor;
+  __syncthreads();
+  for (int pass = 0; pass < 4; ++pass) {
+    const int sh = 8 * pass;
+    if (((varies >> sh) & 0xFFu) == 0u) continue;
+    radix_pass(hist, a, b, n, [&](uint32_t e) { return (key(e) >> sh) & 0xFFu; });
+    uint32_t* t = a;
+    a = b;
+    b = t;
+  }
+  return a;
+}
+
+// Per-instance validation (shared by k_prepare and k_validate): the status
+// and, through *algo_out, the policy the instance runs (the adaptive choice);
+// also the default step cap.
 template <int ALGO>
-__global__ __launch_bounds__(64) void k_prepare(Params P) {
-  __shared__ uint32_t hist[256];
-  const int k = blockIdx.x;
+__device__ __forceinline__ int validate_instance(const Params& P, int k, int* algo_out, int64_t* cap_out) {
   const int lane = threadIdx.x;
   const int64_t b = P.offsets[k];
   const int64_t e = P.offsets[k + 1];
@@ -177,13 +281,49 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
   const int64_t sum_o_all = wave::sum_i64(sum_o);
   int64_t cap = P.step_cap > 0 ? P.step_cap : 4 * (max_a_all + sum_o_all) + 64;
   if (cap > kCapLimit) cap = kCapLimit;
+  *algo_out = algo;
+  *cap_out = cap;
+  return status;
+}
 
-  // per-request outputs start as "not completed, never cancelled"
-  for (int c = 0; c < n; c += 64) {
+// Validation only (sched_validate): status per instance.
+template <int ALGO>
+__global__ __launch_bounds__(64) void k_validate(Params P) {
+  const int k = blockIdx.x;
+  int algo = ALGO;
+  int64_t cap = 0;
+  const int status = validate_instance<ALGO>(P, k, &algo, &cap);
+  if (threadIdx.x == 0) {
+    P.status[k] = status;
+    if (P.algo_used) P.algo_used[k] = algo;
+  }
+}
+
+template <int ALGO>
+__global__ __launch_bounds__(64) void k_prepare(Params P) {
+  __shared__ uint32_t hist[256];
+  const int k = blockIdx.x;
+  const int lane = threadIdx.x;
+  int algo = ALGO;
+  int64_t cap = 0;
+  const int status = validate_instance<ALGO>(P, k, &algo, &cap);
+  const int64_t b = P.offsets[k];
+  const int n = (status == SCHED_OK) ? static_cast<int>(P.offsets[k + 1] - b) : 0;
+  const bool tie = P.tie_key != nullptr;
+
+  // per-request outputs start as "not completed, never cancelled" (with tie
+  // keys, the staging arrays the kernels write too)
+  const int64_t e = P.offsets[k + 1];
+  const int n_init = (b >= 0 && e > b && e <= P.N && e - b <= P.max_requests) ? static_cast<int>(e - b) : 0;
+  for (int c = 0; c < n_init; c += 64) {
     const int i = c + lane;
-    if (i < n) {
+    if (i < n_init) {
       P.completion[b + i] = -1;
       if (P.evictions) P.evictions[b + i] = 0;
+      if (tie) {
+        P.comp_st[b + i] = -1;
+        if (P.evictions) P.ev_st[b + i] = 0;
+      }
     }
   }
   if (lane == 0) {
@@ -194,8 +334,32 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
   }
   if (status != SCHED_OK || n == 0) return;
 
-  // ---- keys (k0 << 17 | index), k0 = u (A_max), l (A_min, A_l), o (H-SF), the
-  // priority (A_random, which plans with o)
+  // ---- tie keys: each request's rank in the order (tie key, index) (A_l:
+  // (arrival, tie key, index), its fresh-queue order) is its identity in the
+  // keys below; tr_of maps index -> rank, idx_of rank -> index
+  if (tie) {
+    const int32_t* tk = P.tie_key + b;
+    uint32_t* S = sort_indices_by(hist, P.sort_a + b, P.sort_b + b, n,
+                                  [&](uint32_t i) { return static_cast<uint32_t>(tk[i]) ^ 0x80000000u; }, true);
+    if (algo == SCHED_AELL && P.arrival) {
+      const int32_t* ar = P.arrival + b;
+      uint32_t* other = S == P.sort_a + b ? P.sort_b + b : P.sort_a + b;
+      S = sort_indices_by(hist, S, other, n, [&](uint32_t i) { return static_cast<uint32_t>(ar[i]); }, false);
+    }
+    for (int c = 0; c < n; c += 64) {
+      const int r = c + lane;
+      if (r < n) {
+        const uint32_t i = S[r];
+        P.tr_of[b + i] = r;
+        P.idx_of[b + r] = static_cast<int32_t>(i);
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- keys (k0 << 17 | id), k0 = u (A_max), l (A_min, A_l), o (H-SF), the
+  // priority (A_random, which plans with o); id = the index, or the tie rank,
+  // placed at position id so that the stable sort below keeps id order
   for (int c = 0; c < n; c += 64) {
     const int i = c + lane;
     if (i < n) {
@@ -203,65 +367,31 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
                     : (algo == SCHED_HSF)  ? P.output[b + i]
                     : (algo == SCHED_ARANDOM) ? P.priority[b + i]
                                            : P.lower[b + i];
-      P.sort_a[b + i] = (static_cast<uint32_t>(est) << kIdxBits) | static_cast<uint32_t>(i);
+      const uint32_t id = tie ? static_cast<uint32_t>(P.tr_of[b + i]) : static_cast<uint32_t>(i);
+      P.sort_a[b + id] = (static_cast<uint32_t>(est) << kIdxBits) | id;
     }
   }
+  __syncthreads();
   // ---- stable LSD radix sort on bits 17..24 then 25..31 (A_l's queue is in
-  // index order: its ranks are the indices, no sort)
-  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  // id order: its ranks are the ids, no sort)
   for (int pass = 0; pass < (algo == SCHED_AELL ? 0 : 2); ++pass) {
-    const uint32_t* src = pass == 0 ? P.sort_a : P.sort_b;
-    uint32_t* dst = pass == 0 ? P.sort_b : P.sort_a;
+    const uint32_t* src = (pass == 0 ? P.sort_a : P.sort_b) + b;
+    uint32_t* dst = (pass == 0 ? P.sort_b : P.sort_a) + b;
     const int shift = kIdxBits + 8 * pass;
-    for (int j = lane; j < 256; j += 64) hist[j] = 0;
-    __syncthreads();
-    for (int c = 0; c < n; c += 64) {
-      const int i = c + lane;
-      if (i < n) atomicAdd(&hist[(src[b + i] >> shift) & 0xFFu], 1u);
-    }
-    __syncthreads();
-    {
-      uint32_t h0 = hist[4 * lane], h1 = hist[4 * lane + 1], h2 = hist[4 * lane + 2], h3 = hist[4 * lane + 3];
-      int32_t tot = static_cast<int32_t>(h0 + h1 + h2 + h3);
-      int32_t ex = wave::inclusive_scan_i32(tot) - tot;
-      __syncthreads();
-      hist[4 * lane] = ex;
-      hist[4 * lane + 1] = ex + h0;
-      hist[4 * lane + 2] = ex + h0 + h1;
-      hist[4 * lane + 3] = ex + h0 + h1 + h2;
-    }
-    __syncthreads();
-    for (int c = 0; c < n; c += 64) {
-      const int i = c + lane;
-      const bool act = i < n;
-      const uint32_t key = act ? src[b + i] : 0u;
-      const uint32_t d = (key >> shift) & 0xFFu;
-      uint64_t eq = wave::ballot(act);
-      for (int bit = 0; bit < 8; ++bit) {
-        const uint64_t bal = wave::ballot(act && ((d >> bit) & 1u));
-        eq &= ((d >> bit) & 1u) ? bal : ~bal;
-      }
-      const int rank = __builtin_popcountll(eq & lt_mask);
-      const uint32_t base = act ? hist[d] : 0u;
-      __syncthreads();
-      if (act) {
-        dst[b + base + rank] = key;
-        if (rank == 0) hist[d] = base + static_cast<uint32_t>(__builtin_popcountll(eq));
-      }
-      __syncthreads();
-    }
-    __syncthreads();
+    radix_pass(hist, src, dst, n, [&](uint32_t key) { return (key >> shift) & 0xFFu; });
   }
-  // ---- ranked records and inverse ranks
+  // ---- ranked records and inverse ranks (rank_of is indexed by request index)
   for (int c = 0; c < n; c += 64) {
     const int r = c + lane;
     if (r < n) {
       const uint32_t key = P.sort_a[b + r];
-      const uint32_t idx = key & kIdxMask;
+      const uint32_t id = key & kIdxMask;
+      const uint32_t idx = tie ? static_cast<uint32_t>(P.idx_of[b + id]) : id;
       const uint32_t s = static_cast<uint32_t>(P.prompt[b + idx]);
       const uint32_t o = static_cast<uint32_t>(P.output[b + idx]);
       P.rec[b + r] = make_uint2(key, s | (o << 16));
       P.rank_of[b + idx] = r;
+      if (algo == SCHED_AELL) P.u_of_rank[b + r] = P.upper[b + idx];
     }
   }
 }
@@ -269,9 +399,6 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
 // ---------------------------------------------------------------------------
 // k_simulate
 // ---------------------------------------------------------------------------
-// Internal status of a first pass whose running set outgrew its register rows;
-// the retry pass (more rows) re-runs exactly those instances.
-constexpr int kRetry = -100;
 // r_end of an empty slot of the running set (below every planned end)
 constexpr int32_t kEmpty = INT32_MIN;
 // r_c of an empty slot (after every step)
@@ -309,8 +436,12 @@ constexpr int kResume = -102;
 // rows and writes its outputs.  A running set that outgrows the rows ends the
 // simulation with `retry_status` (the per-request outputs are then reset), or,
 // with TO_STATE, saves the state to *st and returns kResume at once.  With
-// FROM_STATE the body continues from *st instead of starting at step 0.
-template <int ALGO, int ROWS, bool FROM_STATE = false, bool TO_STATE = false>
+// FROM_STATE the body continues from *st instead of starting at step 0.  A
+// cancelled set that outgrows its P.cap_v LDS slots ends it with
+// P.retry_v_status; with VGLOBAL the set lives in global memory (n slots, the
+// most it can hold).  CAPPED holds the running set to P.run_cap runs.
+template <int ALGO, int ROWS, bool FROM_STATE = false, bool TO_STATE = false, bool VGLOBAL = false,
+          bool CAPPED = false>
 __device__ __forceinline__ int sim_instance(const Params& P, const int k, const int st0, const int retry_status,
                                            SimState* st = nullptr) {
   static_assert(!(FROM_STATE || TO_STATE) || ROWS <= kStateRows, "state holds at most kStateRows rows");
@@ -334,8 +465,9 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     uint64_t* L1 = lds64 + P.nw_max;
     // cancelled requests, one 64-bit entry each.  A_min: key | (s | o << 16) << 32,
     // slots [0, nVe) may start now, [nVe, nV) were cancelled at this step.
-    // A_l: a FIFO ring of index | s << 17 | o << 33 | u << 48 from slot v_head.
-    uint64_t* vent = L1 + P.nw1_max;
+    // A_l: a FIFO ring of id | s << 17 | o << 33 | u << 48 from slot v_head.
+    uint64_t* vent = VGLOBAL ? P.vglob + b : L1 + P.nw1_max;
+    const int32_t cap_v = VGLOBAL ? n : P.cap_v;
     const int nw = (n + 63) >> 6;
     const int nw1 = (nw + 63) >> 6;
     if (!FROM_STATE) {
@@ -350,9 +482,10 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     const uint2* rec = base(P.rec + b);
     const int32_t* arrival = P.arrival ? base(P.arrival + b) : nullptr;
     const int32_t* rank_of = base(P.rank_of + b);
-    const int32_t* upper_k = ALGO == SCHED_AELL ? P.upper + b : nullptr;
-    int32_t* completion = base(P.completion + b);
-    int32_t* evictions = P.evictions ? base(P.evictions + b) : nullptr;
+    const int32_t* upper_k = ALGO == SCHED_AELL ? P.u_of_rank + b : nullptr;  // by rank
+    // per-request outputs by id (with tie keys: the staging arrays)
+    int32_t* completion = base((P.tie_key ? P.comp_st : P.completion) + b);
+    int32_t* evictions = P.evictions ? base((P.tie_key ? P.ev_st : P.evictions) + b) : nullptr;
 
     // running set: register rows; an empty slot has r_end = kEmpty, r_c = kNever,
     // r_key = ~0, which every scan below treats as neutral, so scans cover all rows
@@ -695,8 +828,8 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
             const uint64_t at = wave::ballot(best == iv);
             const uint32_t imin = wave::uniform_u(iv);
             if (imin == 0xFFFFFFFFu) break;
-            if (nV >= P.cap_v) {
-              status = SCHED_E_UNSUPPORTED;
+            if (nV >= cap_v) {
+              status = P.retry_v_status;
               break;
             }
             const int ln = __builtin_ctzll(at);
@@ -717,7 +850,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
             const uint64_t okk = static_cast<uint32_t>(ck - pk);
             if (lane == 0) {
               int slot = v_head + nV;
-              slot = slot >= P.cap_v ? slot - P.cap_v : slot;
+              slot = slot >= cap_v ? slot - cap_v : slot;
               vent[slot] = imin | (sk << 17) | (okk << 33) | (static_cast<uint64_t>(uk) << 48);
               if (evictions) atomicAdd(&evictions[imin], 1);
             }
@@ -762,8 +895,12 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
             const uint32_t kv = wave::min_u32_all(best);
             const uint64_t at = wave::ballot(best == kv);
             const uint32_t kmin = wave::uniform_u(kv);
-            if (kmin == 0xFFFFFFFFu || nV >= P.cap_v) {  // no run: impossible while P > M > 0
+            if (kmin == 0xFFFFFFFFu) {  // no run: impossible while P > M > 0
               status = SCHED_E_UNSUPPORTED;
+              break;
+            }
+            if (nV >= cap_v) {
+              status = P.retry_v_status;
               break;
             }
             const int ln = __builtin_ctzll(at);
@@ -869,6 +1006,10 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
         const int32_t f = wave::uniform(fv);
         // admit: start at p = t; runs whose planned end is in (t+1, E] gain its share
         // a free slot first: without one nothing has changed for this candidate
+        if (CAPPED && N >= P.run_cap) {
+          status = retry_status;
+          break;
+        }
         if (fr_mask == 0ull) {
           int rr = -1;
           uint64_t mm = 0ull;
@@ -935,7 +1076,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
         if (c_fromF) {
           SK_F_TAKE();
         } else if (ALGO == SCHED_AELL) {
-          v_head = v_head + 1 == P.cap_v ? 0 : v_head + 1;
+          v_head = v_head + 1 == cap_v ? 0 : v_head + 1;
           --nV;
           SK_V_HEAD();
         } else {
@@ -991,15 +1132,25 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     if (TO_STATE && status == kResume) return kResume;
   }
 
-  // ---- epilogue: totals from the per-request outputs
+  // ---- epilogue: totals from the per-request outputs (with tie keys, first
+  // copied from the staging arrays, by id, to the outputs, by index)
   __syncthreads();
   const bool keep = (status == SCHED_OK || status == SCHED_E_STEP_CAP) && n > 0;
+  const bool tie = P.tie_key != nullptr;
   int64_t tel = 0, mk = 0;
   if (keep) {
     for (int c = 0; c < n; c += 64) {
       const int i = c + lane;
       if (i < n) {
-        const int32_t ci = P.completion[b + i];
+        int32_t ci;
+        if (tie) {
+          const int32_t id = P.tr_of[b + i];
+          ci = P.comp_st[b + id];
+          P.completion[b + i] = ci;
+          if (P.evictions) P.evictions[b + i] = P.ev_st[b + id];
+        } else {
+          ci = P.completion[b + i];
+        }
         if (ci >= 0) {
           tel += ci - (P.arrival ? P.arrival[b + i] : 0);
           mk = ci > mk ? ci : mk;
@@ -1007,12 +1158,15 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       }
     }
   } else if (status != st0 && n > 0) {
-    // capacity outgrown at run time: report like an invalid instance (or hand it to the retry pass)
+    // capacity outgrown at run time: report like an invalid instance (or hand
+    // it to a retry pass, which starts from these values)
+    int32_t* comp = tie ? P.comp_st : P.completion;
+    int32_t* evs = tie ? P.ev_st : P.evictions;
     for (int c = 0; c < n; c += 64) {
       const int i = c + lane;
       if (i < n) {
-        P.completion[b + i] = -1;
-        if (P.evictions) P.evictions[b + i] = 0;
+        comp[b + i] = -1;
+        if (P.evictions) evs[b + i] = 0;
       }
     }
   }
@@ -1033,17 +1187,19 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
 }
 
 // One wave per instance.  RETRY_PASS: only instances handed over by an
-// earlier launch (status kRetry) run.
-template <int ALGO, int ROWS, bool RETRY_PASS>
+// earlier launch for a reason this pass takes (P.run_mask) run, held to
+// P.run_cap runs at once.
+template <int ALGO, int ROWS, bool RETRY_PASS, bool VGLOBAL = false>
 __global__ __launch_bounds__(64) void k_simulate(Params P) {
   const int k = blockIdx.x;
   if (P.algo_of && P.algo_of[k] != ALGO) return;  // adaptive run: the other policy's instance
   int st0 = P.status[k];
   if (RETRY_PASS) {
-    if (st0 != kRetry) return;
+    const bool take = (st0 == kRetryRows && (P.run_mask & 1)) || (st0 == kRetryV && (P.run_mask & 2));
+    if (!take) return;
     st0 = SCHED_OK;
   }
-  sim_instance<ALGO, ROWS>(P, k, st0, P.retry_status);
+  sim_instance<ALGO, ROWS, false, false, VGLOBAL, RETRY_PASS>(P, k, st0, P.retry_status);
 }
 
 // One wave per instance with ROWS1 rows; when the running set of its instance
@@ -1082,17 +1238,28 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
 // ---------------------------------------------------------------------------
 namespace {
 
-// Kernel variants by register rows.  First launch: `rows`, or with rows2 > 0
-// 5 rows growing to 8 in the same wave (k_simulate_grow).  Retry launch
-// (retry = true): the instances an earlier launch handed over.
+// One launch of the simulation kernel over the batch.
+struct Tier {
+  int rows;         // register rows (first pass: fixed rows, or 5 growing to 8 with grow)
+  bool grow;        // first pass: k_simulate_grow
+  bool retry;       // a retry pass: runs the instances an earlier pass handed over (run_mask)
+  bool vglobal;     // cancelled set in global memory (16 rows)
+  int cap_v;        // LDS slots of the cancelled set (LDS passes)
+  int run_mask;     // retry: bit 0 takes kRetryRows, bit 1 kRetryV
+  int rows_status;  // status for an outgrown running set
+  int v_status;     // status for an outgrown cancelled set
+};
+
 template <int ALGO>
-const void* sim_kernel(int rows, int rows2, bool retry) {
-  if (retry)
-    return rows <= 8    ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, true>)
-           : rows <= 10 ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 10, true>)
-                        : reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true>);
-  if (rows2 > 0) return reinterpret_cast<const void*>(&sk::k_simulate_grow<ALGO, 5>);
-  switch (rows) {
+const void* sim_kernel(const Tier& tr) {
+  if constexpr (ALGO == SCHED_AMIN || ALGO == SCHED_AELL)
+    if (tr.vglobal) return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true, true>);
+  if (tr.retry)
+    return tr.rows <= 8    ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, true>)
+           : tr.rows <= 10 ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 10, true>)
+                           : reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true>);
+  if (tr.grow) return reinterpret_cast<const void*>(&sk::k_simulate_grow<ALGO, 5>);
+  switch (tr.rows) {
     case 1: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 1, false>);
     case 2: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 2, false>);
     case 4: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 4, false>);
@@ -1103,51 +1270,71 @@ const void* sim_kernel(int rows, int rows2, bool retry) {
   }
 }
 
+const void* sim_kernel_any(int algo, const Tier& tr) {
+  switch (algo) {
+    case SCHED_AMAX: return sim_kernel<SCHED_AMAX>(tr);
+    case SCHED_AMIN: return sim_kernel<SCHED_AMIN>(tr);
+    case SCHED_HSF: return sim_kernel<SCHED_HSF>(tr);
+    case SCHED_ARANDOM: return sim_kernel<SCHED_ARANDOM>(tr);
+    default: return sim_kernel<SCHED_AELL>(tr);
+  }
+}
+
 // register rows that hold `want` runs
 int rows_for(int64_t want) {
   const int64_t r = (want + 63) / 64;
   return r <= 1 ? 1 : r <= 2 ? 2 : r <= 4 ? 4 : r <= 5 ? 5 : r <= 6 ? 6 : r <= 8 ? 8 : 16;
 }
 
-struct Tier {
-  int rows, rows2;
-  bool retry;
-};
-
-template <int ALGO>
-hipError_t launch_sim(const Tier& tr, const sk::Params& P, size_t lds, hipStream_t st) {
-  sk::Params p = P;
-  void* args[] = {&p};
-  return hipLaunchKernel(sim_kernel<ALGO>(tr.rows, tr.rows2, tr.retry), dim3(P.K), dim3(64), args, lds, st);
-}
-
-template <int ALGO>
-hipError_t set_lds_limit(const Tier& tr, int bytes) {
-  return hipFuncSetAttribute(sim_kernel<ALGO>(tr.rows, tr.rows2, tr.retry),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-}
-
-hipError_t set_lds_limit_any(int algo, const Tier& tr, int bytes) {
-  switch (algo) {
-    case SCHED_AMAX: return set_lds_limit<SCHED_AMAX>(tr, bytes);
-    case SCHED_AMIN: return set_lds_limit<SCHED_AMIN>(tr, bytes);
-    case SCHED_HSF: return set_lds_limit<SCHED_HSF>(tr, bytes);
-    case SCHED_ARANDOM: return set_lds_limit<SCHED_ARANDOM>(tr, bytes);
-    default: return set_lds_limit<SCHED_AELL>(tr, bytes);
-  }
-}
-
-hipError_t launch_sim_any(int algo, const Tier& tr, const sk::Params& P, size_t lds, hipStream_t st) {
-  switch (algo) {
-    case SCHED_AMAX: return launch_sim<SCHED_AMAX>(tr, P, lds, st);
-    case SCHED_AMIN: return launch_sim<SCHED_AMIN>(tr, P, lds, st);
-    case SCHED_HSF: return launch_sim<SCHED_HSF>(tr, P, lds, st);
-    case SCHED_ARANDOM: return launch_sim<SCHED_ARANDOM>(tr, P, lds, st);
-    default: return launch_sim<SCHED_AELL>(tr, P, lds, st);
-  }
-}
-
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// The launches that simulate a batch under one policy.  The first pass holds
+// up to 320 runs (every run of most instances) and its wave continues with
+// 384, then 512 when its instance outgrows them; instances beyond 512 runs are
+// simulated again with 640 (fewer registers, so more waves per SIMD than with
+// 1024), and beyond 640 with 1024.  The cancelled set (A_min, A_l) first gets
+// cap0 LDS slots (a size chosen for occupancy), an instance that outgrows them
+// is simulated again with as many slots as a workgroup's LDS holds, and one
+// that outgrows those again with a global-memory set of n slots, which always
+// suffices (at most n requests wait cancelled).  So whether an instance
+// completes never depends on the other instances of the batch or on these
+// sizes: only running sets above 1024 runs (or above a caller's forced
+// running capacity) are refused.
+int build_tiers(int algo, int64_t nmax, int forced_rows, int cap0, int cap_fit, Tier* out) {
+  const bool has_v = algo == SCHED_AMIN || algo == SCHED_AELL;
+  const int64_t need_v = has_v ? std::max<int64_t>(nmax, 1) : 0;
+  const int cap1 = has_v ? static_cast<int>(std::min<int64_t>(need_v, cap_fit)) : 0;
+  const bool v_retry = has_v && cap0 < need_v;      // the first pass's set may overflow
+  const bool v_lds_short = has_v && cap1 < need_v;  // even the largest LDS set may
+  int m = 0;
+  if (forced_rows > 0) {
+    out[m++] = Tier{forced_rows, false, false, false, cap0, 0, 0, 0};
+    if (v_retry && cap1 > cap0) out[m++] = Tier{16, false, true, false, cap1, 2, 0, 0};
+    if (v_lds_short) out[m++] = Tier{16, false, true, true, 0, 2, 0, 0};
+  } else if (nmax <= 320) {
+    out[m++] = Tier{rows_for(std::max<int64_t>(nmax, 1)), false, false, false, cap0, 0, 0, 0};
+    if (v_retry && cap1 > cap0) out[m++] = Tier{8, false, true, false, cap1, 2, 0, 0};
+    if (v_lds_short) out[m++] = Tier{16, false, true, true, 0, 2, 0, 0};
+  } else {
+    out[m++] = Tier{5, true, false, false, cap0, 0, 0, 0};
+    if (nmax > 512 || (v_retry && cap1 > cap0))
+      out[m++] = Tier{10, false, true, false, cap1, (nmax > 512 ? 1 : 0) | (v_retry ? 2 : 0), 0, 0};
+    if (nmax > 640) out[m++] = Tier{16, false, true, false, cap1, 1, 0, 0};
+    if (v_lds_short) out[m++] = Tier{16, false, true, true, 0, 2, 0, 0};
+  }
+  // what a pass writes for an instance it cannot hold: a later pass that takes
+  // it, or the final refusal
+  for (int p = 0; p < m; ++p) {
+    bool later_rows = false, later_v = false;
+    for (int q = p + 1; q < m; ++q) {
+      later_rows = later_rows || (out[q].run_mask & 1);
+      later_v = later_v || (out[q].run_mask & 2);
+    }
+    out[p].rows_status = later_rows ? sk::kRetryRows : SCHED_E_UNSUPPORTED;
+    out[p].v_status = later_v ? sk::kRetryV : SCHED_E_UNSUPPORTED;
+  }
+  return m;
+}
 
 // A second stream per device (default priority, created on first use and kept
 // for the life of the process): the adaptive policy runs its A_l launches on
@@ -1170,11 +1357,46 @@ hipError_t side_stream(int dev, hipStream_t* out) {
   return hipSuccess;
 }
 
+// Argument checks shared by the entry points (no HIP call).
+int check_args(const sched_instances_t* in, sched_algo_t algo, int64_t M) {
+  if (!in) return SCHED_E_INVAL;
+  if (algo < SCHED_AMAX || algo > SCHED_ARANDOM) return SCHED_E_INVAL;
+  if (M <= 0 || M >= (int64_t(1) << 30)) return SCHED_E_INVAL;
+  if (in->num_instances < 0 || in->max_requests < 0 || in->total_requests < 0) return SCHED_E_INVAL;
+  if (in->num_instances == 0) return SCHED_OK;
+  if (!in->offsets) return SCHED_E_INVAL;
+  const bool need_l = algo == SCHED_AMIN || algo == SCHED_AELL || algo == SCHED_ADAPTIVE;
+  const bool need_u = algo == SCHED_AMAX || algo == SCHED_AELL || algo == SCHED_ADAPTIVE;
+  if (in->total_requests > 0 && (!in->prompt || !in->output)) return SCHED_E_INVAL;
+  if (in->total_requests > 0 && need_l && !in->lower) return SCHED_E_INVAL;
+  if (in->total_requests > 0 && need_u && !in->upper) return SCHED_E_INVAL;
+  if (in->total_requests > 0 && algo == SCHED_ARANDOM && !in->priority) return SCHED_E_INVAL;
+  if (in->max_requests >= (1 << sk::kIdxBits)) return SCHED_E_UNSUPPORTED;
+  return SCHED_OK;
+}
+
+sk::Params base_params(const sched_instances_t* in, int64_t M) {
+  sk::Params P{};
+  P.K = in->num_instances;
+  P.max_requests = in->max_requests;
+  P.N = in->total_requests;
+  P.offsets = in->offsets;
+  P.arrival = in->arrival;
+  P.prompt = in->prompt;
+  P.output = in->output;
+  P.lower = in->lower;
+  P.upper = in->upper;
+  P.priority = in->priority;
+  P.tie_key = in->total_requests > 0 ? in->tie_key : nullptr;
+  P.M = static_cast<int32_t>(M);
+  return P;
+}
+
 }  // namespace
 
 extern "C" {
 
-int sched_version(void) { return 121; }
+int sched_version(void) { return 130; }
 
 const char* sched_strerror(int code) {
   switch (code) {
@@ -1190,50 +1412,42 @@ const char* sched_strerror(int code) {
   }
 }
 
+int sched_validate(const sched_instances_t* in, sched_algo_t algo, int64_t M, int32_t* status, void* stream) {
+  const int c = check_args(in, algo, M);
+  if (c != SCHED_OK || in->num_instances == 0) return c;
+  if (!status) return SCHED_E_INVAL;
+  sk::Params P = base_params(in, M);
+  P.status = status;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const dim3 grid(P.K), block(64);
+  switch (algo) {
+    case SCHED_AMAX: hipLaunchKernelGGL((sk::k_validate<SCHED_AMAX>), grid, block, 0, st, P); break;
+    case SCHED_AMIN: hipLaunchKernelGGL((sk::k_validate<SCHED_AMIN>), grid, block, 0, st, P); break;
+    case SCHED_HSF: hipLaunchKernelGGL((sk::k_validate<SCHED_HSF>), grid, block, 0, st, P); break;
+    case SCHED_AELL: hipLaunchKernelGGL((sk::k_validate<SCHED_AELL>), grid, block, 0, st, P); break;
+    case SCHED_ARANDOM: hipLaunchKernelGGL((sk::k_validate<SCHED_ARANDOM>), grid, block, 0, st, P); break;
+    default: hipLaunchKernelGGL((sk::k_validate<SCHED_ADAPTIVE>), grid, block, 0, st, P); break;
+  }
+  return hipGetLastError() == hipSuccess ? SCHED_OK : SCHED_E_HIP;
+}
+
 int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t M,
                         const sched_results_t* out, void* stream, const sched_options_t* opts) {
   if (!in || !out) return SCHED_E_INVAL;
-  if (algo < SCHED_AMAX || algo > SCHED_ARANDOM) return SCHED_E_INVAL;
-  const bool need_l = algo == SCHED_AMIN || algo == SCHED_AELL || algo == SCHED_ADAPTIVE;
-  const bool need_u = algo == SCHED_AMAX || algo == SCHED_AELL || algo == SCHED_ADAPTIVE;
-  if (M <= 0 || M >= (int64_t(1) << 30)) return SCHED_E_INVAL;
-  if (in->num_instances < 0 || in->max_requests < 0 || in->total_requests < 0) return SCHED_E_INVAL;
-  if (in->num_instances == 0) return SCHED_OK;
-  if (!in->offsets || !out->total_latency || !out->status) return SCHED_E_INVAL;
-  if (in->total_requests > 0 && (!in->prompt || !in->output || !out->completion)) return SCHED_E_INVAL;
-  if (in->total_requests > 0 && need_l && !in->lower) return SCHED_E_INVAL;
-  if (in->total_requests > 0 && need_u && !in->upper) return SCHED_E_INVAL;
-  if (in->total_requests > 0 && algo == SCHED_ARANDOM && !in->priority) return SCHED_E_INVAL;
-  if (in->max_requests >= (1 << sk::kIdxBits)) return SCHED_E_UNSUPPORTED;
+  {
+    const int c = check_args(in, algo, M);
+    if (c != SCHED_OK || in->num_instances == 0) return c;
+  }
+  if (!out->total_latency || !out->status) return SCHED_E_INVAL;
+  if (in->total_requests > 0 && !out->completion) return SCHED_E_INVAL;
   sched_options_t o{};
   if (opts) o = *opts;
   if (o.step_cap > sk::kCapLimit) return SCHED_E_INVAL;
-  if (o.running_capacity < 0 || o.evicted_capacity < 0) return SCHED_E_INVAL;
+  if (o.running_capacity < 0 || o.evicted_capacity < 0 || o.evicted_lds_limit < 0) return SCHED_E_INVAL;
+  if (o.running_capacity > 1024) return SCHED_E_UNSUPPORTED;
 
   const int64_t nmax = in->max_requests;
-  if (o.running_capacity > 1024) return SCHED_E_UNSUPPORTED;
-  const bool forced = o.running_capacity > 0;
-  // launches: the first holds up to 320 runs (every run of most instances)
-  // and its wave continues with 384, then 512 when its instance outgrows
-  // them; instances beyond 512 runs are simulated again by a launch with 640
-  // (fewer registers, so more waves per SIMD than with 1024), and beyond 640
-  // by one with 1024
-  auto tiers_for = [&](Tier* out) -> int {
-    if (forced) {
-      out[0] = Tier{rows_for(o.running_capacity), 0, false};
-      return 1;
-    }
-    if (nmax <= 320) {
-      out[0] = Tier{rows_for(std::max<int64_t>(nmax, 1)), 0, false};
-      return 1;
-    }
-    int m = 0;
-    out[m++] = Tier{5, 8, false};
-    if (nmax > 512) out[m++] = Tier{10, 0, true};
-    if (nmax > 640) out[m++] = Tier{16, 0, true};
-    return m;
-  };
-
+  const bool tie = in->total_requests > 0 && in->tie_key != nullptr;
   hipStream_t st = static_cast<hipStream_t>(stream);
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return SCHED_E_HIP;
@@ -1243,30 +1457,33 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
 
   const int nw = static_cast<int>((nmax + 63) / 64);
   const int nw1 = (nw + 63) / 64;
-  // evicted-set slots (8 bytes of LDS each).  A_min scans its set per admission,
+  // LDS: the two bitmap levels, then the cancelled set (8 bytes a slot)
+  const size_t lds_bitmaps = 8 * static_cast<size_t>(nw + nw1);
+  if (lds_bitmaps + 8 > static_cast<size_t>(lds_max)) return SCHED_E_UNSUPPORTED;
+  int cap_fit = static_cast<int>((static_cast<size_t>(lds_max) - lds_bitmaps) / 8);
+  if (o.evicted_lds_limit > 0) cap_fit = std::min(cap_fit, o.evicted_lds_limit);
+  // the first pass's cancelled-set slots.  A_min scans its set per admission,
   // so it is kept small where many instances share a CU; A_l's is a FIFO in
   // which every request appears at most once, so n slots never overflow
-  const size_t lds_bitmaps = 8 * static_cast<size_t>(nw + nw1);
-  auto cap_v_for = [&](int a) -> int {
-    if (o.evicted_capacity > 0 && (a == SCHED_AMIN || a == SCHED_AELL)) return o.evicted_capacity;
-    if (a == SCHED_AMIN) {
-      const int64_t def = in->num_instances <= 64 ? 16384 : 1024;
-      return static_cast<int>(std::min<int64_t>(std::max<int64_t>(nmax, 1), def));
-    }
-    if (a == SCHED_AELL) {
-      const int64_t fit = lds_bitmaps < static_cast<size_t>(lds_max)
-                              ? static_cast<int64_t>((static_cast<size_t>(lds_max) - lds_bitmaps) / 8) : 0;
-      return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(std::max<int64_t>(nmax, 1), fit)));
-    }
-    return 0;
+  auto cap0_for = [&](int a) -> int {
+    int64_t c = 0;
+    if (a == SCHED_AMIN) c = std::min<int64_t>(std::max<int64_t>(nmax, 1), in->num_instances <= 64 ? 16384 : 1024);
+    if (a == SCHED_AELL) c = std::max<int64_t>(nmax, 1);
+    if (o.evicted_capacity > 0 && (a == SCHED_AMIN || a == SCHED_AELL)) c = o.evicted_capacity;
+    return static_cast<int>(std::min<int64_t>(c, cap_fit));
   };
-  auto lds_for = [&](int a) -> size_t { return lds_bitmaps + 8 * static_cast<size_t>(cap_v_for(a)); };
+  const int forced_rows = o.running_capacity > 0 ? rows_for(o.running_capacity) : 0;
   // the adaptive policy runs the A_min passes and then the A_l passes; each
   // kernel skips the instances that k_prepare assigned to the other policy
   const int sim_algos[2] = {algo == SCHED_ADAPTIVE ? SCHED_AMIN : static_cast<int>(algo), SCHED_AELL};
   const int n_sim = algo == SCHED_ADAPTIVE ? 2 : 1;
-  for (int a = 0; a < n_sim; ++a)
-    if (lds_for(sim_algos[a]) > static_cast<size_t>(lds_max)) return SCHED_E_UNSUPPORTED;
+  Tier tiers[2][5];
+  int n_tiers[2] = {0, 0};
+  bool any_global = false;
+  for (int a = 0; a < n_sim; ++a) {
+    n_tiers[a] = build_tiers(sim_algos[a], nmax, forced_rows, cap0_for(sim_algos[a]), cap_fit, tiers[a]);
+    for (int p = 0; p < n_tiers[a]; ++p) any_global = any_global || tiers[a][p].vglobal;
+  }
 
   const size_t N = static_cast<size_t>(in->total_requests);
   const size_t K = static_cast<size_t>(in->num_instances);
@@ -1277,21 +1494,16 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   const size_t o_rk = off; off = align_up(off + 4 * N, 256);
   const size_t o_cap = off; off = align_up(off + 4 * K, 256);
   const size_t o_alg = off; off = align_up(off + (algo == SCHED_ADAPTIVE ? 4 * K : 0), 256);
+  const size_t o_tr = off; off = align_up(off + (tie ? 4 * N : 0), 256);
+  const size_t o_ix = off; off = align_up(off + (tie ? 4 * N : 0), 256);
+  const size_t o_cs = off; off = align_up(off + (tie ? 4 * N : 0), 256);
+  const size_t o_es = off; off = align_up(off + (tie && out->evictions ? 4 * N : 0), 256);
+  const size_t o_vg = off; off = align_up(off + (any_global ? 8 * N : 0), 256);
   void* ws = nullptr;
   if (hipMallocAsync(&ws, off, st) != hipSuccess) return SCHED_E_HIP;
   char* base = static_cast<char*>(ws);
 
-  sk::Params P{};
-  P.K = in->num_instances;
-  P.max_requests = in->max_requests;
-  P.N = in->total_requests;
-  P.offsets = in->offsets;
-  P.arrival = in->arrival;
-  P.prompt = in->prompt;
-  P.output = in->output;
-  P.lower = in->lower;
-  P.upper = in->upper;
-  P.priority = in->priority;
+  sk::Params P = base_params(in, M);
   P.completion = out->completion;
   P.evictions = out->evictions;
   P.total_latency = out->total_latency;
@@ -1299,17 +1511,23 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   P.request_steps = out->request_steps;
   P.total_evictions = out->total_evictions;
   P.status = out->status;
-  P.M = static_cast<int32_t>(M);
+  P.algo_used = out->algo_used;
   P.step_cap = o.step_cap;
   P.sort_a = reinterpret_cast<uint32_t*>(base + o_sa);
   P.sort_b = reinterpret_cast<uint32_t*>(base + o_sb);
   P.rec = reinterpret_cast<uint2*>(base + o_rec);
   P.rank_of = reinterpret_cast<int32_t*>(base + o_rk);
+  P.u_of_rank = reinterpret_cast<int32_t*>(P.sort_b);  // free once the keys are sorted (A_l sorts none)
   P.cap = reinterpret_cast<int32_t*>(base + o_cap);
   P.algo_of = algo == SCHED_ADAPTIVE ? reinterpret_cast<int32_t*>(base + o_alg) : nullptr;
-  P.algo_used = out->algo_used;
+  P.tr_of = tie ? reinterpret_cast<int32_t*>(base + o_tr) : nullptr;
+  P.idx_of = tie ? reinterpret_cast<int32_t*>(base + o_ix) : nullptr;
+  P.comp_st = tie ? reinterpret_cast<int32_t*>(base + o_cs) : nullptr;
+  P.ev_st = tie && out->evictions ? reinterpret_cast<int32_t*>(base + o_es) : nullptr;
+  P.vglob = any_global ? reinterpret_cast<uint64_t*>(base + o_vg) : nullptr;
   P.nw_max = nw;
   P.nw1_max = nw1;
+  P.run_cap = forced_rows > 0 ? forced_rows * 64 : INT32_MAX;
 
   hipError_t err = hipSuccess;
   const dim3 grid(P.K), block(64);
@@ -1322,13 +1540,12 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
     default: hipLaunchKernelGGL((sk::k_prepare<SCHED_ADAPTIVE>), grid, block, 0, st, P); break;
   }
   err = hipGetLastError();
-  for (int a = 0; a < n_sim && err == hipSuccess; ++a) {
-    const size_t lds = lds_for(sim_algos[a]);
-    Tier tiers[3];
-    const int n_tiers = tiers_for(tiers);
-    for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass)
-      if (lds > 65536) err = set_lds_limit_any(sim_algos[a], tiers[pass], static_cast<int>(lds));
-  }
+  auto lds_of = [&](const Tier& t) -> size_t { return lds_bitmaps + (t.vglobal ? 0 : 8 * static_cast<size_t>(t.cap_v)); };
+  for (int a = 0; a < n_sim && err == hipSuccess; ++a)
+    for (int p = 0; p < n_tiers[a] && err == hipSuccess; ++p)
+      if (lds_of(tiers[a][p]) > 65536)
+        err = hipFuncSetAttribute(sim_kernel_any(sim_algos[a], tiers[a][p]),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds_of(tiers[a][p])));
   if (err == hipSuccess && o.event_before) err = hipEventRecord(static_cast<hipEvent_t>(o.event_before), st);
   // adaptive: the A_l launches go to the side stream after the preparation,
   // and the caller's stream waits for them before the end (fork and join)
@@ -1342,14 +1559,16 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
     if (err == hipSuccess) err = hipStreamWaitEvent(side, fork, 0);
   }
   for (int a = 0; a < n_sim && err == hipSuccess; ++a) {
-    P.cap_v = cap_v_for(sim_algos[a]);
-    const size_t lds = lds_for(sim_algos[a]);
     const hipStream_t sa = a == 1 ? side : st;
-    Tier tiers[3];
-    const int n_tiers = tiers_for(tiers);
-    for (int pass = 0; pass < n_tiers && err == hipSuccess; ++pass) {
-      P.retry_status = pass + 1 < n_tiers ? sk::kRetry : SCHED_E_UNSUPPORTED;
-      err = launch_sim_any(sim_algos[a], tiers[pass], P, lds, sa);
+    for (int p = 0; p < n_tiers[a] && err == hipSuccess; ++p) {
+      const Tier& t = tiers[a][p];
+      sk::Params q = P;
+      q.cap_v = t.cap_v;
+      q.retry_status = t.rows_status;
+      q.retry_v_status = t.v_status;
+      q.run_mask = t.run_mask;
+      void* args[] = {&q};
+      err = hipLaunchKernel(sim_kernel_any(sim_algos[a], t), grid, block, args, lds_of(t), sa);
     }
   }
   if (side) {

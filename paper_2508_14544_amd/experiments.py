@@ -6,9 +6,9 @@ and instance size n in 200, 400, ..., 2000, it simulates `replicates`
 instances with A_max, A_min, H-SF, A_l and the adaptive A_min/A_l switch on
 the GPU and reports the average end-to-end latency (total latency / n) in
 steps, averaged over the replicates.  Inputs come from
-``workloads.experiment``; the paper's batch-time model (a regression of a
-73B-parameter model on two data-centre GPUs) and its data set are not used:
-every step costs one unit.
+``workloads.experiment``; the paper's batch-time model (Section 6: a linear
+regression predictor of batch time for LLaMA2-70B on two linked A100 GPUs)
+and its data set are not used: every step costs one unit.
 
     python -m paper_2508_14544_amd.experiments [--replicates 64] [--json out.json]
 

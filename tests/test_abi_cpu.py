@@ -47,7 +47,7 @@ def test_probe_library_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strerror(lib):
-    assert lib.sched_version() == 121
+    assert lib.sched_version() == 130
     for code in (0, -1, -2, -3, -4, -5, -6, -7):
         assert B.strerror(code) and B.strerror(code) != "unknown code"
     assert B.strerror(12345) == "unknown code"
@@ -96,5 +96,24 @@ def test_host_validation(lib):
     assert call(lib, _inst(), opts=B.SchedOptions(1 << 31, 0, 0, None, None)) == B.E_INVAL
     assert call(lib, _inst(), opts=B.SchedOptions(0, 2048, 0, None, None)) == B.E_UNSUPPORTED
     assert call(lib, _inst(), opts=B.SchedOptions(0, -1, 0, None, None)) == B.E_INVAL
+    assert call(lib, _inst(), opts=B.SchedOptions(0, 0, -1, None, None)) == B.E_INVAL
+    assert call(lib, _inst(), opts=B.SchedOptions(0, 0, 0, None, None, -1)) == B.E_INVAL
     # an empty batch is a no-op
     assert call(lib, _inst(K=0, N=0)) == B.OK
+
+
+def test_validate_host_checks(lib):
+    # sched_validate rejects the same call-level problems before any HIP call
+    def v(inst, algo=B.AMIN, M=16, status=0x1000):
+        return lib.sched_validate(ctypes.byref(inst) if inst is not None else None, algo, M, status, None)
+    assert v(None) == B.E_INVAL
+    assert v(_inst(), M=0) == B.E_INVAL
+    assert v(_inst(), M=1 << 30) == B.E_INVAL
+    assert v(_inst(), algo=9) == B.E_INVAL
+    assert v(_inst(offsets=None)) == B.E_INVAL
+    assert v(_inst(lower=None), algo=B.AMIN) == B.E_INVAL
+    assert v(_inst(upper=None), algo=B.AMAX) == B.E_INVAL
+    assert v(_inst(priority=None), algo=B.ARANDOM) == B.E_INVAL
+    assert v(_inst(), status=None) == B.E_INVAL
+    assert v(_inst(nmax=1 << 17)) == B.E_UNSUPPORTED
+    assert v(_inst(K=0, N=0)) == B.OK

@@ -115,13 +115,3 @@ def test_twopoint4096_sampled(B, algo):
     _say(f"[oracle] twopoint4096 {algo} on {len(ks)} instances")
     assert_parity(batch, g, oracle_run(batch, a, instances=ks), instances=ks)
     check_algo_used(batch, g, a)  # every instance's choice
-
-
-def test_online1024_aell_sampled(B):
-    # arrivals keep coming after promotions: fresh requests stay ahead of promoted ones
-    batch = W.generate("online1024_n10000_m65536", 0)
-    g = gpu_run(B, batch, O.AELL)
-    ks = [0, 1, 511, 1023] + list(range(100, 1024, 128))
-    ref = oracle_run(batch, O.AELL, instances=ks)
-    assert ref["total_evictions"].sum() > 0
-    assert_parity(batch, g, ref, instances=ks)
