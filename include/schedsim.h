@@ -82,8 +82,13 @@ enum {
                                status: o, u or l >= 2^15, s >= 2^16, n >= 2^17, a priority
                                outside [0, 2^15), or more than 1024 requests (or a forced
                                running_capacity) would run at once                              */
-  SCHED_E_ARRIVAL = -7      /* status: an arrival < 0 or arrivals not non-decreasing in index  */
+  SCHED_E_ARRIVAL = -7,     /* status: an arrival < 0 or arrivals not non-decreasing in index  */
+  SCHED_E_SCRATCH = -8      /* call (sched_simulate_noalloc): the call needs more workspace than
+                               SCHED_NOALLOC_SCRATCH_BYTES                                       */
 };
+
+/* Size of the per-device workspace of sched_simulate_noalloc (96 MiB). */
+#define SCHED_NOALLOC_SCRATCH_BYTES (96u << 20)
 
 /* A batch of K independent instances in CSR layout.  Instance k owns requests
  * [offsets[k], offsets[k+1]); request fields are int32 arrays of length N. */
@@ -176,6 +181,23 @@ int sched_simulate(const sched_instances_t* instances, sched_algo_t algo, int64_
 int sched_simulate_opts(const sched_instances_t* instances, sched_algo_t algo, int64_t M,
                         const sched_results_t* results, void* stream,
                         const sched_options_t* opts);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same as
+ * sched_simulate_opts, but the workspace is a fixed array of
+ * SCHED_NOALLOC_SCRATCH_BYTES in device memory that the library holds on each
+ * device it runs on until the process ends, and nothing is allocated (no
+ * hipMalloc, no stream or event creation: SCHED_ADAPTIVE runs both of its
+ * policies on `stream`).  The workspace needs 20 bytes per request plus 8 per
+ * instance (28 per request with tie keys, 8 more per request when n_max
+ * exceeds the LDS room of the cancelled set); a call that needs more returns
+ * SCHED_E_SCRATCH before queueing anything (e.g. at most about 5.0 million
+ * requests without tie keys).  Every call on a device shares that device's
+ * array: calls whose work overlaps on one device (other streams, other host
+ * threads) race and must be serialised by the caller.  Outputs, statuses and
+ * the caller's pointers are as for sched_simulate_opts. */
+int sched_simulate_noalloc(const sched_instances_t* instances, sched_algo_t algo, int64_t M,
+                           const sched_results_t* results, void* stream, const sched_options_t* opts);
 
 /* Validation only: writes to status[K] (device) the per-instance status that
  * sched_simulate would give each instance before simulating it (SCHED_OK,

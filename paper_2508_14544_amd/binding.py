@@ -17,11 +17,11 @@ LIB_PATH = os.path.join(PKG, "libschedsim.so")
 
 AMAX, AMIN, HSF, AELL, ADAPTIVE, ARANDOM = 0, 1, 2, 3, 4, 5
 ALGOS = {"amax": AMAX, "amin": AMIN, "hsf": HSF, "aell": AELL, "adaptive": ADAPTIVE, "arandom": ARANDOM}
-OK, E_INVAL, E_INTERVAL, E_TOO_BIG, E_STEP_CAP, E_HIP, E_UNSUPPORTED, E_ARRIVAL = 0, -1, -2, -3, -4, -5, -6, -7
+OK, E_INVAL, E_INTERVAL, E_TOO_BIG, E_STEP_CAP, E_HIP, E_UNSUPPORTED, E_ARRIVAL, E_SCRATCH = 0, -1, -2, -3, -4, -5, -6, -7, -8
 
 # every symbol include/schedsim.h declares
-EXPORTED = ("sched_optimum", "sched_simulate", "sched_simulate_opts", "sched_strerror", "sched_validate",
-            "sched_version")
+EXPORTED = ("sched_optimum", "sched_simulate", "sched_simulate_noalloc", "sched_simulate_opts", "sched_strerror",
+            "sched_validate", "sched_version")
 
 
 class SchedInstances(ctypes.Structure):
@@ -84,6 +84,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.sched_simulate_opts.argtypes = [ctypes.POINTER(SchedInstances), ctypes.c_int, ctypes.c_int64,
                                             ctypes.POINTER(SchedResults), ctypes.c_void_p,
                                             ctypes.POINTER(SchedOptions)]
+        lib.sched_simulate_noalloc.restype = ctypes.c_int
+        lib.sched_simulate_noalloc.argtypes = lib.sched_simulate_opts.argtypes
         lib.sched_validate.restype = ctypes.c_int
         lib.sched_validate.argtypes = [ctypes.POINTER(SchedInstances), ctypes.c_int, ctypes.c_int64, ctypes.c_void_p,
                                        ctypes.c_void_p]
@@ -173,8 +175,9 @@ def _instances(db: DeviceBatch, pass_lower: bool = True, pass_upper: bool = True
 def simulate_into(db: DeviceBatch, algo: int, out: Dict[str, object], *, M: Optional[int] = None, stream=None,
                   step_cap: int = 0, running_capacity: int = 0, evicted_capacity: int = 0,
                   evicted_lds_limit: int = 0, event_before=None, event_after=None, pass_lower: bool = True,
-                  pass_upper: bool = True) -> None:
-    """Queue ``sched_simulate_opts`` on ``stream`` (default: torch's current stream)."""
+                  pass_upper: bool = True, no_alloc: bool = False) -> None:
+    """Queue ``sched_simulate_opts`` (``sched_simulate_noalloc`` with no_alloc) on ``stream``
+    (default: torch's current stream)."""
     import torch
     lib = load_library()
     if stream is None:
@@ -186,8 +189,9 @@ def simulate_into(db: DeviceBatch, algo: int, out: Dict[str, object], *, M: Opti
     opts = SchedOptions(int(step_cap), int(running_capacity), int(evicted_capacity),
                         None if event_before is None else int(event_before.cuda_event),
                         None if event_after is None else int(event_after.cuda_event), int(evicted_lds_limit))
-    code = lib.sched_simulate_opts(ctypes.byref(inst), int(algo), int(db.M if M is None else M), ctypes.byref(res),
-                                   ctypes.c_void_p(stream.cuda_stream), ctypes.byref(opts))
+    fn = lib.sched_simulate_noalloc if no_alloc else lib.sched_simulate_opts
+    code = fn(ctypes.byref(inst), int(algo), int(db.M if M is None else M), ctypes.byref(res),
+              ctypes.c_void_p(stream.cuda_stream), ctypes.byref(opts))
     if code != OK:
         raise SchedError(code)
 

@@ -1234,9 +1234,38 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
 }  // namespace sk
 
 // ---------------------------------------------------------------------------
+// The workspace of sched_simulate_noalloc: a fixed array in device memory
+// (each device that runs the library holds its own copy until the process
+// ends).  Host code never passes `scratch` itself to a kernel or a copy (in
+// host code the name is a host-side stand-in): it uses the device address
+// that hipGetSymbolAddress returns, taken once per device.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = size_t(96) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// ---------------------------------------------------------------------------
 // host side: the C ABI
 // ---------------------------------------------------------------------------
 namespace {
+
+// Device address of `scratch` on device `dev` (the current device), looked up
+// on the first call on that device and kept.
+hipError_t scratch_address(int dev, void** out) {
+  constexpr int kMaxDev = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDev] = {};
+  if (dev < 0 || dev >= kMaxDev) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
 
 // One launch of the simulation kernel over the batch.
 struct Tier {
@@ -1408,6 +1437,7 @@ const char* sched_strerror(int code) {
     case SCHED_E_HIP: return "HIP runtime error";
     case SCHED_E_UNSUPPORTED: return "beyond kernel capacity";
     case SCHED_E_ARRIVAL: return "arrivals negative or not non-decreasing";
+    case SCHED_E_SCRATCH: return "workspace beyond the 96 MiB no-allocation scratch";
     default: return "unknown code";
   }
 }
@@ -1431,8 +1461,16 @@ int sched_validate(const sched_instances_t* in, sched_algo_t algo, int64_t M, in
   return hipGetLastError() == hipSuccess ? SCHED_OK : SCHED_E_HIP;
 }
 
-int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t M,
-                        const sched_results_t* out, void* stream, const sched_options_t* opts) {
+}  // extern "C"
+
+namespace {
+
+// sched_simulate_opts and sched_simulate_noalloc.  no_alloc: the workspace is
+// the device's `scratch` array, and the adaptive policy runs both of its
+// policies' launches on the caller's stream (no side stream, no events), so
+// nothing is allocated.
+int simulate_impl(const sched_instances_t* in, sched_algo_t algo, int64_t M, const sched_results_t* out,
+                  void* stream, const sched_options_t* opts, bool no_alloc) {
   if (!in || !out) return SCHED_E_INVAL;
   {
     const int c = check_args(in, algo, M);
@@ -1499,8 +1537,14 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   const size_t o_cs = off; off = align_up(off + (tie ? 4 * N : 0), 256);
   const size_t o_es = off; off = align_up(off + (tie && out->evictions ? 4 * N : 0), 256);
   const size_t o_vg = off; off = align_up(off + (any_global ? 8 * N : 0), 256);
+  // every workspace array is written before it is read (nothing needs clearing)
   void* ws = nullptr;
-  if (hipMallocAsync(&ws, off, st) != hipSuccess) return SCHED_E_HIP;
+  if (no_alloc) {
+    if (off > kScratchBytes) return SCHED_E_SCRATCH;
+    if (scratch_address(dev, &ws) != hipSuccess) return SCHED_E_HIP;
+  } else if (hipMallocAsync(&ws, off, st) != hipSuccess) {
+    return SCHED_E_HIP;
+  }
   char* base = static_cast<char*>(ws);
 
   sk::Params P = base_params(in, M);
@@ -1551,7 +1595,7 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   // and the caller's stream waits for them before the end (fork and join)
   hipStream_t side = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
-  if (err == hipSuccess && n_sim == 2) {
+  if (err == hipSuccess && n_sim == 2 && !no_alloc) {
     err = side_stream(dev, &side);
     if (err == hipSuccess) err = hipEventCreateWithFlags(&fork, hipEventDisableTiming);
     if (err == hipSuccess) err = hipEventCreateWithFlags(&join, hipEventDisableTiming);
@@ -1559,7 +1603,7 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
     if (err == hipSuccess) err = hipStreamWaitEvent(side, fork, 0);
   }
   for (int a = 0; a < n_sim && err == hipSuccess; ++a) {
-    const hipStream_t sa = a == 1 ? side : st;
+    const hipStream_t sa = a == 1 && side ? side : st;
     for (int p = 0; p < n_tiers[a] && err == hipSuccess; ++p) {
       const Tier& t = tiers[a][p];
       sk::Params q = P;
@@ -1582,9 +1626,23 @@ int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t 
   if (fork) (void)hipEventDestroy(fork);
   if (join) (void)hipEventDestroy(join);
   if (err == hipSuccess && o.event_after) err = hipEventRecord(static_cast<hipEvent_t>(o.event_after), st);
-  const hipError_t ferr = hipFreeAsync(ws, st);
+  const hipError_t ferr = no_alloc ? hipSuccess : hipFreeAsync(ws, st);
   if (err != hipSuccess || ferr != hipSuccess) return SCHED_E_HIP;
   return SCHED_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t M,
+                        const sched_results_t* out, void* stream, const sched_options_t* opts) {
+  return simulate_impl(in, algo, M, out, stream, opts, false);
+}
+
+int sched_simulate_noalloc(const sched_instances_t* in, sched_algo_t algo, int64_t M,
+                           const sched_results_t* out, void* stream, const sched_options_t* opts) {
+  return simulate_impl(in, algo, M, out, stream, opts, true);
 }
 
 int sched_simulate(const sched_instances_t* in, sched_algo_t algo, int64_t M,

@@ -48,7 +48,7 @@ def test_probe_library_exports_every_declared_symbol(lib):
 
 def test_version_and_strerror(lib):
     assert lib.sched_version() == 130
-    for code in (0, -1, -2, -3, -4, -5, -6, -7):
+    for code in (0, -1, -2, -3, -4, -5, -6, -7, -8):
         assert B.strerror(code) and B.strerror(code) != "unknown code"
     assert B.strerror(12345) == "unknown code"
 
@@ -100,6 +100,22 @@ def test_host_validation(lib):
     assert call(lib, _inst(), opts=B.SchedOptions(0, 0, 0, None, None, -1)) == B.E_INVAL
     # an empty batch is a no-op
     assert call(lib, _inst(K=0, N=0)) == B.OK
+
+
+def test_noalloc_host_checks(lib):
+    # the no-allocation variant shares the host checks (nothing reaches HIP)
+    def na(inst, algo=B.AMIN, M=16, res=None, opts=None):
+        res = res or _res()
+        return lib.sched_simulate_noalloc(ctypes.byref(inst) if inst is not None else None, algo, M,
+                                          ctypes.byref(res), None, ctypes.byref(opts) if opts else None)
+    assert na(None) == B.E_INVAL
+    assert na(_inst(), M=0) == B.E_INVAL
+    assert na(_inst(), algo=7) == B.E_INVAL
+    assert na(_inst(output=None)) == B.E_INVAL
+    assert na(_inst(), res=_res(status=None)) == B.E_INVAL
+    assert na(_inst(nmax=1 << 17)) == B.E_UNSUPPORTED
+    assert na(_inst(), opts=B.SchedOptions(0, 2048, 0, None, None)) == B.E_UNSUPPORTED
+    assert na(_inst(K=0, N=0)) == B.OK
 
 
 def test_validate_host_checks(lib):
