@@ -414,10 +414,15 @@ __device__ __forceinline__ uint32_t uniform_u32(uint32_t v) {
   return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int32_t>(v)));
 }
 
-// The loop-carried state of one instance's simulation at an admission that
-// found no free register slot: a body with more rows continues from it (its
-// extra rows start empty); the LDS sets stay where they are.
-constexpr int kStateRows = 8;
+// The loop-carried state of one instance's simulation, handed from one body
+// to another with a different number of register rows (the row ladder: 2, 3,
+// 5, 8, 10 rows).  A body grows at an admission that finds no free slot (the
+// next body's extra rows start empty) and shrinks, at the start of a step's
+// admissions, once the running set fits a smaller body with room to spare (it
+// first moves the runs of its upper rows into free slots of the lower ones).
+// The LDS sets stay where they are.  `resume`: continue with the admissions of
+// step t (false: start step t from its arrivals).
+constexpr int kStateRows = 10;
 struct SimState {
   int32_t r_end[kStateRows], r_x[kStateRows], r_c[kStateRows], r_h[kStateRows], r_u[kStateRows];
   uint32_t r_key[kStateRows];
@@ -428,9 +433,34 @@ struct SimState {
   uint64_t f_word;
   int32_t nV, nVe, v_pos, v_head, v_u, n_done, retry_at, t, DT;
   int64_t rsteps, tot_ev;
+  int32_t next_rows;
+  bool resume;
 };
 // Status of a body that handed its state over (TO_STATE) instead of ending.
 constexpr int kResume = -102;
+
+// The row ladder: the body above and below each rung (0: none).
+__host__ __device__ constexpr int ladder_up(int rows) {
+  return rows == 2 ? 3 : rows == 3 ? 5 : rows == 5 ? 8 : rows == 8 ? 10 : 0;
+}
+// A body shrinks to the smallest rung that holds its runs with this many
+// slots to spare (hysteresis: a shrink is never followed at once by a grow).
+constexpr int kShrinkSpare = 16;
+
+// The state of an instance at step 0 (what a body starting fresh holds).
+__device__ __forceinline__ void fresh_state(SimState& st) {
+#pragma unroll
+  for (int r = 0; r < kStateRows; ++r) {
+    st.r_end[r] = INT32_MIN; st.r_x[r] = 0; st.r_c[r] = 0x7FFFFFFF; st.r_h[r] = 0; st.r_key[r] = 0xFFFFFFFFu;
+    st.r_u[r] = 0;
+  }
+  st.fr_row = 0; st.fr_mask = ~0ull; st.N = 0; st.X = 0; st.t_r = 0; st.next_c = 0x7FFFFFFF;
+  st.aw_base = -64; st.aw_a = 0x7FFFFFFF; st.aw_rank = 0; st.arr_ptr = 0; st.next_a = 0;
+  st.f_rank = -1; st.fw_base = -1; st.f_word = 0ull; st.f_key = 0xFFFFFFFFu; st.f_so = 0; st.fw_key = 0xFFFFFFFFu;
+  st.fw_so = 0; st.f_u = 0; st.fw_u = 0; st.nV = 0; st.nVe = 0; st.v_pos = -1; st.v_head = 0;
+  st.v_key = 0xFFFFFFFFu; st.v_so = 0; st.v_u = 0; st.n_done = 0; st.retry_at = 0; st.t = 0; st.DT = 0;
+  st.rsteps = 0; st.tot_ev = 0; st.next_rows = 2; st.resume = false;
+}
 
 // Simulates instance k (whose validation status is st0) with ROWS register
 // rows and writes its outputs.  A running set that outgrows the rows ends the
@@ -452,15 +482,17 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
   extern __shared__ uint64_t lds64[];
   const int lane = threadIdx.x;
   const int64_t b = P.offsets[k];
-  const int n = (st0 == SCHED_OK) ? static_cast<int>(P.offsets[k + 1] - b) : 0;
+  // a body that hands its state over only ever runs valid, non-empty instances
+  const int n = (TO_STATE || st0 == SCHED_OK) ? static_cast<int>(P.offsets[k + 1] - b) : 0;
   const int32_t M = P.M;
 
   int status = st0;
+  int handoff = 0;  // TO_STATE: rows of the body that continues (status kResume)
   // counters live in vector registers (see wave::in_vgpr)
   int64_t rsteps = wave::in_vgpr<int64_t>(FROM_STATE ? st->rsteps : 0);
   int64_t tot_ev = wave::in_vgpr<int64_t>(FROM_STATE ? st->tot_ev : 0);
 
-  if (st0 == SCHED_OK && n > 0) {
+  if (TO_STATE || (st0 == SCHED_OK && n > 0)) {
     uint64_t* L0 = lds64;
     uint64_t* L1 = lds64 + P.nw_max;
     // cancelled requests, one 64-bit entry each.  A_min: key | (s | o << 16) << 32,
@@ -720,7 +752,28 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     }                                                                                \
   } while (0)
     SK_SET_PRIORITY();
-    bool resuming = FROM_STATE;   // continue with the admissions of step t
+    // the state at the admissions of step t, for the body with NR_ rows
+#define SK_SAVE_STATE(NR_)                                                             \
+  do {                                                                                 \
+    _Pragma("unroll") for (int r = 0; r < kStateRows; ++r) {                           \
+      const bool have = r < ROWS;                                                      \
+      st->r_end[r] = have ? r_end[r < ROWS ? r : 0] : kEmpty;                          \
+      st->r_x[r] = have ? r_x[r < ROWS ? r : 0] : 0;                                   \
+      st->r_c[r] = have ? r_c[r < ROWS ? r : 0] : kNever;                              \
+      st->r_h[r] = have ? r_h[r < ROWS ? r : 0] : 0;                                   \
+      st->r_key[r] = have ? r_key[r < ROWS ? r : 0] : 0xFFFFFFFFu;                     \
+      st->r_u[r] = have ? r_u[r < ROWS ? r : 0] : 0;                                   \
+    }                                                                                  \
+    st->fr_row = fr_row; st->fr_mask = fr_mask; st->N = N; st->X = X; st->t_r = t_r;   \
+    st->next_c = next_c; st->aw_base = aw_base; st->aw_a = aw_a; st->aw_rank = aw_rank; \
+    st->arr_ptr = arr_ptr; st->next_a = next_a; st->f_rank = f_rank; st->f_word = f_word; \
+    st->fw_base = fw_base; st->f_key = f_key; st->f_so = f_so; st->fw_key = fw_key;    \
+    st->fw_so = fw_so; st->f_u = f_u; st->fw_u = fw_u; st->nV = nV; st->nVe = nVe;     \
+    st->v_pos = v_pos; st->v_head = v_head; st->v_key = v_key; st->v_so = v_so;        \
+    st->v_u = v_u; st->n_done = n_done; st->retry_at = retry_at; st->t = t; st->DT = DT; \
+    st->rsteps = rsteps; st->tot_ev = tot_ev; st->next_rows = (NR_); st->resume = true; \
+  } while (0)
+    bool resuming = FROM_STATE && st->resume;   // continue with the admissions of step t
     for (;;) {
       if (!resuming) {
       if (t > cap) {
@@ -938,6 +991,57 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       }
       resuming = false;
 
+      // ---- shrink: once the runs fit a smaller body with room to spare, move
+      // the runs of the upper rows into free slots of the lower ones (the
+      // order of slots never matters: every choice is by key) and hand over
+      if constexpr (TO_STATE && ROWS > 2) {
+        int target = 0;
+        if (N <= 64 * 2 - kShrinkSpare) target = 2;
+        else if (ROWS > 3 && N <= 64 * 3 - kShrinkSpare) target = 3;
+        else if (ROWS > 5 && N <= 64 * 5 - kShrinkSpare) target = 5;
+        else if (ROWS > 8 && N <= 64 * 8 - kShrinkSpare) target = 8;
+        if (target > 0) {
+          uint64_t fm[ROWS];
+#pragma unroll
+          for (int r = 0; r < ROWS; ++r) fm[r] = wave::ballot(r_end[r] == kEmpty);
+#pragma unroll
+          for (int h = ROWS - 1; h >= 2; --h) {
+            if (h < target) break;
+            uint64_t m = ~fm[h];
+            while (m) {
+              const int ln = __builtin_ctzll(m);
+              m &= m - 1;
+              // the lowest row below the target with a free lane
+              int l = 0;
+              uint64_t fl_mask = 0;
+#pragma unroll
+              for (int r = ROWS - 1; r >= 0; --r) {
+                const bool ok = r < target && fm[r] != 0ull;
+                l = ok ? r : l;
+                fl_mask = ok ? fm[r] : fl_mask;
+              }
+              const int fl = __builtin_ctzll(fl_mask);
+              const int32_t me = wave::readlane(r_end[h], ln), mx = wave::readlane(r_x[h], ln);
+              const int32_t mc = wave::readlane(r_c[h], ln), mh = wave::readlane(r_h[h], ln);
+              const int32_t mu = wave::readlane(r_u[h], ln);
+              const uint32_t mk = wave::readlane_u(r_key[h], ln);
+              SK_AT_ROW(l, r_end[r] = wave::writelane(r_end[r], me, fl); r_x[r] = wave::writelane(r_x[r], mx, fl);
+                        r_c[r] = wave::writelane(r_c[r], mc, fl); r_h[r] = wave::writelane(r_h[r], mh, fl);
+                        r_u[r] = wave::writelane(r_u[r], mu, fl); r_key[r] = wave::writelane_u(r_key[r], mk, fl);
+                        fm[r] &= ~(1ull << fl);)
+              r_end[h] = wave::writelane(r_end[h], kEmpty, ln);
+              r_c[h] = wave::writelane(r_c[h], kNever, ln);
+              r_key[h] = wave::writelane_u(r_key[h], 0xFFFFFFFFu, ln);
+            }
+          }
+          fr_row = 0;
+          fr_mask = 0ull;  // the next admission looks for a free row
+          handoff = target;
+          status = kResume;
+          break;
+        }
+      }
+
       // ---- 5. admission of the longest feasible prefix in key order
       bool stuck = true;          // the head cannot start before the next event
       int32_t wait_until = t + 1; // otherwise: not before this step
@@ -1020,25 +1124,9 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
             mm = m ? m : mm;
           }
           if (rr < 0) {
-            if (TO_STATE) {
-              // hand the state at this admission to a body with more rows
-#pragma unroll
-              for (int r = 0; r < kStateRows; ++r) {
-                const bool have = r < ROWS;
-                st->r_end[r] = have ? r_end[r < ROWS ? r : 0] : kEmpty;
-                st->r_x[r] = have ? r_x[r < ROWS ? r : 0] : 0;
-                st->r_c[r] = have ? r_c[r < ROWS ? r : 0] : kNever;
-                st->r_h[r] = have ? r_h[r < ROWS ? r : 0] : 0;
-                st->r_key[r] = have ? r_key[r < ROWS ? r : 0] : 0xFFFFFFFFu;
-                st->r_u[r] = have ? r_u[r < ROWS ? r : 0] : 0;
-              }
-              st->fr_row = fr_row; st->fr_mask = fr_mask; st->N = N; st->X = X; st->t_r = t_r;
-              st->next_c = next_c; st->aw_base = aw_base; st->aw_a = aw_a; st->aw_rank = aw_rank;
-              st->arr_ptr = arr_ptr; st->next_a = next_a; st->f_rank = f_rank; st->f_word = f_word; st->fw_base = fw_base;
-              st->f_key = f_key; st->f_so = f_so; st->fw_key = fw_key; st->fw_so = fw_so; st->f_u = f_u;
-              st->fw_u = fw_u; st->nV = nV; st->nVe = nVe; st->v_pos = v_pos; st->v_head = v_head;
-              st->v_key = v_key; st->v_so = v_so; st->v_u = v_u; st->n_done = n_done;
-              st->retry_at = retry_at; st->t = t; st->DT = DT; st->rsteps = rsteps; st->tot_ev = tot_ev;
+            if (TO_STATE && ladder_up(ROWS) > 0) {
+              // hand the state at this admission to the body above
+              handoff = ladder_up(ROWS);
               status = kResume;
             } else {
               status = retry_status;
@@ -1129,7 +1217,12 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       }
       t = tn;
     }
-    if (TO_STATE && status == kResume) return kResume;
+    // every way out of a handing-over body writes the whole state (so that the
+    // state a body started from is dead while it runs)
+    if constexpr (TO_STATE) {
+      SK_SAVE_STATE(handoff);
+      if (status == kResume) return kResume;
+    }
   }
 
   // ---- epilogue: totals from the per-request outputs (with tie keys, first
@@ -1202,23 +1295,55 @@ __global__ __launch_bounds__(64) void k_simulate(Params P) {
   sim_instance<ALGO, ROWS, false, false, VGLOBAL, RETRY_PASS>(P, k, st0, P.retry_status);
 }
 
-// One wave per instance with ROWS1 rows; when the running set of its instance
-// outgrows them, the wave continues the same simulation with 6, then 8 rows
-// (A_l: 8) from the admission that found no free slot (the state moves in
-// registers, the LDS sets stay).  Held to 128 VGPRs so that four waves share
-// a SIMD.
-template <int ALGO, int ROWS1>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_simulate_grow(Params P) {
+// One wave per instance on the row ladder: the simulation starts with 2
+// register rows and moves, state and all, to the body with 3, 5, 8 or 10 rows
+// as its running set grows and back down as it shrinks, so that every scan
+// covers about as many rows as the instance has runs (most of an instance's
+// events happen with at most 128 runs).  A running set beyond 640 runs ends
+// with P.retry_status.  Held to 128 VGPRs so that four waves share a SIMD.
+template <int ALGO>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_simulate_ladder(Params P) {
   const int k = blockIdx.x;
   if (P.algo_of && P.algo_of[k] != ALGO) return;
+  const int st0 = P.status[k];
+  if (st0 == SCHED_OK) {
+    // the bodies all resume from a state, so the bitmaps are cleared here
+    extern __shared__ uint64_t lds64[];
+    const int64_t b = P.offsets[k];
+    const int n = static_cast<int>(P.offsets[k + 1] - b);
+    const int nw = (n + 63) >> 6, nw1 = (nw + 63) >> 6;
+    for (int w = threadIdx.x; w < nw; w += 64) lds64[w] = 0;
+    for (int w = threadIdx.x; w < nw1; w += 64) lds64[P.nw_max + w] = 0;
+    __syncthreads();
+  }
+  const bool empty = st0 == SCHED_OK && P.offsets[k + 1] == P.offsets[k];
+  if (st0 != SCHED_OK || empty) {
+    // nothing to simulate: zero totals (the per-request outputs were set by
+    // the preparation)
+    if (threadIdx.x == 0) {
+      P.total_latency[k] = 0;
+      if (P.makespan) P.makespan[k] = 0;
+      if (P.request_steps) P.request_steps[k] = 0;
+      if (P.total_evictions) P.total_evictions[k] = 0;
+      P.status[k] = st0;
+    }
+    return;
+  }
   SimState st;
-  int r = sim_instance<ALGO, ROWS1, false, true>(P, k, P.status[k], 0, &st);
-  // (A_l's extra register row leaves no room for a third body)
-  if constexpr (ALGO != SCHED_AELL)
-    if (r == kResume) r = sim_instance<ALGO, 6, true, true>(P, k, SCHED_OK, 0, &st);
-  if (r == kResume) sim_instance<ALGO, 8, true, false>(P, k, SCHED_OK, P.retry_status, &st);
+  fresh_state(st);
+  int r;
+  do {
+    switch (st.next_rows) {
+      case 2: r = sim_instance<ALGO, 2, true, true>(P, k, SCHED_OK, P.retry_status, &st); break;
+      case 3: r = sim_instance<ALGO, 3, true, true>(P, k, SCHED_OK, P.retry_status, &st); break;
+      case 5: r = sim_instance<ALGO, 5, true, true>(P, k, SCHED_OK, P.retry_status, &st); break;
+      case 8: r = sim_instance<ALGO, 8, true, true>(P, k, SCHED_OK, P.retry_status, &st); break;
+      default: r = sim_instance<ALGO, 10, true, true>(P, k, SCHED_OK, P.retry_status, &st); break;
+    }
+  } while (r == kResume);
 }
 #undef SK_SET_PRIORITY
+#undef SK_SAVE_STATE
 #undef SK_LOAD_ARRIVALS
 #undef SK_PICK
 #undef SK_F_FIND
@@ -1287,7 +1412,7 @@ const void* sim_kernel(const Tier& tr) {
     return tr.rows <= 8    ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 8, true>)
            : tr.rows <= 10 ? reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 10, true>)
                            : reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 16, true>);
-  if (tr.grow) return reinterpret_cast<const void*>(&sk::k_simulate_grow<ALGO, 5>);
+  if (tr.grow) return reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO>);
   switch (tr.rows) {
     case 1: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 1, false>);
     case 2: return reinterpret_cast<const void*>(&sk::k_simulate<ALGO, 2, false>);
@@ -1340,14 +1465,13 @@ int build_tiers(int algo, int64_t nmax, int forced_rows, int cap0, int cap_fit, 
     out[m++] = Tier{forced_rows, false, false, false, cap0, 0, 0, 0};
     if (v_retry && cap1 > cap0) out[m++] = Tier{16, false, true, false, cap1, 2, 0, 0};
     if (v_lds_short) out[m++] = Tier{16, false, true, true, 0, 2, 0, 0};
-  } else if (nmax <= 320) {
+  } else if (nmax <= 128) {
     out[m++] = Tier{rows_for(std::max<int64_t>(nmax, 1)), false, false, false, cap0, 0, 0, 0};
     if (v_retry && cap1 > cap0) out[m++] = Tier{8, false, true, false, cap1, 2, 0, 0};
     if (v_lds_short) out[m++] = Tier{16, false, true, true, 0, 2, 0, 0};
   } else {
-    out[m++] = Tier{5, true, false, false, cap0, 0, 0, 0};
-    if (nmax > 512 || (v_retry && cap1 > cap0))
-      out[m++] = Tier{10, false, true, false, cap1, (nmax > 512 ? 1 : 0) | (v_retry ? 2 : 0), 0, 0};
+    out[m++] = Tier{2, true, false, false, cap0, 0, 0, 0};
+    if (v_retry && cap1 > cap0) out[m++] = Tier{10, false, true, false, cap1, 2, 0, 0};
     if (nmax > 640) out[m++] = Tier{16, false, true, false, cap1, 1, 0, 0};
     if (v_lds_short) out[m++] = Tier{16, false, true, true, 0, 2, 0, 0};
   }
