@@ -53,6 +53,10 @@
 
 namespace sk {
 
+// global-memory (address space 1) views of device arrays
+typedef __attribute__((address_space(1))) int32_t g_i32;
+typedef __attribute__((address_space(1))) uint64_t g_u64;
+
 constexpr int kIdxBits = 17;
 constexpr uint32_t kIdxMask = (1u << kIdxBits) - 1u;
 constexpr int32_t kEstLimit = 1 << 15;
@@ -433,6 +437,10 @@ struct SimState {
   uint64_t f_word;
   int32_t nV, nVe, v_pos, v_head, v_u, n_done, retry_at, t, DT;
   int64_t rsteps, tot_ev;
+  uint32_t u_key, u_so, u_gate;   // A_min: the register row of recent cancellations (per lane)
+  uint64_t u_used;
+  uint32_t uh_key, uh_so;
+  int32_t uh_lane;
   int32_t next_rows;
   bool resume;
 };
@@ -446,6 +454,9 @@ __host__ __device__ constexpr int ladder_up(int rows) {
 // A body shrinks to the smallest rung that holds its runs with this many
 // slots to spare (hysteresis: a shrink is never followed at once by a grow).
 constexpr int kShrinkSpare = 16;
+// A_min: at the start of a step, a register row of recent cancellations that
+// holds more than this many entries goes to the LDS set
+constexpr int kURowFlush = 48;
 
 // The state of an instance at step 0 (what a body starting fresh holds).
 __device__ __forceinline__ void fresh_state(SimState& st) {
@@ -460,6 +471,8 @@ __device__ __forceinline__ void fresh_state(SimState& st) {
   st.fw_so = 0; st.f_u = 0; st.fw_u = 0; st.nV = 0; st.nVe = 0; st.v_pos = -1; st.v_head = 0;
   st.v_key = 0xFFFFFFFFu; st.v_so = 0; st.v_u = 0; st.n_done = 0; st.retry_at = 0; st.t = 0; st.DT = 0;
   st.rsteps = 0; st.tot_ev = 0; st.next_rows = 2; st.resume = false;
+  st.u_key = 0xFFFFFFFFu; st.u_so = 0; st.u_gate = 0; st.u_used = 0ull;
+  st.uh_key = 0xFFFFFFFFu; st.uh_so = 0; st.uh_lane = -1;
 }
 
 // Simulates instance k (whose validation status is st0) with ROWS register
@@ -510,14 +523,18 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
 
     const int32_t cap = P.cap[k];
     // array bases in vector registers
+    // array bases in vector registers, typed as global memory: plain pointers
+    // would compile to flat accesses, and a flat store or atomic holds the
+    // LDS wait counter until its global write completes, so every later LDS
+    // wait of the wave would also wait for it
     auto base = [](auto* p) { return wave::in_vgpr(p); };
-    const uint2* rec = base(P.rec + b);
-    const int32_t* arrival = P.arrival ? base(P.arrival + b) : nullptr;
-    const int32_t* rank_of = base(P.rank_of + b);
-    const int32_t* upper_k = ALGO == SCHED_AELL ? P.u_of_rank + b : nullptr;  // by rank
+    const g_u64* rec = base((const g_u64*)(P.rec + b));  // (key, s | o << 16) as one 64-bit word
+    const g_i32* arrival = P.arrival ? base((const g_i32*)(P.arrival + b)) : nullptr;
+    const g_i32* rank_of = base((const g_i32*)(P.rank_of + b));
+    const g_i32* upper_k = ALGO == SCHED_AELL ? (const g_i32*)(P.u_of_rank + b) : nullptr;  // by rank
     // per-request outputs by id (with tie keys: the staging arrays)
-    int32_t* completion = base((P.tie_key ? P.comp_st : P.completion) + b);
-    int32_t* evictions = P.evictions ? base((P.tie_key ? P.ev_st : P.evictions) + b) : nullptr;
+    g_i32* completion = base((g_i32*)((P.tie_key ? P.comp_st : P.completion) + b));
+    g_i32* evictions = P.evictions ? base((g_i32*)((P.tie_key ? P.ev_st : P.evictions) + b)) : nullptr;
 
     // running set: register rows; an empty slot has r_end = kEmpty, r_c = kNever,
     // r_key = ~0, which every scan below treats as neutral, so scans cover all rows
@@ -548,6 +565,17 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     int32_t nV = 0, nVe = 0, v_pos = -1, v_head = 0;
     uint32_t v_key = 0xFFFFFFFFu, v_so = 0;
     int32_t v_u = 0;
+    // A_min: requests cancelled recently wait in a register row first (lane j
+    // holds one: key and s | o << 16; u_gate is ~0 in the lanes filled at this
+    // step, which may not start before the next one), with its smallest
+    // startable entry cached in uh_*; a full row goes to the LDS set at the
+    // start of a step.  Requests are usually started again within a step or
+    // two of their cancellation, so most starts find their request here
+    // without a scan of the LDS set.
+    uint32_t u_key = 0xFFFFFFFFu, u_so = 0, u_gate = 0;
+    uint64_t u_used = 0ull;
+    uint32_t uh_key = 0xFFFFFFFFu, uh_so = 0;
+    int32_t uh_lane = -1;
     int32_t n_done = 0;
     // the head cannot start before retry_at; valid until the next event
     int32_t retry_at = 0;
@@ -560,6 +588,8 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       fw_so = st->fw_so; f_u = st->f_u; fw_u = st->fw_u;
       nV = st->nV; nVe = st->nVe; v_pos = st->v_pos; v_head = st->v_head; v_key = st->v_key; v_so = st->v_so;
       v_u = st->v_u; n_done = st->n_done; retry_at = st->retry_at; t = st->t; DT = st->DT;
+      u_key = st->u_key; u_so = st->u_so; u_gate = st->u_gate; u_used = st->u_used;
+      uh_key = st->uh_key; uh_so = st->uh_so; uh_lane = st->uh_lane;
     }
 
 #define SK_LOAD_ARRIVALS()                                                           \
@@ -583,9 +613,9 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       fw_key = 0xFFFFFFFFu;                                                          \
       fw_so = 0u;                                                                    \
       if (rr_ < n) {                                                                 \
-        const uint2 rv_ = rec[rr_];                                                  \
-        fw_key = rv_.x;                                                              \
-        fw_so = rv_.y;                                                               \
+        const uint64_t rv_ = rec[rr_];                                               \
+        fw_key = static_cast<uint32_t>(rv_);                                         \
+        fw_so = static_cast<uint32_t>(rv_ >> 32);                                    \
         if (ALGO == SCHED_AELL) fw_u = upper_k[rr_];                                 \
       }                                                                              \
     }                                                                                \
@@ -699,14 +729,30 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       v_so = s_ | (o_ << 16);                                                        \
     }                                                                                \
   } while (0)
+    // A_min: the smallest startable entry of the register row
+#define SK_U_FIND()                                                                  \
+  do {                                                                               \
+    const uint32_t uk_ = u_key | u_gate;                                             \
+    const uint32_t um_ = wave::min_u32_all(uk_);                                     \
+    const uint64_t ua_ = wave::ballot(uk_ == um_);                                   \
+    uh_key = wave::uniform_u(um_);                                                   \
+    uh_lane = -1;                                                                    \
+    if (uh_key != 0xFFFFFFFFu) {                                                     \
+      uh_lane = __builtin_ctzll(ua_);                                                \
+      uh_so = wave::readlane_u(u_so, uh_lane);                                       \
+    }                                                                                \
+  } while (0)
     // the head of the waiting set: smaller key of the fresh and cancelled heads
     // (A_l: every fresh request comes before the promoted ones); derived where
     // it is used rather than carried through the loop
 #define SK_PICK()                                                                    \
-  const bool c_any = f_rank >= 0 || (kHasV && v_pos >= 0);                           \
-  const bool c_fromF = !kHasV || (f_rank >= 0 && (ALGO == SCHED_AELL || f_key < v_key)); \
-  const uint32_t c_key = c_fromF ? f_key : v_key;                                    \
-  const uint32_t c_so = c_fromF ? f_so : v_so;                                       \
+  const bool c_fromU = ALGO == SCHED_AMIN && uh_key < v_key;                         \
+  const uint32_t vh_key = c_fromU ? uh_key : v_key;                                  \
+  const uint32_t vh_so = c_fromU ? uh_so : v_so;                                     \
+  const bool c_any = f_rank >= 0 || (kHasV && (v_pos >= 0 || c_fromU));              \
+  const bool c_fromF = !kHasV || (f_rank >= 0 && (ALGO == SCHED_AELL || f_key < vh_key)); \
+  const uint32_t c_key = c_fromF ? f_key : vh_key;                                   \
+  const uint32_t c_so = c_fromF ? f_so : vh_so;                                      \
   const int32_t c_s = static_cast<int32_t>(c_so & 0xFFFFu);                          \
   const int32_t c_o = static_cast<int32_t>(c_so >> 16);                              \
   const int32_t c_est = ALGO == SCHED_ARANDOM ? c_o : static_cast<int32_t>(c_key >> kIdxBits); \
@@ -772,6 +818,8 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     st->v_pos = v_pos; st->v_head = v_head; st->v_key = v_key; st->v_so = v_so;        \
     st->v_u = v_u; st->n_done = n_done; st->retry_at = retry_at; st->t = t; st->DT = DT; \
     st->rsteps = rsteps; st->tot_ev = tot_ev; st->next_rows = (NR_); st->resume = true; \
+    st->u_key = u_key; st->u_so = u_so; st->u_gate = u_gate; st->u_used = u_used;     \
+    st->uh_key = uh_key; st->uh_so = uh_so; st->uh_lane = uh_lane;                    \
   } while (0)
     bool resuming = FROM_STATE && st->resume;   // continue with the admissions of step t
     for (;;) {
@@ -820,6 +868,45 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       if (ALGO == SCHED_AMIN && nVe != nV) {
         SK_V_MERGE();
         heads_changed = true;
+      }
+      if (ALGO == SCHED_AMIN && u_used != 0ull) {
+        const int cnt = __builtin_popcountll(u_used);
+        const bool fresh_u = wave::ballot(u_gate != 0u) != 0ull;  // cancelled at the last step
+        if (cnt > kURowFlush) {
+          // the row goes to the LDS set (every entry of it may start now)
+          if (nV + cnt > cap_v) {
+            status = P.retry_v_status;
+            break;
+          }
+          const bool mine = (u_used >> lane) & 1ull;
+          const int slot = nV + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                                   static_cast<uint32_t>(u_used >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(u_used), 0u)));
+          if (mine) vent[slot] = (static_cast<uint64_t>(u_so) << 32) | u_key;
+          const uint32_t k_ = u_key;
+          u_key = 0xFFFFFFFFu;
+          u_gate = 0u;
+          u_used = 0ull;
+          // its smallest entry competes with the LDS set's head
+          const uint32_t um_ = wave::min_u32_all(mine ? k_ : 0xFFFFFFFFu);
+          const uint64_t ua_ = wave::ballot(mine && k_ == um_);
+          const uint32_t mk_ = wave::uniform_u(um_);
+          if (mk_ < v_key) {
+            const int ln_ = __builtin_ctzll(ua_);
+            v_key = mk_;
+            v_so = wave::readlane_u(u_so, ln_);
+            v_pos = wave::readlane(slot, ln_);
+          }
+          nV += cnt;
+          nVe = nV;
+          uh_key = 0xFFFFFFFFu;
+          uh_lane = -1;
+          heads_changed = true;
+        } else if (fresh_u) {
+          u_gate = 0u;
+          SK_U_FIND();
+          heads_changed = true;
+        }
       }
       if (heads_changed) event = true;
 
@@ -905,7 +992,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
               int slot = v_head + nV;
               slot = slot >= cap_v ? slot - cap_v : slot;
               vent[slot] = imin | (sk << 17) | (okk << 33) | (static_cast<uint64_t>(uk) << 48);
-              if (evictions) atomicAdd(&evictions[imin], 1);
+              if (evictions) __hip_atomic_fetch_add(&evictions[imin], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             ++nV;
             ++tot_ev;
@@ -952,7 +1039,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
               status = SCHED_E_UNSUPPORTED;
               break;
             }
-            if (nV >= cap_v) {
+            if (u_used == ~0ull && nV >= cap_v) {
               status = P.retry_v_status;
               break;
             }
@@ -975,12 +1062,24 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
             const int32_t nh = gen > oh ? gen : oh;
             const int32_t sk = xk - t_r + pk;
             const int32_t okk = ck - pk;
-            if (lane == 0) {
-              const uint32_t so = static_cast<uint32_t>(sk) | (static_cast<uint32_t>(okk) << 16);
-              vent[nV] = (static_cast<uint64_t>(so) << 32) | ((static_cast<uint32_t>(nh) << kIdxBits) | idx);
-              if (evictions) atomicAdd(&evictions[idx], 1);
+            const uint32_t so = static_cast<uint32_t>(sk) | (static_cast<uint32_t>(okk) << 16);
+            const uint32_t nkey = (static_cast<uint32_t>(nh) << kIdxBits) | idx;
+            if (u_used != ~0ull) {
+              // into a free lane of the register row, startable from the next step
+              const int ul = __builtin_ctzll(~u_used);
+              u_key = wave::writelane_u(u_key, nkey, ul);
+              u_so = wave::writelane_u(u_so, so, ul);
+              u_gate = wave::writelane_u(u_gate, 0xFFFFFFFFu, ul);
+              u_used |= 1ull << ul;
+              if (lane == 0 && evictions)
+                __hip_atomic_fetch_add(&evictions[idx], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            } else {
+              if (lane == 0) {
+                vent[nV] = (static_cast<uint64_t>(so) << 32) | nkey;
+                if (evictions) __hip_atomic_fetch_add(&evictions[idx], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              }
+              ++nV;
             }
-            ++nV;
             ++tot_ev;
           }
           if (status != SCHED_OK) break;
@@ -1167,6 +1266,11 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
           v_head = v_head + 1 == cap_v ? 0 : v_head + 1;
           --nV;
           SK_V_HEAD();
+        } else if (ALGO == SCHED_AMIN && c_fromU) {
+          // from the register row
+          u_key = wave::writelane_u(u_key, 0xFFFFFFFFu, uh_lane);
+          u_used &= ~(1ull << uh_lane);
+          SK_U_FIND();
         } else {
           // the last eligible entry moves into the hole; the last pending one fills
           // its place.  Lane 0 and lane 1 do the two moves with one read and one
@@ -1192,7 +1296,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       // ---- 6. this step processes every running request once
       rsteps += N;
       int32_t tn = t + 1;
-      if (ALGO != SCHED_AMIN || nV == nVe) {
+      if (ALGO != SCHED_AMIN || (nV == nVe && !wave::ballot(u_gate != 0u))) {
         // Nothing changes before the next completion, arrival or (A_min)
         // overflow; until then the head cannot start before wait_until (or at
         // all when stuck: the memory at t+1 only grows).
@@ -1353,6 +1457,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
 #undef SK_V_SCAN
 #undef SK_V_MERGE
 #undef SK_V_HEAD
+#undef SK_U_FIND
 #undef SK_AT_ROW
 #undef SK_DROP_SHARE
 
