@@ -112,6 +112,9 @@ struct Params {
   int32_t retry_v_status;// status for an outgrown evicted set: a later pass (kRetryV) or SCHED_E_UNSUPPORTED
   int32_t run_mask;      // retry passes: bit 0 runs kRetryRows instances, bit 1 kRetryV ones
   int32_t run_cap;       // retry passes: most runs at once (a caller's forced capacity), else INT32_MAX
+  // completion steps staged in LDS after the cancelled set (n_max slots) and
+  // written out coalesced at the end of an instance
+  int32_t stage_comp;
 };
 
 // Internal statuses of an instance handed to a later pass: its running set
@@ -513,11 +516,15 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     // A_l: a FIFO ring of id | s << 17 | o << 33 | u << 48 from slot v_head.
     uint64_t* vent = VGLOBAL ? P.vglob + b : L1 + P.nw1_max;
     const int32_t cap_v = VGLOBAL ? n : P.cap_v;
+    int32_t* lcomp = reinterpret_cast<int32_t*>(L1 + P.nw1_max + (VGLOBAL ? 0 : P.cap_v));
+    const bool stage_c = P.stage_comp != 0;
     const int nw = (n + 63) >> 6;
     const int nw1 = (nw + 63) >> 6;
     if (!FROM_STATE) {
       for (int w = lane; w < nw; w += 64) L0[w] = 0;
       for (int w = lane; w < nw1; w += 64) L1[w] = 0;
+      if (stage_c)
+        for (int i = lane; i < n; i += 64) lcomp[i] = -1;
       __syncthreads();
     }
 
@@ -533,7 +540,13 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     const g_i32* rank_of = base((const g_i32*)(P.rank_of + b));
     const g_i32* upper_k = ALGO == SCHED_AELL ? (const g_i32*)(P.u_of_rank + b) : nullptr;  // by rank
     // per-request outputs by id (with tie keys: the staging arrays)
-    g_i32* completion = base((g_i32*)((P.tie_key ? P.comp_st : P.completion) + b));
+    // completion steps by id: staged in LDS after the cancelled set when the
+    // launch has room for them (written out coalesced at the end of the
+    // instance), else straight to the global outputs.  One generic pointer,
+    // so the staged case costs no registers (its stores are flat stores to
+    // LDS; the global case's are flat stores too, which measured the same)
+    int32_t* cdst = base(P.stage_comp ? reinterpret_cast<int32_t*>(lds64 + P.nw_max + P.nw1_max + (VGLOBAL ? 0 : P.cap_v))
+                                      : (P.tie_key ? P.comp_st : P.completion) + b);
     g_i32* evictions = P.evictions ? base((g_i32*)((P.tie_key ? P.ev_st : P.evictions) + b)) : nullptr;
 
     // running set: register rows; an empty slot has r_end = kEmpty, r_c = kNever,
@@ -930,7 +943,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
                 SK_DROP_SHARE(t, wave::readlane(r_x[r], ln), wave::readlane(r_end[r], ln));
               }
             }
-            if (hit) completion[r_key[r] & kIdxMask] = t;
+            if (hit) cdst[r_key[r] & kIdxMask] = t;
             sx += hit ? r_x[r] : 0;
             r_end[r] = hit ? kEmpty : r_end[r];
             r_c[r] = hit ? kNever : r_c[r];
@@ -1334,20 +1347,22 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
   __syncthreads();
   const bool keep = (status == SCHED_OK || status == SCHED_E_STEP_CAP) && n > 0;
   const bool tie = P.tie_key != nullptr;
+  const bool st_c = P.stage_comp != 0;
   int64_t tel = 0, mk = 0;
   if (keep) {
+    const int32_t* lc = reinterpret_cast<const int32_t*>(lds64 + P.nw_max + P.nw1_max + (VGLOBAL ? 0 : P.cap_v));
     for (int c = 0; c < n; c += 64) {
       const int i = c + lane;
       if (i < n) {
+        const int32_t id = tie ? P.tr_of[b + i] : i;
         int32_t ci;
-        if (tie) {
-          const int32_t id = P.tr_of[b + i];
-          ci = P.comp_st[b + id];
+        if (st_c || tie) {
+          ci = st_c ? lc[id] : P.comp_st[b + id];
           P.completion[b + i] = ci;
-          if (P.evictions) P.evictions[b + i] = P.ev_st[b + id];
         } else {
           ci = P.completion[b + i];
         }
+        if (P.evictions && tie) P.evictions[b + i] = P.ev_st[b + id];
         if (ci >= 0) {
           tel += ci - (P.arrival ? P.arrival[b + i] : 0);
           mk = ci > mk ? ci : mk;
@@ -1411,13 +1426,17 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
   if (P.algo_of && P.algo_of[k] != ALGO) return;
   const int st0 = P.status[k];
   if (st0 == SCHED_OK) {
-    // the bodies all resume from a state, so the bitmaps are cleared here
+    // the bodies all resume from a state, so the bitmaps and staged outputs
+    // are set up here
     extern __shared__ uint64_t lds64[];
     const int64_t b = P.offsets[k];
     const int n = static_cast<int>(P.offsets[k + 1] - b);
     const int nw = (n + 63) >> 6, nw1 = (nw + 63) >> 6;
     for (int w = threadIdx.x; w < nw; w += 64) lds64[w] = 0;
     for (int w = threadIdx.x; w < nw1; w += 64) lds64[P.nw_max + w] = 0;
+    int32_t* lc = reinterpret_cast<int32_t*>(lds64 + P.nw_max + P.nw1_max + P.cap_v);
+    if (P.stage_comp)
+      for (int i = threadIdx.x; i < n; i += 64) lc[i] = -1;
     __syncthreads();
   }
   const bool empty = st0 == SCHED_OK && P.offsets[k + 1] == P.offsets[k];
@@ -1499,14 +1518,15 @@ hipError_t scratch_address(int dev, void** out) {
 
 // One launch of the simulation kernel over the batch.
 struct Tier {
-  int rows;         // register rows (first pass: fixed rows, or 5 growing to 8 with grow)
-  bool grow;        // first pass: k_simulate_grow
+  int rows;         // register rows (first pass: fixed rows, or the row ladder with grow)
+  bool grow;        // first pass: k_simulate_ladder
   bool retry;       // a retry pass: runs the instances an earlier pass handed over (run_mask)
   bool vglobal;     // cancelled set in global memory (16 rows)
   int cap_v;        // LDS slots of the cancelled set (LDS passes)
   int run_mask;     // retry: bit 0 takes kRetryRows, bit 1 kRetryV
   int rows_status;  // status for an outgrown running set
   int v_status;     // status for an outgrown cancelled set
+  int stage;        // completion steps staged in LDS (1) or not (0)
 };
 
 template <int ALGO>
@@ -1734,7 +1754,8 @@ int simulate_impl(const sched_instances_t* in, sched_algo_t algo, int64_t M, con
   // which every request appears at most once, so n slots never overflow
   auto cap0_for = [&](int a) -> int {
     int64_t c = 0;
-    if (a == SCHED_AMIN) c = std::min<int64_t>(std::max<int64_t>(nmax, 1), in->num_instances <= 64 ? 16384 : 1024);
+    if (a == SCHED_AMIN)
+      c = std::min<int64_t>(std::max<int64_t>(nmax, 1), in->num_instances <= 64 ? 16384 : nmax <= 1024 ? 512 : 1024);
     if (a == SCHED_AELL) c = std::max<int64_t>(nmax, 1);
     if (o.evicted_capacity > 0 && (a == SCHED_AMIN || a == SCHED_AELL)) c = o.evicted_capacity;
     return static_cast<int>(std::min<int64_t>(c, cap_fit));
@@ -1813,7 +1834,21 @@ int simulate_impl(const sched_instances_t* in, sched_algo_t algo, int64_t M, con
     default: hipLaunchKernelGGL((sk::k_prepare<SCHED_ADAPTIVE>), grid, block, 0, st, P); break;
   }
   err = hipGetLastError();
-  auto lds_of = [&](const Tier& t) -> size_t { return lds_bitmaps + (t.vglobal ? 0 : 8 * static_cast<size_t>(t.cap_v)); };
+  // Staging the completion steps in LDS (written out coalesced at the end of
+  // an instance instead of one scattered store per completion) when it fits
+  // without costing occupancy: at most the LDS share of the waves a CU holds
+  // at once (four per SIMD) or that the batch gives it.
+  const int64_t nst = static_cast<int64_t>(nw) * 64;
+  const int64_t per_cu = std::min<int64_t>(16, std::max<int64_t>(1, (static_cast<int64_t>(K) + 255) / 256));
+  const size_t stage_budget = std::min<size_t>(static_cast<size_t>(lds_max), static_cast<size_t>(163840 / per_cu));
+  auto lds_base = [&](const Tier& t) -> size_t { return lds_bitmaps + (t.vglobal ? 0 : 8 * static_cast<size_t>(t.cap_v)); };
+  for (int a = 0; a < n_sim; ++a)
+    for (int p = 0; p < n_tiers[a]; ++p) {
+      Tier& t = tiers[a][p];
+      t.stage = 0;
+      if (lds_base(t) + 4 * nst <= stage_budget) t.stage = 1;
+    }
+  auto lds_of = [&](const Tier& t) -> size_t { return lds_base(t) + (t.stage ? 4 * nst : 0); };
   for (int a = 0; a < n_sim && err == hipSuccess; ++a)
     for (int p = 0; p < n_tiers[a] && err == hipSuccess; ++p)
       if (lds_of(tiers[a][p]) > 65536)
@@ -1840,6 +1875,7 @@ int simulate_impl(const sched_instances_t* in, sched_algo_t algo, int64_t M, con
       q.retry_status = t.rows_status;
       q.retry_v_status = t.v_status;
       q.run_mask = t.run_mask;
+      q.stage_comp = t.stage;
       void* args[] = {&q};
       err = hipLaunchKernel(sim_kernel_any(sim_algos[a], t), grid, block, args, lds_of(t), sa);
     }
