@@ -165,7 +165,9 @@ typedef struct {
                                For tests of the global-memory set on small instances.      */
 } sched_options_t;
 
-/* Simulate every instance with the given policy and budget M (0 < M < 2^30).
+/* Simulate every instance with the given policy (algo: a sched_algo_t value,
+ * passed as int32_t so that any value is well defined; others give
+ * SCHED_E_INVAL) and budget M (0 < M < 2^30).
  * Returns SCHED_OK once the work is queued, or a call-level error code (then
  * nothing was queued).  Per-instance problems are reported in results.status;
  * other instances still run.  Scratch memory is allocated stream-ordered on
@@ -174,11 +176,11 @@ typedef struct {
  * device (default priority, kept until the process ends) and joins back into
  * `stream` with events, so all of the call's work is ordered before whatever
  * the caller queues on `stream` next. */
-int sched_simulate(const sched_instances_t* instances, sched_algo_t algo, int64_t M,
+int sched_simulate(const sched_instances_t* instances, int32_t algo, int64_t M,
                    const sched_results_t* results, void* stream);
 
 /* Same, with options (opts may be NULL = all defaults). */
-int sched_simulate_opts(const sched_instances_t* instances, sched_algo_t algo, int64_t M,
+int sched_simulate_opts(const sched_instances_t* instances, int32_t algo, int64_t M,
                         const sched_results_t* results, void* stream,
                         const sched_options_t* opts);
 
@@ -196,7 +198,7 @@ int sched_simulate_opts(const sched_instances_t* instances, sched_algo_t algo, i
  * array: calls whose work overlaps on one device (other streams, other host
  * threads) race and must be serialised by the caller.  Outputs, statuses and
  * the caller's pointers are as for sched_simulate_opts. */
-int sched_simulate_noalloc(const sched_instances_t* instances, sched_algo_t algo, int64_t M,
+int sched_simulate_noalloc(const sched_instances_t* instances, int32_t algo, int64_t M,
                            const sched_results_t* results, void* stream, const sched_options_t* opts);
 
 /* Validation only: writes to status[K] (device) the per-instance status that
@@ -207,7 +209,7 @@ int sched_simulate_noalloc(const sched_instances_t* instances, sched_algo_t algo
  * `algo` (the adaptive policy validates with the policy it picks).  No
  * workspace; asynchronous on `stream`.  Returns a call-level code like
  * sched_simulate (SCHED_E_INVAL for NULL pointers or M outside (0, 2^30)). */
-int sched_validate(const sched_instances_t* instances, sched_algo_t algo, int64_t M, int32_t* status,
+int sched_validate(const sched_instances_t* instances, int32_t algo, int64_t M, int32_t* status,
                    void* stream);
 
 /* The hindsight optimum of tiny instances (n_k <= 8): the minimum total

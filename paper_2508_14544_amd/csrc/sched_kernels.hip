@@ -1636,7 +1636,7 @@ hipError_t side_stream(int dev, hipStream_t* out) {
 }
 
 // Argument checks shared by the entry points (no HIP call).
-int check_args(const sched_instances_t* in, sched_algo_t algo, int64_t M) {
+int check_args(const sched_instances_t* in, int32_t algo, int64_t M) {
   if (!in) return SCHED_E_INVAL;
   if (algo < SCHED_AMAX || algo > SCHED_ARANDOM) return SCHED_E_INVAL;
   if (M <= 0 || M >= (int64_t(1) << 30)) return SCHED_E_INVAL;
@@ -1691,7 +1691,7 @@ const char* sched_strerror(int code) {
   }
 }
 
-int sched_validate(const sched_instances_t* in, sched_algo_t algo, int64_t M, int32_t* status, void* stream) {
+int sched_validate(const sched_instances_t* in, int32_t algo, int64_t M, int32_t* status, void* stream) {
   const int c = check_args(in, algo, M);
   if (c != SCHED_OK || in->num_instances == 0) return c;
   if (!status) return SCHED_E_INVAL;
@@ -1718,7 +1718,7 @@ namespace {
 // the device's `scratch` array, and the adaptive policy runs both of its
 // policies' launches on the caller's stream (no side stream, no events), so
 // nothing is allocated.
-int simulate_impl(const sched_instances_t* in, sched_algo_t algo, int64_t M, const sched_results_t* out,
+int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sched_results_t* out,
                   void* stream, const sched_options_t* opts, bool no_alloc) {
   if (!in || !out) return SCHED_E_INVAL;
   {
@@ -1900,17 +1900,17 @@ int simulate_impl(const sched_instances_t* in, sched_algo_t algo, int64_t M, con
 
 extern "C" {
 
-int sched_simulate_opts(const sched_instances_t* in, sched_algo_t algo, int64_t M,
+int sched_simulate_opts(const sched_instances_t* in, int32_t algo, int64_t M,
                         const sched_results_t* out, void* stream, const sched_options_t* opts) {
   return simulate_impl(in, algo, M, out, stream, opts, false);
 }
 
-int sched_simulate_noalloc(const sched_instances_t* in, sched_algo_t algo, int64_t M,
+int sched_simulate_noalloc(const sched_instances_t* in, int32_t algo, int64_t M,
                            const sched_results_t* out, void* stream, const sched_options_t* opts) {
   return simulate_impl(in, algo, M, out, stream, opts, true);
 }
 
-int sched_simulate(const sched_instances_t* in, sched_algo_t algo, int64_t M,
+int sched_simulate(const sched_instances_t* in, int32_t algo, int64_t M,
                    const sched_results_t* out, void* stream) {
   return sched_simulate_opts(in, algo, M, out, stream, nullptr);
 }
