@@ -8,8 +8,10 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libschedsim.so")
-SOURCES = [os.path.join(PKG, "csrc", "sched_kernels.hip"), os.path.join(PKG, "csrc", "opt_kernels.hip")]
-HEADERS = [os.path.join(PKG, "csrc", "wave.hpp"), os.path.join(ROOT, "include", "schedsim.h")]
+SOURCES = [os.path.join(PKG, "csrc", "sched_kernels.hip"), os.path.join(PKG, "csrc", "sched_wide.hip"),
+           os.path.join(PKG, "csrc", "opt_kernels.hip")]
+HEADERS = [os.path.join(PKG, "csrc", "wave.hpp"), os.path.join(PKG, "csrc", "sim_device.hpp"),
+           os.path.join(ROOT, "include", "schedsim.h")]
 # throughput probes for the roofline (measurement infrastructure, own library)
 PROBE_LIB = os.path.join(PKG, "libschedprobe.so")
 PROBE_SOURCES = [os.path.join(PKG, "csrc", "probe_kernels.hip")]
