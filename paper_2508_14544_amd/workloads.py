@@ -216,16 +216,38 @@ def _bins_for(alpha: Fraction, o: np.ndarray, max_o: int):
     return tab[0][o], tab[1][o]
 
 
+# the workloads whose policies are given only lower bounds by default
+_LOWER_ONLY = {"sweep65536_n2000_m32768"}
+_CHUNK_REQUESTS = 1 << 23  # larger batches are drawn in chunks of instances (bounded memory)
+
+
 def generate(name: str, seed: int = 0, instance_ids: Optional[Sequence[int]] = None,
-             with_upper: bool = True) -> Instances:
-    """Generate a workload (or a subset of its instances) deterministically."""
+             with_upper: Optional[bool] = None) -> Instances:
+    """Generate a workload (or a subset of its instances) deterministically.
+
+    with_upper: whether to draw the upper bounds u (default: all workloads
+    except the sweep, whose A_min is given only lower bounds)."""
     w = WORKLOADS[name]
+    if with_upper is None:
+        with_upper = name not in _LOWER_ONLY
     if instance_ids is None:
         ids = np.arange(w.num_instances, dtype=np.int64)
     else:
         ids = np.asarray(list(instance_ids), dtype=np.int64)
         if ids.size and (ids.min() < 0 or ids.max() >= w.num_instances):
             raise ValueError("instance id out of range")
+    step = max(1, _CHUNK_REQUESTS // max(1, w.n))
+    if ids.size > step:
+        # every instance has its own random streams, so chunks concatenate to
+        # exactly the batch drawn at once
+        parts = [generate(name, seed, ids[c:c + step], with_upper) for c in range(0, ids.size, step)]
+        cat = lambda f: (None if getattr(parts[0], f) is None
+                         else np.concatenate([getattr(p, f) for p in parts]).astype(np.int32))
+        meta = dict(parts[0].meta)
+        if "alpha" in meta:
+            meta["alpha"] = [a for p in parts for a in p.meta["alpha"]]
+        return Instances(name, w.M, np.arange(ids.size + 1, dtype=np.int64) * w.n, cat("arrival"), cat("prompt"),
+                         cat("output"), cat("lower"), cat("upper"), ids, meta)
     K, n, wid = ids.size, w.n, w.workload_id
     R = lambda fld: raw64(seed, wid, fld, ids, n)
     meta: Dict[str, object] = {"seed": seed, "workload": name}

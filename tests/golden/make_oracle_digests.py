@@ -5,7 +5,7 @@ Only the oracle and the seeded generator are called.  Run from the repo root:
     python tests/golden/make_oracle_digests.py [workload[:algo,...] ...] [--threads T]
 With no arguments every (workload, policy) pair below is (re)computed; the
 file is rewritten after each pair, so an interrupted run keeps what finished.
-The whole set takes about 3.5 hours of CPU time (the 65536-instance sweep
+The whole set takes about 9 hours of CPU time (the 65536-instance sweep
 under A_min is most of it).
 """
 import argparse
@@ -33,6 +33,8 @@ PLAN = [
     ("online1024_n10000_m65536", ["amin", "amax", "hsf", "aell"], True),
     # A_min is given only the lower bounds here (H-SF reads neither bound)
     ("sweep65536_n2000_m32768", ["amin", "hsf"], False),
+    # the two-point workload of Section 5.1 (A_l and the adaptive switch)
+    ("twopoint4096_n1000_m16384", ["aell", "adaptive", "amin", "hsf"], True),
 ]
 CHUNK = 2048  # instances generated and simulated at once (a multiple of the digest block)
 

@@ -179,7 +179,7 @@ def test_reduction_exact_predictions_all_equal():
         rs = [O.simulate(inst, a, b.M) for a in (O.AMAX, O.AMIN, O.HSF)]
         assert same(rs[0], rs[2]) and same(rs[1], rs[2])
     # a generated batch instance with alpha = 0
-    g = W.generate("sweep65536_n2000_m32768", 0, instance_ids=[3])
+    g = W.generate("sweep65536_n2000_m32768", 0, instance_ids=[3], with_upper=True)
     inst = g.instance(0)
     assert np.array_equal(inst["lower"], inst["output"])
     rs = [O.simulate(inst, a, g.M) for a in (O.AMAX, O.AMIN, O.HSF)]

@@ -53,7 +53,7 @@ def test_deterministic_and_subset_independent():
 ])
 def test_ranges(name, ids):
     w = W.WORKLOADS[name]
-    b = W.generate(name, 0, instance_ids=ids)
+    b = W.generate(name, 0, instance_ids=ids, with_upper=True)
     assert b.M == w.M and b.max_requests == w.n and b.num_instances == len(ids)
     assert np.all(b.lower >= 1) and np.all(b.lower <= b.output) and np.all(b.output <= b.upper)
     assert np.all(b.prompt + b.upper <= b.M)
@@ -127,3 +127,16 @@ def test_experiment_recipe():
     oo = e3.output.astype(np.int64)
     assert (e3.lower == np.maximum(1, 5 * oo // 100)).all()
     assert (e3.upper == -((-195 * oo) // 100)).all()
+
+
+def test_chunked_generation_equals_drawing_at_once(monkeypatch):
+    # large batches are drawn in chunks of instances; every instance has its
+    # own random streams, so the result is the same batch
+    import paper_2508_14544_amd.workloads as WW
+    a = W.generate("batch4096_n1000_m16384", 0, instance_ids=range(100, 400))
+    monkeypatch.setattr(WW, "_CHUNK_REQUESTS", 1 << 15)
+    b = W.generate("batch4096_n1000_m16384", 0, instance_ids=range(100, 400))
+    for f in ("offsets", "arrival", "prompt", "output", "lower", "upper", "instance_ids"):
+        assert np.array_equal(getattr(a, f), getattr(b, f)), f
+    assert a.meta["alpha"] == b.meta["alpha"]
+    assert W.generate("sweep65536_n2000_m32768", 0, instance_ids=range(3)).upper is None
