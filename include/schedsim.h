@@ -150,14 +150,16 @@ typedef struct {
                                a larger one starts with 320, grows to 384 and 512 within the
                                same launch, and is simulated again from step 0 with 640,
                                then 1024, if it outgrows that)                             */
-  int32_t evicted_capacity; /* LDS slots of the cancelled set (A_min, A_l) in the first launch;
-                               0: default (A_min: min(n_max, 16384) for batches of at most 64
-                               instances, else min(n_max, 1024); A_l: n_max; both clipped to
-                               what a workgroup's LDS holds).  An instance that outgrows them
-                               is simulated again with as many slots as the LDS holds, and
-                               one that outgrows those with a set of n slots in global memory
-                               (8 bytes of workspace per request when n_max exceeds the LDS
-                               room).                                                       */
+  int32_t evicted_capacity; /* LDS slots of A_min's cancelled set in the first launch; 0:
+                               default (min(n_max, 16384) for batches of at most 64 instances,
+                               else min(n_max, 512) for n_max <= 1024 and min(n_max, 1024)
+                               above; clipped to what a workgroup's LDS holds).  An instance
+                               that outgrows them is simulated again with as many slots as the
+                               LDS holds, and one that outgrows those with a set of n slots in
+                               global memory (8 bytes of workspace per request when n_max
+                               exceeds the LDS room).  A_l's queue of promoted requests is
+                               always an array of n entries in global memory (8 bytes of
+                               workspace per request).                                      */
   void* event_before;       /* hipEvent_t recorded just before the simulation kernel, or NULL */
   void* event_after;        /* hipEvent_t recorded just after it, or NULL                  */
   int32_t evicted_lds_limit;/* > 0: at most this many LDS slots for the cancelled set in any
@@ -191,8 +193,9 @@ int sched_simulate_opts(const sched_instances_t* instances, int32_t algo, int64_
  * device it runs on until the process ends, and nothing is allocated (no
  * hipMalloc, no stream or event creation: SCHED_ADAPTIVE runs both of its
  * policies on `stream`).  The workspace needs 20 bytes per request plus 8 per
- * instance (28 per request with tie keys, 8 more per request when n_max
- * exceeds the LDS room of the cancelled set); a call that needs more returns
+ * instance, 16 more per request with tie keys, and 8 more per request for
+ * A_l and the adaptive policy or when n_max exceeds the LDS room of A_min's
+ * cancelled set; a call that needs more returns
  * SCHED_E_SCRATCH before queueing anything (e.g. at most about 5.0 million
  * requests without tie keys).  Every call on a device shares that device's
  * array: calls whose work overlaps on one device (other streams, other host

@@ -114,7 +114,8 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 // batch or on these sizes: only running sets above 1024 runs, or above a
 // caller's forced running capacity, are refused.
 int build_tiers(int algo, int64_t nmax, int64_t K, int forced_rows, int cap0, int cap_fit, Tier* out) {
-  const bool has_v = algo == SCHED_AMIN || algo == SCHED_AELL;
+  // (A_l's queue lives in global memory and never overflows)
+  const bool has_v = algo == SCHED_AMIN;
   const int64_t need_v = has_v ? std::max<int64_t>(nmax, 1) : 0;
   const int cap1 = has_v ? static_cast<int>(std::min<int64_t>(need_v, cap_fit)) : 0;
   const bool v_retry = has_v && cap0 < need_v && cap1 > cap0;  // a larger LDS set may help
@@ -286,15 +287,14 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   if (lds_bitmaps + 8 > static_cast<size_t>(lds_max)) return SCHED_E_UNSUPPORTED;
   int cap_fit = static_cast<int>((static_cast<size_t>(lds_max) - lds_bitmaps) / 8);
   if (o.evicted_lds_limit > 0) cap_fit = std::min(cap_fit, o.evicted_lds_limit);
-  // the first pass's cancelled-set slots.  A_min scans its set per admission,
-  // so it is kept small where many instances share a CU; A_l's is a FIFO in
-  // which every request appears at most once, so n slots never overflow
+  // the first pass's cancelled-set slots (A_min; A_l's promoted queue is an
+  // array of n entries in global memory).  A_min scans its set per
+  // admission, so it is kept small where many instances share a CU
   auto cap0_for = [&](int a) -> int {
     int64_t c = 0;
     if (a == SCHED_AMIN)
       c = std::min<int64_t>(std::max<int64_t>(nmax, 1), in->num_instances <= 64 ? 16384 : nmax <= 1024 ? 512 : 1024);
-    if (a == SCHED_AELL) c = std::max<int64_t>(nmax, 1);
-    if (o.evicted_capacity > 0 && (a == SCHED_AMIN || a == SCHED_AELL)) c = o.evicted_capacity;
+    if (o.evicted_capacity > 0 && a == SCHED_AMIN) c = o.evicted_capacity;
     return static_cast<int>(std::min<int64_t>(c, cap_fit));
   };
   const int forced_rows = o.running_capacity > 0 ? rows_for(o.running_capacity) : 0;
@@ -304,7 +304,7 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   const int n_sim = algo == SCHED_ADAPTIVE ? 2 : 1;
   Tier tiers[2][5];
   int n_tiers[2] = {0, 0};
-  bool any_global = false;
+  bool any_global = algo == SCHED_AELL || algo == SCHED_ADAPTIVE;  // A_l's promoted queue
   for (int a = 0; a < n_sim; ++a) {
     n_tiers[a] = build_tiers(sim_algos[a], nmax, in->num_instances, forced_rows, cap0_for(sim_algos[a]), cap_fit,
                              tiers[a]);

@@ -450,6 +450,8 @@ struct SimStateT {
   int32_t uh_lane;
   int32_t next_rows;
   bool resume;
+  uint32_t vw_lo, vw_hi;          // A_l: register window of the promoted queue (per lane)
+  int32_t vw_base;
 };
 // the narrow ladder (up to 10 rows, four waves a SIMD) and the wide one (up
 // to 16 rows, for few large instances and for instances that outgrow the
@@ -488,6 +490,7 @@ __device__ __forceinline__ void fresh_state(ST& st) {
   st.rsteps = 0; st.tot_ev = 0; st.next_rows = 2; st.resume = false;
   st.u_key = 0xFFFFFFFFu; st.u_so = 0; st.u_gate = 0; st.u_used = 0ull;
   st.uh_key = 0xFFFFFFFFu; st.uh_so = 0; st.uh_lane = -1;
+  st.vw_lo = 0; st.vw_hi = 0; st.vw_base = -(1 << 30);
 }
 
 // Simulates instance k (whose validation status is st0) with ROWS register
@@ -528,7 +531,12 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     // slots [0, nVe) may start now, [nVe, nV) were cancelled at this step.
     // A_l: a FIFO ring of id | s << 17 | o << 33 | u << 48 from slot v_head.
     uint64_t* vent = VGLOBAL ? P.vglob + b : L1 + P.nw1_max;
-    const int32_t cap_v = VGLOBAL ? n : P.cap_v;
+    // A_l: every request is promoted at most once, so its queue is an
+    // append-only array of n entries in global memory (the instance's slice
+    // of the workspace), read through a 64-entry register window
+    constexpr bool kQueue = ALGO == SCHED_AELL;
+    g_u64* qg = kQueue ? (g_u64*)(P.vglob + b) : nullptr;
+    const int32_t cap_v = (VGLOBAL || kQueue) ? n : P.cap_v;
     int32_t* lcomp = reinterpret_cast<int32_t*>(L1 + P.nw1_max + (VGLOBAL ? 0 : P.cap_v));
     const bool stage_c = P.stage_comp != 0;
     const int nw = (n + 63) >> 6;
@@ -591,6 +599,10 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     int32_t nV = 0, nVe = 0, v_pos = -1, v_head = 0;
     uint32_t v_key = 0xFFFFFFFFu, v_so = 0;
     int32_t v_u = 0;
+    // A_l: queue entries [vw_base, vw_base + 64) in lane order (entries
+    // appended inside the window are written to it as well)
+    uint32_t vw_lo = 0, vw_hi = 0;
+    int32_t vw_base = -(1 << 30);
     // A_min: requests cancelled recently wait in a register row first (lane j
     // holds one: key and s | o << 16; u_gate is ~0 in the lanes filled at this
     // step, which may not start before the next one), with its smallest
@@ -614,8 +626,13 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       fw_so = st->fw_so; f_u = st->f_u; fw_u = st->fw_u;
       nV = st->nV; nVe = st->nVe; v_pos = st->v_pos; v_head = st->v_head; v_key = st->v_key; v_so = st->v_so;
       v_u = st->v_u; n_done = st->n_done; retry_at = st->retry_at; t = st->t; DT = st->DT;
-      u_key = st->u_key; u_so = st->u_so; u_gate = st->u_gate; u_used = st->u_used;
-      uh_key = st->uh_key; uh_so = st->uh_so; uh_lane = st->uh_lane;
+      if constexpr (ALGO == SCHED_AMIN) {
+        u_key = st->u_key; u_so = st->u_so; u_gate = st->u_gate; u_used = st->u_used;
+        uh_key = st->uh_key; uh_so = st->uh_so; uh_lane = st->uh_lane;
+      }
+      if constexpr (ALGO == SCHED_AELL) {
+        vw_lo = st->vw_lo; vw_hi = st->vw_hi; vw_base = st->vw_base;
+      }
     }
 
 #define SK_LOAD_ARRIVALS()                                                           \
@@ -739,13 +756,25 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     }                                                                                \
     nVe = nV;                                                                        \
   } while (0)
-    // A_l: the oldest promoted request (head of the ring), planned with u
+    // A_l: the oldest promoted request (head of the queue), planned with u.
+    // The window moves to the head when the head leaves it; the fence makes
+    // the lane-0 appends visible to the other lanes' loads.
 #define SK_V_HEAD()                                                                  \
   do {                                                                               \
     v_pos = -1;                                                                      \
     v_key = 0xFFFFFFFFu;                                                             \
     if (nV > 0) {                                                                    \
-      const uint64_t e_ = uniform_u64(vent[v_head]);                                 \
+      if (v_head - vw_base >= 64 || v_head < vw_base) {                              \
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup");                       \
+        vw_base = v_head;                                                            \
+        const int j_ = v_head + lane;                                                \
+        const uint64_t w_ = j_ < n ? static_cast<uint64_t>(qg[j_]) : 0ull;           \
+        vw_lo = static_cast<uint32_t>(w_);                                           \
+        vw_hi = static_cast<uint32_t>(w_ >> 32);                                     \
+      }                                                                              \
+      const int d_ = v_head - vw_base;                                               \
+      const uint64_t e_ = (static_cast<uint64_t>(wave::readlane_u(vw_hi, d_)) << 32) | \
+                          wave::readlane_u(vw_lo, d_);                               \
       const uint32_t ix_ = static_cast<uint32_t>(e_) & kIdxMask;                     \
       const uint32_t s_ = static_cast<uint32_t>(e_ >> 17) & 0xFFFFu;                 \
       const uint32_t o_ = static_cast<uint32_t>(e_ >> 33) & 0x7FFFu;                 \
@@ -844,8 +873,13 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     st->v_pos = v_pos; st->v_head = v_head; st->v_key = v_key; st->v_so = v_so;        \
     st->v_u = v_u; st->n_done = n_done; st->retry_at = retry_at; st->t = t; st->DT = DT; \
     st->rsteps = rsteps; st->tot_ev = tot_ev; st->next_rows = (NR_); st->resume = true; \
-    st->u_key = u_key; st->u_so = u_so; st->u_gate = u_gate; st->u_used = u_used;     \
-    st->uh_key = uh_key; st->uh_so = uh_so; st->uh_lane = uh_lane;                    \
+    if constexpr (ALGO == SCHED_AMIN) {                                                \
+      st->u_key = u_key; st->u_so = u_so; st->u_gate = u_gate; st->u_used = u_used;   \
+      st->uh_key = uh_key; st->uh_so = uh_so; st->uh_lane = uh_lane;                  \
+    }                                                                                  \
+    if constexpr (ALGO == SCHED_AELL) {                                                \
+      st->vw_lo = vw_lo; st->vw_hi = vw_hi; st->vw_base = vw_base;                     \
+    }                                                                                  \
   } while (0)
     bool resuming = FROM_STATE && st->resume;   // continue with the admissions of step t
     for (;;) {
@@ -1014,11 +1048,17 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
             const int32_t pk = t - static_cast<int32_t>(kk >> kIdxBits);
             const uint64_t sk = static_cast<uint32_t>(xk - t_r + pk);
             const uint64_t okk = static_cast<uint32_t>(ck - pk);
-            if (lane == 0) {
-              int slot = v_head + nV;
-              slot = slot >= cap_v ? slot - cap_v : slot;
-              vent[slot] = imin | (sk << 17) | (okk << 33) | (static_cast<uint64_t>(uk) << 48);
-              if (evictions) __hip_atomic_fetch_add(&evictions[imin], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            {
+              const int slot = v_head + nV;  // < n: each request is promoted at most once
+              const uint64_t qe = imin | (sk << 17) | (okk << 33) | (static_cast<uint64_t>(uk) << 48);
+              if (lane == 0) {
+                qg[slot] = qe;
+                if (evictions) __hip_atomic_fetch_add(&evictions[imin], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              }
+              if (slot >= vw_base && slot - vw_base < 64) {
+                vw_lo = wave::writelane_u(vw_lo, static_cast<uint32_t>(qe), slot - vw_base);
+                vw_hi = wave::writelane_u(vw_hi, static_cast<uint32_t>(qe >> 32), slot - vw_base);
+              }
             }
             ++nV;
             ++tot_ev;
@@ -1291,7 +1331,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
         if (c_fromF) {
           SK_F_TAKE();
         } else if (ALGO == SCHED_AELL) {
-          v_head = v_head + 1 == cap_v ? 0 : v_head + 1;
+          ++v_head;
           --nV;
           SK_V_HEAD();
         } else if (ALGO == SCHED_AMIN && c_fromU) {
