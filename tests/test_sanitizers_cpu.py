@@ -35,17 +35,26 @@ def test_library_host_checks_under_asan_ubsan(tmp_path):
     hipcc = "/opt/rocm/bin/hipcc"
     if not os.path.exists(hipcc) or not shutil.which("gcc"):
         pytest.skip("hipcc or gcc not found")
-    drv, lib, exe = str(tmp_path / "abi_driver.o"), str(tmp_path / "sk.o"), str(tmp_path / "abi_san")
+    drv, exe = str(tmp_path / "abi_driver.o"), str(tmp_path / "abi_san")
     rc, log = _run(["gcc", "-O1", "-g", "-std=c99", "-c", "-I", os.path.join(ROOT, "include"),
                     os.path.join(SAN, "abi_driver.c"), "-o", drv])
     assert rc == 0, log
     # host-only sanitizers on the library: each -fsanitize= right after -Xarch_host
     san = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined"]
-    rc, log = _run([hipcc, "--offload-arch=gfx950", "-O1", "-g", "-std=c++17", *san, "-Xclang", "-target-feature",
-                    "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"), "-c",
-                    os.path.join(ROOT, "paper_2508_14544_amd", "csrc", "sched_kernels.hip"), "-o", lib], timeout=900)
-    assert rc == 0, log
-    rc, log = _run([hipcc, "--offload-arch=gfx950", *san, lib, drv, "-o", exe], timeout=300)
+    # the three translation units compile concurrently (device code unoptimised:
+    # nothing here launches a kernel)
+    objs, procs = [], []
+    for src in ("sched_kernels.hip", "sched_wide.hip", "opt_kernels.hip"):
+        obj = str(tmp_path / (src + ".o"))
+        objs.append(obj)
+        procs.append(subprocess.Popen([hipcc, "--offload-arch=gfx950", "-Xarch_device", "-O0", "-O1", "-g",
+                                       "-std=c++17", *san, "-I", os.path.join(ROOT, "include"), "-c",
+                                       os.path.join(ROOT, "paper_2508_14544_amd", "csrc", src), "-o", obj],
+                                      stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True))
+    for pr in procs:
+        log = pr.communicate(timeout=900)[0]
+        assert pr.returncode == 0, log
+    rc, log = _run([hipcc, "--offload-arch=gfx950", *san, *objs, drv, "-o", exe], timeout=300)
     assert rc == 0, log
     rc, log = _run([exe], env=ENV, timeout=120)
     assert rc == 0 and "ERROR: AddressSanitizer" not in log and "runtime error" not in log, log
