@@ -39,7 +39,8 @@ def kernel_source_hash() -> str:
     h = hashlib.sha256()
     # the kernel sources and the build script (its compiler flags shape the code)
     for p in ("paper_2508_14544_amd/csrc/sched_kernels.hip", "paper_2508_14544_amd/csrc/sim_device.hpp",
-              "paper_2508_14544_amd/csrc/sched_wide.hip", "paper_2508_14544_amd/csrc/wave.hpp",
+              "paper_2508_14544_amd/csrc/sched_wide.hip", "paper_2508_14544_amd/csrc/sched_group.hip",
+              "paper_2508_14544_amd/csrc/wave.hpp",
               "paper_2508_14544_amd/build.py"):
         h.update(open(os.path.join(ROOT, p), "rb").read())
     return h.hexdigest()[:16]

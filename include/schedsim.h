@@ -136,20 +136,21 @@ typedef struct {
 /* Capacities.  Outputs never depend on any of the sizes below, nor on which
  * other instances share a batch: an instance whose running set or cancelled
  * set outgrows the room of one launch is simulated again from step 0 by a
- * later launch with more room.  Only an instance that needs more than 1024
- * concurrently running requests (or more than a forced running_capacity)
- * ends with status SCHED_E_UNSUPPORTED. */
+ * later launch with more room.  One wave holds up to 1024 concurrently running
+ * requests; an instance that needs more is simulated again by a workgroup of 4
+ * waves (4096 runs), then of 8 waves (8192 runs; for A_max and A_l only when
+ * n_max is below about 96000, where the LDS holds eight copies of the waiting
+ * set's bitmaps and the completion lists).  Only an instance that needs more,
+ * or more than a forced running_capacity, ends with SCHED_E_UNSUPPORTED. */
 typedef struct {
   int64_t step_cap;         /* last simulated step; <= 0: per instance
                                min(2^30, 4*(max a + sum(o+1)) + 64)                       */
   int32_t running_capacity; /* > 0 (<= 1024): hold at most this many concurrently running
                                requests per instance, rounded up to 64, 128, 256, 320, 384,
-                               512 or 1024; an instance that needs more gets
-                               SCHED_E_UNSUPPORTED.  0: as many as it needs, up to 1024 (an
-                               instance of up to 320 requests gets room for all of them;
-                               a larger one starts with 320, grows to 384 and 512 within the
-                               same launch, and is simulated again from step 0 with 640,
-                               then 1024, if it outgrows that)                             */
+                               512 or 1024, on one wave; an instance that needs more gets
+                               SCHED_E_UNSUPPORTED.  0: as many as it needs (one wave's
+                               register rows follow the running set, 128 to 640 runs, then
+                               1024 in a retry launch; beyond that, workgroups as above)    */
   int32_t evicted_capacity; /* LDS slots of A_min's cancelled set in the first launch; 0:
                                default (min(n_max, 16384) for batches of at most 64 instances,
                                else min(n_max, 512) for n_max <= 1024 and min(n_max, 1024)
@@ -165,6 +166,15 @@ typedef struct {
   int32_t evicted_lds_limit;/* > 0: at most this many LDS slots for the cancelled set in any
                                launch (beyond them the global-memory set); 0: as many as fit.
                                For tests of the global-memory set on small instances.      */
+  int32_t workgroup_waves;  /* 0 or 1: one wave per instance first (the default).  2 or 4:
+                               every instance is simulated by a workgroup of that many waves
+                               from the start, each wave holding 1/W of the running set in
+                               1024/(64 W) register rows (SCHED_AMAX, SCHED_AMIN, SCHED_HSF
+                               only; other values or policies give SCHED_E_INVAL).  The waves
+                               agree on each step's decisions through LDS and a barrier; the
+                               outputs are the same.  A_min's cancelled set then lives in
+                               global memory (n entries per wave) unless two waves' copies
+                               fit the LDS.                                                  */
 } sched_options_t;
 
 /* Simulate every instance with the given policy (algo: a sched_algo_t value,

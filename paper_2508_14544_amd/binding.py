@@ -61,6 +61,7 @@ class SchedOptions(ctypes.Structure):
         ("event_before", ctypes.c_void_p),
         ("event_after", ctypes.c_void_p),
         ("evicted_lds_limit", ctypes.c_int32),
+        ("workgroup_waves", ctypes.c_int32),
     ]
 
 
@@ -175,7 +176,7 @@ def _instances(db: DeviceBatch, pass_lower: bool = True, pass_upper: bool = True
 def simulate_into(db: DeviceBatch, algo: int, out: Dict[str, object], *, M: Optional[int] = None, stream=None,
                   step_cap: int = 0, running_capacity: int = 0, evicted_capacity: int = 0,
                   evicted_lds_limit: int = 0, event_before=None, event_after=None, pass_lower: bool = True,
-                  pass_upper: bool = True, no_alloc: bool = False) -> None:
+                  pass_upper: bool = True, no_alloc: bool = False, workgroup_waves: int = 0) -> None:
     """Queue ``sched_simulate_opts`` (``sched_simulate_noalloc`` with no_alloc) on ``stream``
     (default: torch's current stream)."""
     import torch
@@ -188,7 +189,8 @@ def simulate_into(db: DeviceBatch, algo: int, out: Dict[str, object], *, M: Opti
                        _ptr(out["status"]), _ptr(out.get("algo_used")))
     opts = SchedOptions(int(step_cap), int(running_capacity), int(evicted_capacity),
                         None if event_before is None else int(event_before.cuda_event),
-                        None if event_after is None else int(event_after.cuda_event), int(evicted_lds_limit))
+                        None if event_after is None else int(event_after.cuda_event), int(evicted_lds_limit),
+                        int(workgroup_waves))
     fn = lib.sched_simulate_noalloc if no_alloc else lib.sched_simulate_opts
     code = fn(ctypes.byref(inst), int(algo), int(db.M if M is None else M), ctypes.byref(res),
               ctypes.c_void_p(stream.cuda_stream), ctypes.byref(opts))

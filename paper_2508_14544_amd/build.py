@@ -9,7 +9,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libschedsim.so")
 SOURCES = [os.path.join(PKG, "csrc", "sched_kernels.hip"), os.path.join(PKG, "csrc", "sched_wide.hip"),
-           os.path.join(PKG, "csrc", "opt_kernels.hip")]
+           os.path.join(PKG, "csrc", "sched_group.hip"), os.path.join(PKG, "csrc", "opt_kernels.hip")]
 HEADERS = [os.path.join(PKG, "csrc", "wave.hpp"), os.path.join(PKG, "csrc", "sim_device.hpp"),
            os.path.join(ROOT, "include", "schedsim.h")]
 # throughput probes for the roofline (measurement infrastructure, own library)
@@ -30,12 +30,30 @@ SIM_FLAGS = ["-mllvm", "--amdgpu-sched-strategy=iterative-ilp"]
 
 
 def _compile(sources, lib, verbose, extra):
-    tmp = lib + f".tmp{os.getpid()}"
-    cmd = [HIPCC, *FLAGS, *extra, *sources, "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.check_call(cmd)
-    os.replace(tmp, lib)
+    """Each translation unit to an object (concurrently, in _build/), then one
+    shared library (every object carries its own device code)."""
+    objdir = os.path.join(ROOT, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    tag = f"{os.getpid()}"
+    objs, procs = [], []
+    for src in sources:
+        obj = os.path.join(objdir, os.path.basename(src) + f".{tag}.o")
+        cmd = [HIPCC, *[f for f in FLAGS if f != "-shared"], *extra, "-c", src, "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        procs.append((subprocess.Popen(cmd), cmd))
+        objs.append(obj)
+    failed = [cmd for p, cmd in procs if p.wait() != 0]
+    try:
+        if failed:
+            raise subprocess.CalledProcessError(1, failed[0])
+        tmp = lib + f".tmp{tag}"
+        subprocess.check_call([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp])
+        os.replace(tmp, lib)
+    finally:
+        for obj in objs:
+            if os.path.exists(obj):
+                os.remove(obj)
 
 
 def build(verbose: bool = True, extra=()) -> str:

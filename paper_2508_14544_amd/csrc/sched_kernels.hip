@@ -11,6 +11,26 @@ extern template __global__ void k_simulate_ladder_wide<SCHED_AMIN>(Params);
 extern template __global__ void k_simulate_ladder_wide<SCHED_HSF>(Params);
 extern template __global__ void k_simulate_ladder_wide<SCHED_AELL>(Params);
 extern template __global__ void k_simulate_ladder_wide<SCHED_ARANDOM>(Params);
+// defined in sched_group.hip
+extern template __global__ void k_simulate_group<SCHED_AMAX, 2, 8, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_AMAX, 4, 4, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_AMAX, 4, 16, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_AMAX, 8, 16, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_HSF, 2, 8, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_HSF, 4, 4, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_HSF, 4, 16, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_HSF, 8, 16, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_ARANDOM, 4, 16, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_ARANDOM, 8, 16, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_AELL, 4, 16, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_AELL, 8, 16, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_AMIN, 2, 8, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_AMIN, 2, 8, true>(Params);
+extern template __global__ void k_simulate_group<SCHED_AMIN, 4, 4, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_AMIN, 4, 4, true>(Params);
+extern template __global__ void k_simulate_group<SCHED_AMIN, 4, 16, false>(Params);
+extern template __global__ void k_simulate_group<SCHED_AMIN, 4, 16, true>(Params);
+extern template __global__ void k_simulate_group<SCHED_AMIN, 8, 16, true>(Params);
 }  // namespace sk
 
 // ---------------------------------------------------------------------------
@@ -49,7 +69,7 @@ hipError_t scratch_address(int dev, void** out) {
 
 // One launch of the simulation kernel over the batch.
 struct Tier {
-  int rows;         // register rows (fixed-row kernels)
+  int rows;         // register rows (fixed-row kernels; per wave in a workgroup)
   bool grow;        // a row ladder: k_simulate_ladder, or k_simulate_ladder_wide with wide
   bool wide;
   bool retry;       // a retry pass: runs the instances an earlier pass handed over (run_mask)
@@ -59,10 +79,37 @@ struct Tier {
   int rows_status;  // status for an outgrown running set
   int v_status;     // status for an outgrown cancelled set
   int stage;        // completion steps staged in LDS (1) or not (0)
+  int gw;           // > 1: a workgroup of gw waves per instance (k_simulate_group)
+  int grid;         // workgroups of the launch (0: one per instance)
 };
+
+// The workgroup kernels that exist (sched_group.hip), else NULL.
+template <int ALGO>
+const void* group_kernel(int w, int rows, bool vglobal) {
+  using P = sk::Params;
+  void (*f)(P) = nullptr;
+  if constexpr (ALGO == SCHED_AMAX || ALGO == SCHED_HSF) {
+    if (!vglobal) {
+      if (w == 2 && rows == 8) f = &sk::k_simulate_group<ALGO, 2, 8, false>;
+      if (w == 4 && rows == 4) f = &sk::k_simulate_group<ALGO, 4, 4, false>;
+    }
+  }
+  if constexpr (ALGO != SCHED_AMIN) {
+    if (!vglobal && w == 4 && rows == 16) f = &sk::k_simulate_group<ALGO, 4, 16, false>;
+    if (!vglobal && w == 8 && rows == 16) f = &sk::k_simulate_group<ALGO, 8, 16, false>;
+  } else {
+    if (w == 2 && rows == 8) f = vglobal ? &sk::k_simulate_group<ALGO, 2, 8, true> : &sk::k_simulate_group<ALGO, 2, 8, false>;
+    if (w == 4 && rows == 4) f = vglobal ? &sk::k_simulate_group<ALGO, 4, 4, true> : &sk::k_simulate_group<ALGO, 4, 4, false>;
+    if (w == 4 && rows == 16)
+      f = vglobal ? &sk::k_simulate_group<ALGO, 4, 16, true> : &sk::k_simulate_group<ALGO, 4, 16, false>;
+    if (w == 8 && rows == 16 && vglobal) f = &sk::k_simulate_group<ALGO, 8, 16, true>;
+  }
+  return reinterpret_cast<const void*>(f);
+}
 
 template <int ALGO>
 const void* sim_kernel(const Tier& tr) {
+  if (tr.gw > 1) return group_kernel<ALGO>(tr.gw, tr.rows, tr.vglobal);
   if (tr.grow)
     return tr.wide ? reinterpret_cast<const void*>(&sk::k_simulate_ladder_wide<ALGO>)
                    : reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO>);
@@ -100,20 +147,45 @@ int rows_for(int64_t want) {
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+// The LDS of a launch: the bitmaps' words and the most a workgroup holds.
+struct Room {
+  size_t lds_max;
+  int nw, nw1;
+};
+
+// LDS bytes of a workgroup launch (W waves, `rows` rows each) whose waves
+// each hold cap_v cancelled-set slots (0: a global set), staging aside.
+size_t group_lds(int algo, int w, int rows, const Room& rm, int cap_v) {
+  return 8 * (static_cast<size_t>(sk::group_pre_words(algo, w, rows)) +
+              static_cast<size_t>(w) * (static_cast<size_t>(rm.nw) + rm.nw1 + cap_v));
+}
+
+// Cancelled-set slots per wave that the LDS of such a launch leaves room for
+// (-1: not even the bitmaps fit).
+int64_t group_cap_fit(int algo, int w, int rows, const Room& rm) {
+  const size_t base = group_lds(algo, w, rows, rm, 0);
+  return base > rm.lds_max ? -1 : static_cast<int64_t>((rm.lds_max - base) / (8 * static_cast<size_t>(w)));
+}
+
 // The launches that simulate a batch under one policy.  The first holds an
 // instance's running set in register rows whose number follows it (the row
 // ladder: 2, 3, 5, 8, 10 rows, four waves a SIMD); an instance that needs more
 // than 640 runs is simulated again from step 0 by the wide ladder (12 and 16
 // more rows, 1024 runs, fewer waves a SIMD), which is also the first launch of a
-// batch of few instances that may need it.  The cancelled set (A_min, A_l)
+// batch of few instances that may need it; one that needs more than 1024 runs,
+// by a workgroup of 4 waves with 16 rows each (4096 runs), then of 8 waves
+// (8192).  With workgroup_waves = W (2 or 4), the first launch is a workgroup
+// of W waves with 1024 / (64 W) rows each instead.  The cancelled set (A_min)
 // first gets cap0 LDS slots (a size chosen for occupancy); an instance that
 // outgrows them is simulated again with as many slots as a workgroup's LDS
 // holds, and one that outgrows those again with a global-memory set of n
-// slots, which always suffices (at most n requests wait cancelled).  So
-// whether an instance completes never depends on the other instances of the
-// batch or on these sizes: only running sets above 1024 runs, or above a
-// caller's forced running capacity, are refused.
-int build_tiers(int algo, int64_t nmax, int64_t K, int forced_rows, int cap0, int cap_fit, Tier* out) {
+// slots (per wave), which always suffices (at most n requests wait
+// cancelled).  So whether an instance completes never depends on the other
+// instances of the batch or on these sizes: only running sets above 8192 runs
+// (4096 where eight waves' bitmaps do not fit the LDS), or above a caller's
+// forced running capacity, are refused.
+int build_tiers(int algo, int64_t nmax, int64_t K, int forced_rows, int cap0, int cap_fit, int ww, const Room& rm,
+                Tier* out) {
   // (A_l's queue lives in global memory and never overflows)
   const bool has_v = algo == SCHED_AMIN;
   const int64_t need_v = has_v ? std::max<int64_t>(nmax, 1) : 0;
@@ -121,22 +193,48 @@ int build_tiers(int algo, int64_t nmax, int64_t K, int forced_rows, int cap0, in
   const bool v_retry = has_v && cap0 < need_v && cap1 > cap0;  // a larger LDS set may help
   const bool v_lds_short = has_v && cap1 < need_v;              // even the largest LDS set may not
   int m = 0;
-  if (forced_rows > 0) {
-    out[m++] = Tier{forced_rows, false, false, false, false, cap0, 0, 0, 0, 0};
-    if (v_retry) out[m++] = Tier{16, false, false, true, false, cap1, 2, 0, 0, 0};
-    if (v_lds_short) out[m++] = Tier{16, false, false, true, true, 0, 2, 0, 0, 0};
+  // a workgroup launch: with an LDS cancelled set when `want` slots per wave
+  // fit (and a global-set retry if that may be short), else a global set
+  auto group = [&](int w, int rows, int mask) {
+    if (!has_v) {
+      out[m++] = Tier{rows, false, false, mask != 0, false, 0, mask, 0, 0, 0, w, 0};
+      return;
+    }
+    const int64_t want = std::min<int64_t>(need_v, 16384);
+    const int64_t fit = std::min<int64_t>(group_cap_fit(algo, w, rows, rm), cap_fit);
+    const bool lds = fit >= want && group_kernel<SCHED_AMIN>(w, rows, false) != nullptr;
+    if (lds) out[m++] = Tier{rows, false, false, mask != 0, false, static_cast<int>(want), mask, 0, 0, 0, w, 0};
+    if (!lds || want < need_v) out[m++] = Tier{rows, false, false, true, true, 0, lds ? 2 : (mask ? mask : 0), 0, 0, 0, w, 0};
+  };
+  if (ww > 1) {
+    group(ww, 1024 / (64 * ww), 0);
+  } else if (forced_rows > 0) {
+    out[m++] = Tier{forced_rows, false, false, false, false, cap0, 0, 0, 0, 0, 0, 0};
+    if (v_retry) out[m++] = Tier{16, false, false, true, false, cap1, 2, 0, 0, 0, 0, 0};
+    if (v_lds_short) out[m++] = Tier{16, false, false, true, true, 0, 2, 0, 0, 0, 0, 0};
   } else if (nmax <= 128) {
-    out[m++] = Tier{rows_for(std::max<int64_t>(nmax, 1)), false, false, false, false, cap0, 0, 0, 0, 0};
-    if (v_retry) out[m++] = Tier{8, false, false, true, false, cap1, 2, 0, 0, 0};
-    if (v_lds_short) out[m++] = Tier{16, false, false, true, true, 0, 2, 0, 0, 0};
+    out[m++] = Tier{rows_for(std::max<int64_t>(nmax, 1)), false, false, false, false, cap0, 0, 0, 0, 0, 0, 0};
+    if (v_retry) out[m++] = Tier{8, false, false, true, false, cap1, 2, 0, 0, 0, 0, 0};
+    if (v_lds_short) out[m++] = Tier{16, false, false, true, true, 0, 2, 0, 0, 0, 0, 0};
   } else {
     // few instances of many requests start on the wide ladder (they would
     // likely outgrow the narrow one, and the retry would simulate them again)
     const bool wide0 = nmax > 4096 && K <= 256;
-    out[m++] = Tier{0, true, wide0, false, false, cap0, 0, 0, 0, 0};
+    out[m++] = Tier{0, true, wide0, false, false, cap0, 0, 0, 0, 0, 0, 0};
     const int mask = (!wide0 && nmax > 640 ? 1 : 0) | (v_retry ? 2 : 0);
-    if (mask) out[m++] = Tier{0, true, true, true, false, cap1, mask, 0, 0, 0};
-    if (v_lds_short) out[m++] = Tier{16, false, false, true, true, 0, 2, 0, 0, 0};
+    if (mask) out[m++] = Tier{0, true, true, true, false, cap1, mask, 0, 0, 0, 0, 0};
+    if (v_lds_short) out[m++] = Tier{16, false, false, true, true, 0, 2, 0, 0, 0, 0, 0};
+  }
+  // beyond 1024 runs: workgroups (a forced capacity holds instead)
+  if (forced_rows == 0 && nmax > 1024) {
+    group(4, 16, 1);
+    // eight waves when their bitmaps (and lists) fit the LDS
+    if (group_cap_fit(algo, 8, 16, rm) >= 0) {
+      if (has_v)
+        out[m++] = Tier{16, false, false, true, true, 0, 1, 0, 0, 0, 8, 0};
+      else
+        out[m++] = Tier{16, false, false, true, false, 0, 1, 0, 0, 0, 8, 0};
+    }
   }
   // what a pass writes for an instance it cannot hold: a later pass that takes
   // it, or the final refusal
@@ -212,7 +310,7 @@ sk::Params base_params(const sched_instances_t* in, int64_t M) {
 
 extern "C" {
 
-int sched_version(void) { return 130; }
+int sched_version(void) { return 131; }
 
 const char* sched_strerror(int code) {
   switch (code) {
@@ -270,6 +368,10 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   if (o.step_cap > sk::kCapLimit) return SCHED_E_INVAL;
   if (o.running_capacity < 0 || o.evicted_capacity < 0 || o.evicted_lds_limit < 0) return SCHED_E_INVAL;
   if (o.running_capacity > 1024) return SCHED_E_UNSUPPORTED;
+  const int ww = o.workgroup_waves <= 1 ? 0 : o.workgroup_waves;
+  if (o.workgroup_waves < 0 || (ww != 0 && ww != 2 && ww != 4)) return SCHED_E_INVAL;
+  if (ww && (o.running_capacity > 0 || (algo != SCHED_AMAX && algo != SCHED_AMIN && algo != SCHED_HSF)))
+    return SCHED_E_INVAL;
 
   const int64_t nmax = in->max_requests;
   const bool tie = in->total_requests > 0 && in->tie_key != nullptr;
@@ -302,14 +404,37 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   // kernel skips the instances that k_prepare assigned to the other policy
   const int sim_algos[2] = {algo == SCHED_ADAPTIVE ? SCHED_AMIN : static_cast<int>(algo), SCHED_AELL};
   const int n_sim = algo == SCHED_ADAPTIVE ? 2 : 1;
-  Tier tiers[2][5];
+  const Room rm{static_cast<size_t>(lds_max), nw, nw1};
+  Tier tiers[2][8];
   int n_tiers[2] = {0, 0};
   bool any_global = algo == SCHED_AELL || algo == SCHED_ADAPTIVE;  // A_l's promoted queue
+  // workgroup launches with global cancelled sets: each workgroup simulates
+  // its instances one after the other, with n_max entries per wave of its own
+  // (at most 64 MiB of them, and at least one workgroup)
+  int64_t group_words = 0;
   for (int a = 0; a < n_sim; ++a) {
     n_tiers[a] = build_tiers(sim_algos[a], nmax, in->num_instances, forced_rows, cap0_for(sim_algos[a]), cap_fit,
-                             tiers[a]);
-    for (int p = 0; p < n_tiers[a]; ++p) any_global = any_global || tiers[a][p].vglobal;
+                             ww, rm, tiers[a]);
+    for (int p = 0; p < n_tiers[a]; ++p) {
+      Tier& t = tiers[a][p];
+      if (t.gw > 1 && t.vglobal) {
+        const int64_t per = static_cast<int64_t>(t.gw) * std::max<int64_t>(nmax, 1);
+        t.grid = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(in->num_instances, (int64_t(8) << 20) / per)));
+        group_words = std::max<int64_t>(group_words, per * t.grid);
+      } else {
+        any_global = any_global || t.vglobal;
+      }
+      if (t.gw > 1 && !sim_kernel_any(sim_algos[a], t)) return SCHED_E_UNSUPPORTED;
+    }
   }
+  // LDS of a launch before staging (every launch fits, by the choices above)
+  auto lds_base = [&](int a, const Tier& t) -> size_t {
+    if (t.gw > 1) return group_lds(sim_algos[a], t.gw, t.rows, rm, t.vglobal ? 0 : t.cap_v);
+    return lds_bitmaps + (t.vglobal ? 0 : 8 * static_cast<size_t>(t.cap_v));
+  };
+  for (int a = 0; a < n_sim; ++a)
+    for (int p = 0; p < n_tiers[a]; ++p)
+      if (lds_base(a, tiers[a][p]) > static_cast<size_t>(lds_max)) return SCHED_E_UNSUPPORTED;
 
   const size_t N = static_cast<size_t>(in->total_requests);
   const size_t K = static_cast<size_t>(in->num_instances);
@@ -325,6 +450,7 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   const size_t o_cs = off; off = align_up(off + (tie ? 4 * N : 0), 256);
   const size_t o_es = off; off = align_up(off + (tie && out->evictions ? 4 * N : 0), 256);
   const size_t o_vg = off; off = align_up(off + (any_global ? 8 * N : 0), 256);
+  const size_t o_gv = off; off = align_up(off + 8 * static_cast<size_t>(group_words), 256);
   // every workspace array is written before it is read (nothing needs clearing)
   void* ws = nullptr;
   if (no_alloc) {
@@ -357,6 +483,7 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   P.comp_st = tie ? reinterpret_cast<int32_t*>(base + o_cs) : nullptr;
   P.ev_st = tie && out->evictions ? reinterpret_cast<int32_t*>(base + o_es) : nullptr;
   P.vglob = any_global ? reinterpret_cast<uint64_t*>(base + o_vg) : nullptr;
+  P.vgroup = group_words ? reinterpret_cast<uint64_t*>(base + o_gv) : nullptr;
   P.nw_max = nw;
   P.nw1_max = nw1;
   P.run_cap = forced_rows > 0 ? forced_rows * 64 : INT32_MAX;
@@ -379,19 +506,19 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   const int64_t nst = static_cast<int64_t>(nw) * 64;
   const int64_t per_cu = std::min<int64_t>(16, std::max<int64_t>(1, (static_cast<int64_t>(K) + 255) / 256));
   const size_t stage_budget = std::min<size_t>(static_cast<size_t>(lds_max), static_cast<size_t>(163840 / per_cu));
-  auto lds_base = [&](const Tier& t) -> size_t { return lds_bitmaps + (t.vglobal ? 0 : 8 * static_cast<size_t>(t.cap_v)); };
   for (int a = 0; a < n_sim; ++a)
     for (int p = 0; p < n_tiers[a]; ++p) {
       Tier& t = tiers[a][p];
       t.stage = 0;
-      if (lds_base(t) + 4 * nst <= stage_budget) t.stage = 1;
+      // (a workgroup launch: when it fits at all; few instances run at once)
+      if (lds_base(a, t) + 4 * nst <= (t.gw > 1 ? static_cast<size_t>(lds_max) : stage_budget)) t.stage = 1;
     }
-  auto lds_of = [&](const Tier& t) -> size_t { return lds_base(t) + (t.stage ? 4 * nst : 0); };
+  auto lds_of = [&](int a, const Tier& t) -> size_t { return lds_base(a, t) + (t.stage ? 4 * nst : 0); };
   for (int a = 0; a < n_sim && err == hipSuccess; ++a)
     for (int p = 0; p < n_tiers[a] && err == hipSuccess; ++p)
-      if (lds_of(tiers[a][p]) > 65536)
+      if (lds_of(a, tiers[a][p]) > 65536)
         err = hipFuncSetAttribute(sim_kernel_any(sim_algos[a], tiers[a][p]),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds_of(tiers[a][p])));
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds_of(a, tiers[a][p])));
   if (err == hipSuccess && o.event_before) err = hipEventRecord(static_cast<hipEvent_t>(o.event_before), st);
   // adaptive: the A_l launches go to the side stream after the preparation,
   // and the caller's stream waits for them before the end (fork and join)
@@ -415,7 +542,8 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
       q.run_mask = t.run_mask;
       q.stage_comp = t.stage;
       void* args[] = {&q};
-      err = hipLaunchKernel(sim_kernel_any(sim_algos[a], t), grid, block, args, lds_of(t), sa);
+      const dim3 tgrid(t.grid > 0 ? t.grid : P.K), tblock(64 * (t.gw > 1 ? t.gw : 1));
+      err = hipLaunchKernel(sim_kernel_any(sim_algos[a], t), tgrid, tblock, args, lds_of(a, t), sa);
     }
   }
   if (side) {

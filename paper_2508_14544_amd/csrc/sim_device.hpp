@@ -118,6 +118,9 @@ struct Params {
   // completion steps staged in LDS after the cancelled set (n_max slots) and
   // written out coalesced at the end of an instance
   int32_t stage_comp;
+  // workgroup passes with global cancelled sets: n_max entries per wave of
+  // each workgroup of the launch
+  uint64_t* vgroup;
 };
 
 // Internal statuses of an instance handed to a later pass: its running set
@@ -493,6 +496,64 @@ __device__ __forceinline__ void fresh_state(ST& st) {
   st.vw_lo = 0; st.vw_hi = 0; st.vw_base = -(1 << 30);
 }
 
+// ---------------------------------------------------------------------------
+// A workgroup of W > 1 waves simulating one instance.  Every wave holds its
+// own ROWS register rows of the running set (W x 64 x ROWS slots) and its own
+// copy of the rest of the state (the bitmaps and the cancelled set in an LDS
+// block of its own, the scalars, the register row of recent cancellations),
+// which it updates exactly as the other waves do.  What depends on the whole
+// running set is agreed at exchanges: each wave writes its partial results
+// (a wave reduction over its rows), a barrier, and lane j < W of every wave
+// reads wave j's partials, which one fold inside a 16-lane row combines.  A
+// branch around an exchange depends only on state that every wave holds
+// alike, so every wave reaches the same exchanges in the same order.  A new
+// run goes to the wave that holds the fewest (counts kept alike in every
+// wave: lane j holds wave j's).
+// ---------------------------------------------------------------------------
+// 64-bit LDS words before the waves' blocks: two alternating exchange buffers
+// of W x 8 32-bit words, and for the policies whose runs may complete before
+// their planned end (A_max, A_l) a list of each wave's completions at a step
+// (W x 64 x ROWS entries).
+__host__ __device__ constexpr int group_pre_words(int algo, int w, int rows) {
+  return 8 * w + ((algo == SCHED_AMAX || algo == SCHED_AELL) ? w * 64 * rows : 0);
+}
+
+// A workgroup barrier that orders LDS accesses only (pending global stores
+// are not waited for).
+__device__ __forceinline__ void group_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// One exchange of four 32-bit words per wave (two with `b`): lane j < W gets
+// wave j's words; lanes >= W get their own wave's.  The two buffers alternate,
+// so a wave can be at most one exchange ahead of another while it writes.
+template <int W>
+__device__ __forceinline__ uint4 group_exchange(uint4* red, int& par, int wv, int lane, uint4 a, uint4* b = nullptr) {
+  uint4* buf = red + par * 2 * W;
+  if (lane == 0) {
+    buf[wv] = a;
+    if (b) buf[W + wv] = *b;
+  }
+  group_barrier();
+  par ^= 1;
+  const int j = lane < W ? lane : wv;
+  if (b) *b = buf[W + j];
+  return buf[j];
+}
+
+// Folds over the lanes of the first 16-lane row (lanes >= W hold neutral values).
+__device__ __forceinline__ uint32_t lanes_min_u32(uint32_t v) {
+  return uniform_u32(wave::fold_in_row(v, wave::OpMinU32{}));
+}
+__device__ __forceinline__ int32_t lanes_max_i32(int32_t v) {
+  return wave::uniform(static_cast<int32_t>(wave::fold_in_row(static_cast<uint32_t>(v), wave::OpMaxI32{})));
+}
+__device__ __forceinline__ int32_t lanes_sum_i32(int32_t v) {
+  return wave::uniform(static_cast<int32_t>(wave::fold_in_row(static_cast<uint32_t>(v), wave::OpAddU32{})));
+}
+
 // Simulates instance k (whose validation status is st0) with ROWS register
 // rows and writes its outputs.  A running set that outgrows the rows ends the
 // simulation with `retry_status` (the per-request outputs are then reset), or,
@@ -500,19 +561,22 @@ __device__ __forceinline__ void fresh_state(ST& st) {
 // FROM_STATE the body continues from *st instead of starting at step 0.  A
 // cancelled set that outgrows its P.cap_v LDS slots ends it with
 // P.retry_v_status; with VGLOBAL the set lives in global memory (n slots, the
-// most it can hold).  CAPPED holds the running set to P.run_cap runs.
+// most it can hold).  CAPPED holds the running set to P.run_cap runs.  W > 1:
+// a workgroup of W waves simulates the instance (see group_exchange).
 template <int ALGO, int ROWS, bool FROM_STATE = false, bool TO_STATE = false, bool VGLOBAL = false,
-          bool CAPPED = false, typename ST = SimState>
+          bool CAPPED = false, typename ST = SimState, int W = 1>
 __device__ __forceinline__ int sim_instance(const Params& P, const int k, const int st0, const int retry_status,
                                            ST* st = nullptr) {
   constexpr int kStateRows = ST::kRows;
   static_assert(!(FROM_STATE || TO_STATE) || ROWS <= kStateRows, "state holds at most kStateRows rows");
+  static_assert(W == 1 || (W <= 16 && !FROM_STATE && !TO_STATE && !CAPPED), "a workgroup runs fixed rows");
   // only A_min and A_l have cancelled (or promoted) requests waiting: for the
   // other policies every head is fresh, and the code of the cancelled set is
   // left out of their kernels
   constexpr bool kHasV = ALGO == SCHED_AMIN || ALGO == SCHED_AELL;
   extern __shared__ uint64_t lds64[];
-  const int lane = threadIdx.x;
+  const int lane = W > 1 ? static_cast<int>(threadIdx.x & 63u) : static_cast<int>(threadIdx.x);
+  const int wv = W > 1 ? wave::uniform(static_cast<int32_t>(threadIdx.x >> 6)) : 0;
   const int64_t b = P.offsets[k];
   // a body that hands its state over only ever runs valid, non-empty instances
   const int n = (TO_STATE || st0 == SCHED_OK) ? static_cast<int>(P.offsets[k + 1] - b) : 0;
@@ -525,19 +589,30 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
   int64_t tot_ev = wave::in_vgpr<int64_t>(FROM_STATE ? st->tot_ev : 0);
 
   if (TO_STATE || (st0 == SCHED_OK && n > 0)) {
-    uint64_t* L0 = lds64;
-    uint64_t* L1 = lds64 + P.nw_max;
+    // W > 1: each wave's block (bitmaps, cancelled set) follows the exchange
+    // area, and the staged completion steps (one array for the workgroup)
+    // follow the blocks; a global cancelled set has n entries per wave
+    const int gstride = P.nw_max + P.nw1_max + (VGLOBAL ? 0 : P.cap_v);
+    uint64_t* const lw = W > 1 ? lds64 + group_pre_words(ALGO, W, ROWS) + wv * gstride : lds64;
+    uint64_t* L0 = lw;
+    uint64_t* L1 = lw + P.nw_max;
     // cancelled requests, one 64-bit entry each.  A_min: key | (s | o << 16) << 32,
     // slots [0, nVe) may start now, [nVe, nV) were cancelled at this step.
     // A_l: a FIFO ring of id | s << 17 | o << 33 | u << 48 from slot v_head.
-    uint64_t* vent = VGLOBAL ? P.vglob + b : L1 + P.nw1_max;
+    // (W > 1, global: each wave of workgroup g has the n_max entries at
+    // P.vgroup + (g W + wave) n_max; the workgroup simulates its instances
+    // one after the other)
+    uint64_t* vent = VGLOBAL ? (W > 1 ? P.vgroup + (static_cast<int64_t>(blockIdx.x) * W + wv) * P.max_requests
+                                      : P.vglob + b)
+                             : L1 + P.nw1_max;
     // A_l: every request is promoted at most once, so its queue is an
     // append-only array of n entries in global memory (the instance's slice
     // of the workspace), read through a 64-entry register window
     constexpr bool kQueue = ALGO == SCHED_AELL;
     g_u64* qg = kQueue ? (g_u64*)(P.vglob + b) : nullptr;
     const int32_t cap_v = (VGLOBAL || kQueue) ? n : P.cap_v;
-    int32_t* lcomp = reinterpret_cast<int32_t*>(L1 + P.nw1_max + (VGLOBAL ? 0 : P.cap_v));
+    int32_t* lcomp = W > 1 ? reinterpret_cast<int32_t*>(lds64 + group_pre_words(ALGO, W, ROWS) + W * gstride)
+                           : reinterpret_cast<int32_t*>(L1 + P.nw1_max + (VGLOBAL ? 0 : P.cap_v));
     const bool stage_c = P.stage_comp != 0;
     const int nw = (n + 63) >> 6;
     const int nw1 = (nw + 63) >> 6;
@@ -545,9 +620,14 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       for (int w = lane; w < nw; w += 64) L0[w] = 0;
       for (int w = lane; w < nw1; w += 64) L1[w] = 0;
       if (stage_c)
-        for (int i = lane; i < n; i += 64) lcomp[i] = -1;
+        for (int i = W > 1 ? static_cast<int>(threadIdx.x) : lane; i < n; i += 64 * W) lcomp[i] = -1;
       __syncthreads();
     }
+    // W > 1: the exchange buffers, the completion lists, the run counts
+    uint4* const gred = reinterpret_cast<uint4*>(lds64);
+    uint64_t* const glist = lds64 + 8 * W + wv * 64 * ROWS;
+    int gpar = 0;
+    int32_t occ = 0;
 
     const int32_t cap = P.cap[k];
     // array bases in vector registers
@@ -566,7 +646,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     // instance), else straight to the global outputs.  One generic pointer,
     // so the staged case costs no registers (its stores are flat stores to
     // LDS; the global case's are flat stores too, which measured the same)
-    int32_t* cdst = base(P.stage_comp ? reinterpret_cast<int32_t*>(lds64 + P.nw_max + P.nw1_max + (VGLOBAL ? 0 : P.cap_v))
+    int32_t* cdst = base(P.stage_comp ? (W > 1 ? lcomp : reinterpret_cast<int32_t*>(lds64 + P.nw_max + P.nw1_max + (VGLOBAL ? 0 : P.cap_v)))
                                       : (P.tie_key ? P.comp_st : P.completion) + b);
     g_i32* evictions = P.evictions ? base((g_i32*)((P.tie_key ? P.ev_st : P.evictions) + b)) : nullptr;
 
@@ -975,13 +1055,25 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
       if (t >= next_c) {
         int32_t sx = 0;
         int ndone = 0;
+        int lc = 0;                    // W > 1: this wave's completions listed
+        uint32_t gcmin = 0xFFFFFFFFu;  // W > 1: the next event, agreed
 #pragma unroll
         for (int r = 0; r < ROWS; ++r) {
           const bool hit = r_c[r] == t;
           const uint64_t m = wave::ballot(hit);
           if (m) {
             ndone += __builtin_popcountll(m);
-            if (ALGO == SCHED_AMAX || ALGO == SCHED_AELL) {
+            if constexpr (W > 1 && (ALGO == SCHED_AMAX || ALGO == SCHED_AELL)) {
+              // every wave drops the shares of every wave's completions: list them
+              if (hit) {
+                const int pos = lc + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                                         static_cast<uint32_t>(m >> 32),
+                                         __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0u)));
+                glist[pos] = static_cast<uint64_t>(static_cast<uint32_t>(r_x[r])) |
+                             (static_cast<uint64_t>(static_cast<uint32_t>(r_end[r])) << 32);
+              }
+              lc += __builtin_popcountll(m);
+            } else if (ALGO == SCHED_AMAX || ALGO == SCHED_AELL) {
               // planned with u >= o: the run may end before its planned end
               uint64_t mm = m;
               while (mm) {
@@ -998,7 +1090,52 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
             if (r == fr_row) fr_mask |= m;
           }
         }
-        if (ndone) {
+        if constexpr (W > 1) {
+          // agree on the completions (and, but for A_l, the next one)
+          uint32_t cl = 0xFFFFFFFFu;
+          if constexpr (ALGO != SCHED_AELL) {
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+              const uint32_t ev = static_cast<uint32_t>(r_c[r]);
+              cl = ev < cl ? ev : cl;
+            }
+            cl = wave::min_u32(cl);
+          }
+          const uint4 g = group_exchange<W>(gred, gpar, wv, lane,
+                                            make_uint4(static_cast<uint32_t>(ndone), static_cast<uint32_t>(wave::sum_i32(sx)),
+                                                       cl, static_cast<uint32_t>(lc)));
+          const int32_t nd_j = lane < W ? static_cast<int32_t>(g.x) : 0;
+          occ -= nd_j;
+          const int32_t nd = lanes_sum_i32(nd_j);
+          const int32_t sxw = lanes_sum_i32(lane < W ? static_cast<int32_t>(g.y) : 0);
+          gcmin = lanes_min_u32(lane < W ? g.z : 0xFFFFFFFFu);
+          if constexpr (ALGO == SCHED_AMAX || ALGO == SCHED_AELL) {
+            if (lanes_sum_i32(lane < W ? static_cast<int32_t>(g.w) : 0) > 0) {
+              for (int j = 0; j < W; ++j) {
+                const int cj = wave::readlane(static_cast<int32_t>(g.w), j);
+                const uint64_t* lj = lds64 + 8 * W + j * 64 * ROWS;
+                for (int e0 = 0; e0 < cj; e0 += 64) {
+                  const uint64_t ev = e0 + lane < cj ? lj[e0 + lane] : 0ull;
+                  const int ne = cj - e0 < 64 ? cj - e0 : 64;
+                  for (int q = 0; q < ne; ++q) {
+                    const int32_t xq = wave::readlane(static_cast<int32_t>(static_cast<uint32_t>(ev)), q);
+                    const int32_t eq = wave::readlane(static_cast<int32_t>(ev >> 32), q);
+                    SK_DROP_SHARE(t, xq, eq);
+                  }
+                }
+              }
+              group_barrier();  // every wave has read the lists: they may be written again
+            }
+          }
+          if (nd) {
+            event = true;
+            X -= sxw;
+            N -= nd;
+            DT = sxw + nd * (t - t_r);
+            n_done += nd;
+            SK_SET_PRIORITY();
+          }
+        } else if (ndone) {
           event = true;
           const int32_t sxw = wave::sum_i32(sx);
           X -= sxw;
@@ -1014,6 +1151,89 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
         // the queue, lowest index first among this step's promotions
         if (ALGO == SCHED_AELL) {
           bool promoted = false;
+          if constexpr (W > 1) {
+          for (;;) {
+            uint32_t best = 0xFFFFFFFFu;
+            int32_t brow = 0;
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+              const uint32_t kk = r_end[r] == t ? (r_key[r] & kIdxMask) : 0xFFFFFFFFu;
+              const bool lt = kk < best;
+              best = lt ? kk : best;
+              brow = lt ? r : brow;
+            }
+            const uint32_t iv = wave::min_u32_all(best);
+            const uint64_t at = wave::ballot(best == iv);
+            // the smallest index over the waves; its wave removes the run (the
+            // exchange that finds nothing left to promote also agrees on the
+            // next event)
+            const uint32_t il = wave::uniform_u(iv);
+            int ln = 0, rr = 0;
+            int32_t xk = 0, ck = 0, uk = 0;
+            uint32_t kk = 0;
+            if (il != 0xFFFFFFFFu) {
+              ln = __builtin_ctzll(at);
+              rr = wave::readlane(brow, ln);
+              SK_AT_ROW(rr, xk = wave::readlane(r_x[r], ln); ck = wave::readlane(r_c[r], ln);
+                        uk = wave::readlane(r_u[r], ln); kk = wave::readlane_u(r_key[r], ln);)
+            }
+            uint32_t cl = 0xFFFFFFFFu;
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+              const uint32_t ev = static_cast<uint32_t>(r_c[r]), pe = static_cast<uint32_t>(r_end[r]);
+              cl = ev < cl ? ev : cl;
+              cl = pe < cl ? pe : cl;
+            }
+            uint4 g2 = make_uint4(kk, wave::min_u32(cl), 0u, 0u);
+            const uint4 g = group_exchange<W>(gred, gpar, wv, lane,
+                                              make_uint4(il, static_cast<uint32_t>(xk), static_cast<uint32_t>(ck),
+                                                         static_cast<uint32_t>(uk)), &g2);
+            const uint32_t gi = lane < W ? g.x : 0xFFFFFFFFu;
+            const uint32_t imin = lanes_min_u32(gi);
+            if (imin == 0xFFFFFFFFu) {
+              gcmin = lanes_min_u32(lane < W ? g2.y : 0xFFFFFFFFu);
+              break;
+            }
+            if (nV >= cap_v) {
+              status = P.retry_v_status;
+              break;
+            }
+            const int win = __builtin_ctzll(wave::ballot(gi == imin));
+            xk = wave::readlane(static_cast<int32_t>(g.y), win);
+            ck = wave::readlane(static_cast<int32_t>(g.z), win);
+            uk = wave::readlane(static_cast<int32_t>(g.w), win);
+            kk = wave::readlane_u(g2.x, win);
+            if (wv == win) {
+              SK_AT_ROW(rr, r_end[r] = wave::writelane(r_end[r], kEmpty, ln);
+                        r_c[r] = wave::writelane(r_c[r], kNever, ln);
+                        r_key[r] = wave::writelane_u(r_key[r], 0xFFFFFFFFu, ln);)
+              if (rr == fr_row) fr_mask |= 1ull << ln;
+            }
+            occ -= lane == win ? 1 : 0;
+            X -= xk;
+            N -= 1;
+            const int32_t pk = t - static_cast<int32_t>(kk >> kIdxBits);
+            const uint64_t sk = static_cast<uint32_t>(xk - t_r + pk);
+            const uint64_t okk = static_cast<uint32_t>(ck - pk);
+            {
+              // every wave appends the same entry; one counts the promotion
+              const int slot = v_head + nV;
+              const uint64_t qe = imin | (sk << 17) | (okk << 33) | (static_cast<uint64_t>(uk) << 48);
+              if (lane == 0) {
+                qg[slot] = qe;
+                if (evictions && wv == 0)
+                  __hip_atomic_fetch_add(&evictions[imin], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              }
+              if (slot >= vw_base && slot - vw_base < 64) {
+                vw_lo = wave::writelane_u(vw_lo, static_cast<uint32_t>(qe), slot - vw_base);
+                vw_hi = wave::writelane_u(vw_hi, static_cast<uint32_t>(qe >> 32), slot - vw_base);
+              }
+            }
+            ++nV;
+            ++tot_ev;
+            promoted = true;
+          }
+          } else {
           for (;;) {
             uint32_t best = 0xFFFFFFFFu;
             int32_t brow = 0;
@@ -1064,6 +1284,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
             ++tot_ev;
             promoted = true;
           }
+          }
           if (status != SCHED_OK) break;
           if (promoted) {
             event = true;
@@ -1072,6 +1293,9 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
         }
         // next event: a completion (A_l: or a planned end, where a run is promoted);
         // empty slots read as unsigned are above every step
+        if constexpr (W > 1) {
+          next_c = static_cast<int32_t>(gcmin);
+        } else {
         uint32_t cmin = 0xFFFFFFFFu;
 #pragma unroll
         for (int r = 0; r < ROWS; ++r) {
@@ -1083,6 +1307,7 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
           cmin = ev < cmin ? ev : cmin;
         }
         next_c = static_cast<int32_t>(wave::min_u32(cmin));  // kNever when nothing runs
+        }
       }
 
       // ---- 4. A_min: cancel in ascending (o~, index) while memory at t+1 > M
@@ -1100,7 +1325,44 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
             }
             const uint32_t kv = wave::min_u32_all(best);
             const uint64_t at = wave::ballot(best == kv);
-            const uint32_t kmin = wave::uniform_u(kv);
+            uint32_t kmin = 0xFFFFFFFFu;
+            int32_t ek = 0, xk = 0, ck = 0;
+            if constexpr (W > 1) {
+              // the smallest key over the waves; its wave removes the run
+              const uint32_t kl = wave::uniform_u(kv);
+              int ln = 0, rr = 0;
+              if (kl != 0xFFFFFFFFu) {
+                ln = __builtin_ctzll(at);
+                rr = wave::readlane(brow, ln);
+                SK_AT_ROW(rr, ek = wave::readlane(r_end[r], ln); xk = wave::readlane(r_x[r], ln);
+                          ck = wave::readlane(r_c[r], ln);)
+              }
+              const uint4 g = group_exchange<W>(gred, gpar, wv, lane,
+                                                make_uint4(kl, static_cast<uint32_t>(ek), static_cast<uint32_t>(xk),
+                                                           static_cast<uint32_t>(ck)));
+              const uint32_t gk = lane < W ? g.x : 0xFFFFFFFFu;
+              kmin = lanes_min_u32(gk);
+              if (kmin == 0xFFFFFFFFu) {  // no run: impossible while P > M > 0
+                status = SCHED_E_UNSUPPORTED;
+                break;
+              }
+              if (u_used == ~0ull && nV >= cap_v) {
+                status = P.retry_v_status;
+                break;
+              }
+              const int win = __builtin_ctzll(wave::ballot(gk == kmin));
+              ek = wave::readlane(static_cast<int32_t>(g.y), win);
+              xk = wave::readlane(static_cast<int32_t>(g.z), win);
+              ck = wave::readlane(static_cast<int32_t>(g.w), win);
+              if (wv == win) {
+                SK_AT_ROW(rr, r_end[r] = wave::writelane(r_end[r], kEmpty, ln);
+                          r_c[r] = wave::writelane(r_c[r], kNever, ln);
+                          r_key[r] = wave::writelane_u(r_key[r], 0xFFFFFFFFu, ln);)
+                if (rr == fr_row) fr_mask |= 1ull << ln;
+              }
+              occ -= lane == win ? 1 : 0;
+            } else {
+            kmin = wave::uniform_u(kv);
             if (kmin == 0xFFFFFFFFu) {  // no run: impossible while P > M > 0
               status = SCHED_E_UNSUPPORTED;
               break;
@@ -1111,12 +1373,12 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
             }
             const int ln = __builtin_ctzll(at);
             const int rr = wave::readlane(brow, ln);
-            int32_t ek = 0, xk = 0, ck = 0;
             SK_AT_ROW(rr, ek = wave::readlane(r_end[r], ln); xk = wave::readlane(r_x[r], ln);
                       ck = wave::readlane(r_c[r], ln); r_end[r] = wave::writelane(r_end[r], kEmpty, ln);
                       r_c[r] = wave::writelane(r_c[r], kNever, ln);
                       r_key[r] = wave::writelane_u(r_key[r], 0xFFFFFFFFu, ln);)
             if (rr == fr_row) fr_mask |= 1ull << ln;
+            }
             SK_DROP_SHARE(t, xk, ek);
             X -= xk;
             N -= 1;
@@ -1137,12 +1399,13 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
               u_so = wave::writelane_u(u_so, so, ul);
               u_gate = wave::writelane_u(u_gate, 0xFFFFFFFFu, ul);
               u_used |= 1ull << ul;
-              if (lane == 0 && evictions)
+              if (lane == 0 && wv == 0 && evictions)
                 __hip_atomic_fetch_add(&evictions[idx], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             } else {
               if (lane == 0) {
                 vent[nV] = (static_cast<uint64_t>(so) << 32) | nkey;
-                if (evictions) __hip_atomic_fetch_add(&evictions[idx], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (evictions && wv == 0)
+                  __hip_atomic_fetch_add(&evictions[idx], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
               }
               ++nV;
             }
@@ -1245,6 +1508,37 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
           hmx = hv > hmx ? hv : hmx;
           fl += e >= E ? r_x[r] + cE : 0;
         }
+        if constexpr (W > 1) {
+          // one exchange agrees on both conditions and on the step to retry at
+          // (both ways of failing are prepared, see below)
+          int32_t fix = 0, emin = kNever;
+#pragma unroll
+          for (int r = 0; r < ROWS; ++r) {
+            const int32_t a = r_h[r] - lim, bb = r_end[r] - 1 - t;
+            const int32_t m = a < bb ? a : bb;
+            const bool in = static_cast<uint32_t>(r_end[r]) - lo2 <= span;
+            fix = (in && r_h[r] > lim && m > fix) ? m : fix;
+            const int32_t e = r_end[r];
+            emin = (e >= E && e < emin) ? e : emin;
+          }
+          const uint4 g = group_exchange<W>(
+              gred, gpar, wv, lane,
+              make_uint4(static_cast<uint32_t>(wave::max_i32(hmx)), static_cast<uint32_t>(wave::sum_i32(fl)),
+                         static_cast<uint32_t>(wave::max_i32(fix)), wave::min_u32(static_cast<uint32_t>(emin))));
+          const int32_t hg = lanes_max_i32(lane < W ? static_cast<int32_t>(g.x) : INT32_MIN);
+          const int32_t fg = lanes_sum_i32(lane < W ? static_cast<int32_t>(g.y) : 0);
+          if (hg > lim || (win && fg + s + est > M)) {
+            if (hg > lim)
+              retry_at = t + lanes_max_i32(lane < W ? static_cast<int32_t>(g.z) : 0);
+            else
+              retry_at = static_cast<int32_t>(lanes_min_u32(lane < W ? g.w : 0xFFFFFFFFu)) - est + 1;
+            wait_until = retry_at;
+            break;
+          }
+          // passed: the test below (one wave's) then passes with f = fg
+          fl = lane == 0 ? fg : 0;
+          hmx = INT32_MIN;
+        }
         // both conditions in one ballot: the sum is left in every lane, so the
         // passing case costs a single vector-to-scalar hand-off
         const int32_t fv = wave::sum_i32_all(fl);
@@ -1281,7 +1575,31 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
           status = retry_status;
           break;
         }
-        if (fr_mask == 0ull) {
+        int owner = 0;  // W > 1: the wave that takes the run
+        if constexpr (W > 1) {
+          // the wave with the fewest runs (the lowest such); all full: outgrown
+          const uint32_t oc = lane < W ? (static_cast<uint32_t>(occ) << 4) | static_cast<uint32_t>(lane) : 0xFFFFFFFFu;
+          const uint32_t om = lanes_min_u32(oc);
+          if (static_cast<int>(om >> 4) >= 64 * ROWS) {
+            status = retry_status;
+            break;
+          }
+          owner = static_cast<int>(om & 15u);
+          occ += lane == owner ? 1 : 0;
+          if (wv == owner && fr_mask == 0ull) {
+            // it has a free slot (its count is below its rows' slots)
+            int rr = 0;
+            uint64_t mm = 0ull;
+#pragma unroll
+            for (int r = ROWS - 1; r >= 0; --r) {
+              const uint64_t m = wave::ballot(r_end[r] == kEmpty);
+              rr = m ? r : rr;
+              mm = m ? m : mm;
+            }
+            fr_row = rr;
+            fr_mask = mm;
+          }
+        } else if (fr_mask == 0ull) {
           int rr = -1;
           uint64_t mm = 0ull;
 #pragma unroll
@@ -1314,15 +1632,17 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
           }
         }
         {
+          const int32_t cw = t + c_o;
+          if (W == 1 || wv == owner) {
           const int ln = __builtin_ctzll(fr_mask);
           fr_mask &= fr_mask - 1;
-          const int32_t cw = t + c_o;
           const uint32_t kw = c_key;
           const int32_t uw = c_u;
           SK_AT_ROW(fr_row, r_end[r] = wave::writelane(r_end[r], E, ln); r_x[r] = wave::writelane(r_x[r], xw, ln);
                     r_c[r] = wave::writelane(r_c[r], cw, ln); r_key[r] = wave::writelane_u(r_key[r], kw, ln);
                     r_h[r] = wave::writelane(r_h[r], hw, ln);
                     if (ALGO == SCHED_AELL) r_u[r] = wave::writelane(r_u[r], uw, ln);)
+          }
           const int32_t ew = ALGO == SCHED_AELL && E < cw ? E : cw;  // A_l: promotion at E
           next_c = ew < next_c ? ew : next_c;
         }
@@ -1405,9 +1725,12 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
   const bool st_c = P.stage_comp != 0;
   int64_t tel = 0, mk = 0;
   if (keep) {
-    const int32_t* lc = reinterpret_cast<const int32_t*>(lds64 + P.nw_max + P.nw1_max + (VGLOBAL ? 0 : P.cap_v));
-    for (int c = 0; c < n; c += 64) {
-      const int i = c + lane;
+    const int32_t* lc =
+        W > 1 ? reinterpret_cast<const int32_t*>(lds64 + group_pre_words(ALGO, W, ROWS) +
+                                                 W * (P.nw_max + P.nw1_max + (VGLOBAL ? 0 : P.cap_v)))
+              : reinterpret_cast<const int32_t*>(lds64 + P.nw_max + P.nw1_max + (VGLOBAL ? 0 : P.cap_v));
+    for (int c = 0; c < n; c += 64 * W) {
+      const int i = c + (W > 1 ? static_cast<int>(threadIdx.x) : lane);
       if (i < n) {
         const int32_t id = tie ? P.tr_of[b + i] : i;
         int32_t ci;
@@ -1429,8 +1752,8 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     // it to a retry pass, which starts from these values)
     int32_t* comp = tie ? P.comp_st : P.completion;
     int32_t* evs = tie ? P.ev_st : P.evictions;
-    for (int c = 0; c < n; c += 64) {
-      const int i = c + lane;
+    for (int c = 0; c < n; c += 64 * W) {
+      const int i = c + (W > 1 ? static_cast<int>(threadIdx.x) : lane);
       if (i < n) {
         comp[b + i] = -1;
         if (P.evictions) evs[b + i] = 0;
@@ -1439,11 +1762,27 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
   }
   tel = wave::sum_i64(tel);
   mk = wave::max_i64(mk);
+  if constexpr (W > 1) {
+    // over the waves (the exchange area is free: every wave is past the
+    // barrier above, so past its last exchange)
+    int64_t* gt = reinterpret_cast<int64_t*>(lds64);
+    if (lane == 0) {
+      gt[2 * wv] = tel;
+      gt[2 * wv + 1] = mk;
+    }
+    __syncthreads();
+    tel = 0;
+    mk = 0;
+    for (int j = 0; j < W; ++j) {
+      tel += gt[2 * j];
+      mk = gt[2 * j + 1] > mk ? gt[2 * j + 1] : mk;
+    }
+  }
   if (!keep) {
     rsteps = 0;
     tot_ev = 0;
   }
-  if (lane == 0) {
+  if (W > 1 ? threadIdx.x == 0 : lane == 0) {
     P.total_latency[k] = tel;
     if (P.makespan) P.makespan[k] = static_cast<int32_t>(mk);
     if (P.request_steps) P.request_steps[k] = rsteps;
@@ -1596,6 +1935,27 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
 template <int ALGO>
 __global__ __launch_bounds__(64) void k_simulate_ladder_wide(Params P) {
   ladder_instance<ALGO, true>(P, blockIdx.x);
+}
+// A workgroup of W waves per instance, ROWS register rows each (W x 64 x ROWS
+// runs): for few large instances, and for the instances whose running set
+// outgrows one wave's rows (a retry pass).  With P.run_mask set, only the
+// instances an earlier pass handed over run.
+// Workgroup g simulates instances g, g + grid, ... (a launch with global
+// cancelled sets has fewer workgroups than instances: each workgroup's sets
+// are its own).
+template <int ALGO, int W, int ROWS, bool VGLOBAL>
+__global__ __launch_bounds__(64 * W) void k_simulate_group(Params P) {
+  for (int k = blockIdx.x; k < P.K; k += gridDim.x) {
+    if (P.algo_of && P.algo_of[k] != ALGO) continue;
+    int st0 = P.status[k];
+    if (P.run_mask) {
+      const bool take = (st0 == kRetryRows && (P.run_mask & 1)) || (st0 == kRetryV && (P.run_mask & 2));
+      if (!take) continue;
+      st0 = SCHED_OK;
+    }
+    sim_instance<ALGO, ROWS, false, false, VGLOBAL, false, SimState, W>(P, k, st0, P.retry_status);
+    __syncthreads();  // the next instance reuses the LDS
+  }
 }
 #undef SK_SET_PRIORITY
 #undef SK_SAVE_STATE

@@ -47,7 +47,7 @@ def test_probe_library_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strerror(lib):
-    assert lib.sched_version() == 130
+    assert lib.sched_version() == 131
     for code in (0, -1, -2, -3, -4, -5, -6, -7, -8):
         assert B.strerror(code) and B.strerror(code) != "unknown code"
     assert B.strerror(12345) == "unknown code"

@@ -89,3 +89,23 @@ def test_every_instance_matches_oracle(B, workload, algo):
     if bad:
         pytest.fail(f"{len(bad)} of {len(got)} blocks differ; first: {_first_difference(batch, g, algo, bad[0])}")
     _say(f"[digest] {workload} {algo}: {batch.num_instances} instances bit-exact")
+
+
+# the large single instance simulated by a workgroup of 2 or 4 waves from the
+# start (the running set split over the waves): the same bits as one wave's
+WG_CASES = [(w, a, ww) for (w, a) in CASES if w == "single_n100000_m1048576" and a in ("amax", "amin", "hsf")
+            for ww in (2, 4)]
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("workload,algo,ww", WG_CASES, ids=[f"{w}-{a}-w{ww}" for w, a, ww in WG_CASES])
+def test_workgroup_matches_oracle(B, workload, algo, ww):
+    entry = DIG["workloads"][workload]
+    d = entry["algos"][algo]
+    batch, inputs_sha = _batch(workload, entry["with_upper"])
+    assert inputs_sha == d["inputs_sha"]
+    g = gpu_run(B, batch, O.ALGOS[algo], pass_upper=entry["with_upper"], workgroup_waves=ww)
+    assert (g["status"] == 0).all()
+    assert D.totals(g) == d["totals"]
+    assert D.block_digests(batch.offsets, g) == d["blocks"]
+    _say(f"[digest] {workload} {algo} workgroup of {ww}: bit-exact")

@@ -44,7 +44,7 @@ def test_library_host_checks_under_asan_ubsan(tmp_path):
     # the three translation units compile concurrently (device code unoptimised:
     # nothing here launches a kernel)
     objs, procs = [], []
-    for src in ("sched_kernels.hip", "sched_wide.hip", "opt_kernels.hip"):
+    for src in ("sched_kernels.hip", "sched_wide.hip", "sched_group.hip", "opt_kernels.hip"):
         obj = str(tmp_path / (src + ".o"))
         objs.append(obj)
         procs.append(subprocess.Popen([hipcc, "--offload-arch=gfx950", "-Xarch_device", "-O0", "-O1", "-g",
