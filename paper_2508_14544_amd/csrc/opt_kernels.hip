@@ -25,7 +25,10 @@
 //   * starts range over [a_i, max a + sum(o + 1) + 1], a horizon within which
 //     the sequential schedule already finishes every request (an instance
 //     whose horizon reaches 2^27 is not searched: SCHED_E_UNSUPPORTED).
-// A node budget per instance guarantees every lane reaches the exit.
+// A node budget per lane guarantees every lane reaches the exit.  Instances
+// that the one-lane first pass does not finish within a short budget are
+// searched again by one wave each, split over its lanes (k_optimum_split).
+// The first pass keeps 2 VGPRs in scratch (12 bytes per lane).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -51,7 +54,13 @@ struct OptParams {
   int64_t* total_latency;
   int32_t* status;
   int64_t* nodes;
+  int32_t unfinished;       // first pass: status of an instance not finished within node_cap
 };
+
+// status of an instance left to the second pass
+constexpr int kSplit = -100;
+// nodes of the first pass (one lane per instance)
+constexpr int64_t kFirstPassNodes = int64_t(1) << 15;
 
 // One instance, sorted into search order.
 struct Inst {
@@ -78,8 +87,8 @@ struct Search {
 // Level D places request D, runs 0..D-1 being placed at total cost `cost`.
 // Every array index below is a compile-time constant, so the state stays in
 // registers.
-template <int D>
-__device__ __forceinline__ void place(const Inst& I, Search& S, int32_t cost) {
+template <int D, bool SHARED = false>
+__device__ __forceinline__ void place(const Inst& I, Search& S, int32_t cost, int32_t* sb = nullptr) {
   if constexpr (D < kMaxN) {
     const int32_t lo = (D > 0 && ((I.same >> D) & 1u)) ? S.c[D > 0 ? D - 1 : 0] - I.o[D > 0 ? D - 1 : 0] : I.a[D];
     for (int32_t pd = lo;; ++pd) {
@@ -90,6 +99,13 @@ __device__ __forceinline__ void place(const Inst& I, Search& S, int32_t cost) {
       if (++S.nodes > S.cap) {
         S.stop = true;
         return;
+      }
+      if constexpr (SHARED) {
+        // every 256 nodes: the best total that any lane of the wave has found
+        if ((S.nodes & 255) == 0) {
+          const int32_t g = __hip_atomic_load(sb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+          S.best = g < S.best ? g : S.best;
+        }
       }
       const int32_t c = cost + (pd + I.o[D] - I.a[D]);
       if (pd > I.horizon || c + I.rem[D + 1] >= S.best) return;  // later starts only cost more
@@ -105,6 +121,7 @@ __device__ __forceinline__ void place(const Inst& I, Search& S, int32_t cost) {
       if (!ok || mend > I.M) continue;
       if (D == I.n - 1) {
         S.best = c;  // a complete schedule; later starts here cost more
+        if constexpr (SHARED) atomicMin(sb, c);
         return;
       }
       S.c[D] = end;
@@ -114,7 +131,7 @@ __device__ __forceinline__ void place(const Inst& I, Search& S, int32_t cost) {
         if (cq >= pd && cq <= end) S.mem[q] += I.s[D] + (cq - pd);
       }
       S.mem[D] = mend;
-      place<D + 1>(I, S, c);
+      place<D + 1, SHARED>(I, S, c, sb);
 #pragma unroll
       for (int q = 0; q < D; ++q) {
         const int32_t cq = S.c[q];
@@ -125,21 +142,67 @@ __device__ __forceinline__ void place(const Inst& I, Search& S, int32_t cost) {
   }
 }
 
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_optimum(OptParams P) {
-  const int k = blockIdx.x * 64 + threadIdx.x;
-  if (k >= P.K) return;
+// The first two levels of a search split over the 64 lanes of a wave: every
+// lane walks the same feasible starts of the first two requests (without the
+// bound's pruning, so that the walk is the same in every lane) and searches
+// below the q-th pair of starts when q mod 64 is its lane, with the best total
+// found by any lane shared through LDS.
+template <int D>
+__device__ __forceinline__ void top(const Inst& I, Search& S, int32_t cost, int32_t* sb, int lane, int32_t& q) {
+  const int32_t lo = (D > 0 && ((I.same >> D) & 1u)) ? S.c[D > 0 ? D - 1 : 0] - I.o[D > 0 ? D - 1 : 0] : I.a[D];
+  for (int32_t pd = lo; pd <= I.horizon; ++pd) {
+    ++S.nodes;
+    const int32_t c = cost + (pd + I.o[D] - I.a[D]);
+    const int32_t end = pd + I.o[D];
+    bool ok = true;
+    int32_t mend = I.s[D] + I.o[D];
+#pragma unroll
+    for (int r = 0; r < D; ++r) {
+      const int32_t cr = S.c[r], pr = cr - I.o[r];
+      if (cr >= pd && cr <= end) ok = ok && S.mem[r] + I.s[D] + (cr - pd) <= I.M;
+      if (pr <= end && end <= cr) mend += I.s[r] + (end - pr);
+    }
+    if (!ok || mend > I.M) continue;
+    if (D == I.n - 1) {
+      // a complete schedule at the top (n <= 2): the same in every lane
+      S.best = c < S.best ? c : S.best;
+      return;
+    }
+    S.c[D] = end;
+#pragma unroll
+    for (int r = 0; r < D; ++r) {
+      const int32_t cr = S.c[r];
+      if (cr >= pd && cr <= end) S.mem[r] += I.s[D] + (cr - pd);
+    }
+    S.mem[D] = mend;
+    if constexpr (D == 1) {
+      if ((q++ & 63) == lane && c + I.rem[2] < S.best) {
+        const int32_t g = __hip_atomic_load(sb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        S.best = g < S.best ? g : S.best;
+        place<2, true>(I, S, c, sb);
+      }
+    } else {
+      top<D + 1>(I, S, c, sb, lane, q);
+    }
+#pragma unroll
+    for (int r = 0; r < D; ++r) {
+      const int32_t cr = S.c[r];
+      if (cr >= pd && cr <= end) S.mem[r] -= I.s[D] + (cr - pd);
+    }
+    if (S.stop) return;
+  }
+}
+
+// Validates instance k and brings it into search order (I), with the first
+// bound in S.best; returns its status.
+__device__ __forceinline__ int setup(const OptParams& P, const int k, Inst& I, Search& S) {
   const int64_t b = P.offsets[k];
   const int64_t e = P.offsets[k + 1];
   int status = SCHED_OK;
-  Search S;
   S.best = 0;
-  S.nodes = 0;
-  S.cap = static_cast<int32_t>(P.node_cap < 0x7FFFFFFF ? P.node_cap : 0x7FFFFFFF);
-  S.stop = false;
   if (b < 0 || e < b || e > P.N) status = SCHED_E_INVAL;
   const int n = status == SCHED_OK ? static_cast<int>(e - b) : 0;
   if (n > kMaxN) status = SCHED_E_UNSUPPORTED;
-  Inst I;
   I.n = n;
   I.M = P.M;
   if (status == SCHED_OK && n > 0) {
@@ -205,14 +268,62 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
         S.c[i] = 0;
         S.mem[i] = 0;
       }
-      place<0>(I, S, 0);
-      if (S.stop) status = SCHED_E_STEP_CAP;
     }
   }
-  if (status != SCHED_OK && status != SCHED_E_STEP_CAP) S.best = 0;
+  return status;
+}
+
+// First pass: one lane per instance, at most P.node_cap nodes; an instance
+// not finished within them gets P.unfinished (the second pass's mark, with
+// the best total found as its bound, or SCHED_E_STEP_CAP).
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_optimum(OptParams P) {
+  const int k = blockIdx.x * 64 + threadIdx.x;
+  if (k >= P.K) return;
+  Search S;
+  S.nodes = 0;
+  S.cap = static_cast<int32_t>(P.node_cap < 0x7FFFFFFF ? P.node_cap : 0x7FFFFFFF);
+  S.stop = false;
+  Inst I;
+  int status = setup(P, k, I, S);
+  if (status == SCHED_OK && I.n > 0) {
+    place<0>(I, S, 0);
+    if (S.stop) status = P.unfinished;
+  }
+  if (status != SCHED_OK && status != SCHED_E_STEP_CAP && status != kSplit) S.best = 0;
   P.total_latency[k] = S.best;
   P.status[k] = status;
   if (P.nodes) P.nodes[k] = S.nodes;
+}
+
+// Second pass: one wave per instance that the first pass left unfinished,
+// its search split over the lanes (see top), each lane with at most
+// P.node_cap nodes; the first pass's best total is the first bound.
+__global__ __launch_bounds__(64) void k_optimum_split(OptParams P) {
+  const int k = blockIdx.x;
+  if (P.status[k] != kSplit) return;
+  __shared__ int32_t sbest;
+  const int lane = static_cast<int>(threadIdx.x);
+  Search S;
+  S.nodes = 0;
+  S.cap = static_cast<int32_t>(P.node_cap < 0x7FFFFFFF ? P.node_cap : 0x7FFFFFFF);
+  S.stop = false;
+  Inst I;
+  (void)setup(P, k, I, S);  // valid: the first pass searched it
+  S.best = static_cast<int32_t>(P.total_latency[k]);
+  if (lane == 0) sbest = S.best;
+  __syncthreads();
+  int32_t q = 0;
+  top<0>(I, S, 0, &sbest, lane, q);
+  atomicMin(&sbest, S.best);
+  __syncthreads();
+  const bool cut = __builtin_amdgcn_ballot_w64(S.stop) != 0ull;
+  int64_t nodes = S.nodes;
+  for (int off = 32; off >= 1; off >>= 1) nodes += __shfl_xor(nodes, off, 64);
+  if (lane == 0) {
+    P.total_latency[k] = sbest;
+    P.status[k] = cut ? SCHED_E_STEP_CAP : SCHED_OK;
+    if (P.nodes) P.nodes[k] += nodes;
+  }
 }
 
 }  // namespace opt
@@ -234,11 +345,20 @@ extern "C" int sched_optimum(const sched_instances_t* in, int64_t M, const int64
   P.prompt = in->prompt;
   P.output = in->output;
   P.M = static_cast<int32_t>(M);
-  P.node_cap = node_cap > 0 ? node_cap : (int64_t(1) << 22);
+  const int64_t cap = node_cap > 0 ? node_cap : (int64_t(1) << 22);
   P.upper_bound = upper_bound;
   P.total_latency = total_latency;
   P.status = status;
   P.nodes = nodes;
-  hipLaunchKernelGGL(opt::k_optimum, dim3((P.K + 63) / 64), dim3(64), 0, static_cast<hipStream_t>(stream), P);
+  // a short first pass, then the unfinished instances one wave each
+  const bool split = cap > opt::kFirstPassNodes;
+  P.node_cap = split ? opt::kFirstPassNodes : cap;
+  P.unfinished = split ? opt::kSplit : SCHED_E_STEP_CAP;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  hipLaunchKernelGGL(opt::k_optimum, dim3((P.K + 63) / 64), dim3(64), 0, st, P);
+  if (split && hipGetLastError() == hipSuccess) {
+    P.node_cap = cap;
+    hipLaunchKernelGGL(opt::k_optimum_split, dim3(P.K), dim3(64), 0, st, P);
+  }
   return hipGetLastError() == hipSuccess ? SCHED_OK : SCHED_E_HIP;
 }
