@@ -264,6 +264,8 @@ def main():
     ap.add_argument("--algo", default="amin", choices=["amin", "amax", "hsf", "aell", "adaptive", "arandom"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--running-capacity", type=int, default=0)
+    ap.add_argument("--workgroup-waves", type=int, default=0,
+                    help="2 or 4: every instance simulated by a workgroup of that many waves (A_max, A_min, H-SF)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -309,7 +311,7 @@ def main():
                     if t is not None)
     out = B.alloc_results(db)
     stream = torch.cuda.current_stream(dev)
-    kw = dict(stream=stream, running_capacity=args.running_capacity)
+    kw = dict(stream=stream, running_capacity=args.running_capacity, workgroup_waves=args.workgroup_waves)
 
     for _ in range(args.warmup):
         B.simulate_into(db, algo, out, **kw)
@@ -350,7 +352,9 @@ def main():
         torch.cuda.synchronize()
 
     achieved = OPS_PER_REQUEST_STEP * rs / (sim_avg_ms / 1e3)
-    traffic = load_traffic(args.workload, args.algo)
+    # (the committed profiles are of the default launches, one wave per instance)
+    profiled = args.workgroup_waves <= 1 and not args.running_capacity
+    traffic = load_traffic(args.workload, args.algo) if profiled else None
     measured_peaks = None if args.no_peak_probe else probe_peaks()
     result = {
         "metric": METRIC,
@@ -379,6 +383,7 @@ def main():
             "instance_steps_per_step": int(g["makespan"].astype(np.int64).sum()),
             "requests_x_makespan_per_step": int((np.diff(batch.offsets) * g["makespan"].astype(np.int64)).sum()),
             "instances_subset": subset or None,
+            "workgroup_waves": args.workgroup_waves or 1,
             "instances_per_policy": ({"A_min": int((g["algo_used"] == B.AMIN).sum()),
                                       "A_l": int((g["algo_used"] == B.AELL).sum())}
                                      if args.algo == "adaptive" else None),
@@ -392,7 +397,7 @@ def main():
             "unit": "TOP/s",
             "frac": achieved / PEAK_INT32_LANE_OPS,
             "traffic": traffic,
-            "hardware_fraction": load_hardware_fraction(args.workload, args.algo, sim_avg_ms),
+            "hardware_fraction": load_hardware_fraction(args.workload, args.algo, sim_avg_ms) if profiled else None,
             "kernel_ms": sim_avg_ms,
             "kernel_ms_median": float(np.median(sim_ms)),
             "ops_per_request_step": OPS_PER_REQUEST_STEP,

@@ -1,7 +1,8 @@
 // sched_kernels.hip -- the C ABI of the scheduler simulator (host side) and
-// the kernels it launches, except the wide row ladder (sched_wide.hip, its
-// own translation unit so that its large bodies do not change how the other
-// kernels are compiled).  The device code is in sim_device.hpp.
+// the kernels it launches, except the wide row ladder (sched_wide.hip) and
+// the workgroup kernels (sched_group.hip), each its own translation unit so
+// that their large bodies do not change how the other kernels are compiled.
+// The device code is in sim_device.hpp.
 #include "sim_device.hpp"
 
 namespace sk {

@@ -1,47 +1,50 @@
 // sim_device.hpp -- gfx950 kernels of the scheduler simulator (device code).
 //
-// One wave64 workgroup simulates one instance from t = 0 to its last
-// completion; nothing returns to the host between steps.
+// One wave64 simulates one instance from t = 0 to its last completion (or a
+// workgroup of W waves, see group_exchange); nothing returns to the host
+// between steps.
 //
 // k_prepare (per instance): validates the requests, computes the default step
 //   cap, initialises the per-request outputs, and ranks the requests by
-//   (initial planning length, index) with a stable two-pass LSD radix sort
+//   (initial planning length, tie key, index) with a stable LSD radix sort
 //   (8-bit digits, LDS histogram, ballot-based stable scatter).  The ranked
 //   records (key, s | o << 16) go to a workspace slice of the instance.
 //
-// k_simulate (per instance), one body per policy (A_max, A_min, H-SF, A_l,
-// A_random; the adaptive policy runs the A_min and the A_l bodies, each on
-// its own instances), state:
+// k_simulate_ladder / k_simulate_ladder_wide / k_simulate / k_simulate_group
+// (per instance), one body per policy (A_max, A_min, H-SF, A_l, A_random; the
+// adaptive policy runs the A_min and the A_l bodies, each on its own
+// instances), state:
 //   running set R    -- ROWS x 64 register slots, row r lane j holds one run:
 //                       planned end Rend = p + est, x = s - p + t_r, completion
-//                       C = p + o, key = est << 17 | index, and h = f(Rend) +
+//                       C = p + o, key = est << 17 | rank, and h = f(Rend) +
 //                       Rend - t_r, where f(c) is the planned memory at step c of
 //                       all runs whose planned end is >= c (equation (2) summed
 //                       over the planned set).  t_r is a base step that keeps the
-//                       int32 values small (rebased every 2^16 steps).  The first
-//                       body has 5 rows; a wave whose instance outgrows them
-//                       hands its state to a 6-row, then an 8-row body in the
-//                       same kernel (A_l: straight to 8), and instances beyond
-//                       512 runs are simulated again by a 10-row, then a 16-row
-//                       retry launch.  Scans cover every row: a uniform branch
-//                       per row to stop at the last occupied one measured slower,
-//                       although runs occupy 2 or 3 of the 5 rows most of the time.
+//                       int32 values small (rebased every 2^16 steps).  A wave
+//                       moves, state and all, along a ladder of bodies with 2, 3,
+//                       5, 8, 10 (then 12, 16) rows as its running set grows and
+//                       shrinks; instances beyond 1024 runs go to workgroups.
+//                       Scans cover every row of the current body.
 //   fresh waiting F  -- two-level bitmap over key ranks in LDS; the smallest
 //                       waiting key is the first set bit.  Its word is cached in
 //                       scalar registers until it empties.
-//   cancelled V      -- A_min: unsorted (key, s | o << 16) array in LDS, the
-//                       smallest key found by a wave min-reduction; A_l: a FIFO
-//                       ring of promoted requests in LDS.
+//   cancelled V      -- A_min: a register row U of recent cancellations in
+//                       front of an unsorted (key, s | o << 16) array in LDS
+//                       (or global memory), the smallest key found by a wave
+//                       min-reduction; A_l: an append-only queue of promoted
+//                       requests in global memory read through a register
+//                       window.
 // Per step: arrivals set bits of F; runs with C == t complete (A_l: runs still
-// present at their planned end are promoted to the back of V); for A_min the
-// projected memory P at t+1 is compared with M and runs are cancelled in
-// ascending key while P > M; then candidates (smallest key of F and V; A_l:
-// F first) are admitted while equation (2) holds.  The admission test needs
-// only O(1) wave reductions because the planned set before the test is always
-// feasible (every checkpoint after the candidate's planned end was verified
-// when its runs were admitted), so it checks: step t (runs completing now hold
-// s+o), step t+1 when a run is already past its planned end, every existing
-// planned end <= the candidate's via max h, and the candidate's own planned end.
+// present at their planned end are promoted to the back of the queue); for
+// A_min the projected memory P at t+1 is compared with M and runs are
+// cancelled in ascending key while P > M; then candidates (smallest key of F,
+// U and V; A_l: F first) are admitted while equation (2) holds.  The admission
+// test needs only O(1) wave reductions because the planned set before the test
+// is always feasible (every checkpoint after the candidate's planned end was
+// verified when its runs were admitted), so it checks: step t (runs completing
+// now hold s+o), step t+1 when a run is already past its planned end, every
+// existing planned end <= the candidate's via max h, and the candidate's own
+// planned end.
 #pragma once
 
 #include <hip/hip_runtime.h>
