@@ -80,7 +80,8 @@ enum {
   SCHED_E_HIP = -5,         /* call: a HIP runtime call failed                                  */
   SCHED_E_UNSUPPORTED = -6, /* call: capacity request beyond what the kernels hold.
                                status: o, u or l >= 2^15, s >= 2^16, n >= 2^17, a priority
-                               outside [0, 2^15), or more than 1024 requests (or a forced
+                               outside [0, 2^15), or more than 8192 requests (4096 where eight
+                               waves' bitmaps do not fit the LDS; or more than a forced
                                running_capacity) would run at once                              */
   SCHED_E_ARRIVAL = -7,     /* status: an arrival < 0 or arrivals not non-decreasing in index  */
   SCHED_E_SCRATCH = -8      /* call (sched_simulate_noalloc): the call needs more workspace than
@@ -229,11 +230,12 @@ int sched_validate(const sched_instances_t* instances, int32_t algo, int64_t M, 
  * latency (equation (3)) over every non-preemptive schedule that knows the
  * true outputs and keeps equation (1) (the OPT of the competitive analysis,
  * Section 2), by exhaustive branch and bound: a first launch searches every
- * instance on one GPU lane for at most min(node_cap, 2^15) nodes; an instance
- * not finished by then is searched again by a whole wave, its search tree
- * split over the 64 lanes at the starts of its first two requests, each lane
- * with at most node_cap nodes and the best total found by any lane shared
- * through LDS (the first launch's best is the starting bound).  Reads offsets, arrival (NULL = all 0), prompt and output of `instances`
+ * instance on one GPU lane for at most min(node_cap, 2^16) nodes; an instance
+ * not finished by then is searched again by a whole wave, its search tree cut
+ * at the starts of its first three requests into pieces that the 64 lanes
+ * claim one at a time, each lane with at most node_cap nodes and the best
+ * total found by any lane shared through LDS (the first launch's best is the
+ * starting bound).  Reads offsets, arrival (NULL = all 0), prompt and output of `instances`
  * (device pointers; lower, upper and priority are ignored).  upper_bound
  * (device, [K] or NULL) may give, per instance, the total latency of a known
  * feasible schedule (e.g. a policy's), which only speeds the search up

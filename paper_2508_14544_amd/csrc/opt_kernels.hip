@@ -60,7 +60,7 @@ struct OptParams {
 // status of an instance left to the second pass
 constexpr int kSplit = -100;
 // nodes of the first pass (one lane per instance)
-constexpr int64_t kFirstPassNodes = int64_t(1) << 15;
+constexpr int64_t kFirstPassNodes = int64_t(1) << 16;
 
 // One instance, sorted into search order.
 struct Inst {
@@ -142,13 +142,18 @@ __device__ __forceinline__ void place(const Inst& I, Search& S, int32_t cost, in
   }
 }
 
-// The first two levels of a search split over the 64 lanes of a wave: every
-// lane walks the same feasible starts of the first two requests (without the
-// bound's pruning, so that the walk is the same in every lane) and searches
-// below the q-th pair of starts when q mod 64 is its lane, with the best total
-// found by any lane shared through LDS.
+// The first kSplitDepth levels of a search split over the 64 lanes of a wave:
+// every lane walks the same feasible starts of the first kSplitDepth requests
+// (without the bound's pruning, so that the walk, and the numbering of its
+// leaves, is the same in every lane) and searches below the leaves it claims:
+// a lane claims the next unclaimed leaf from a counter in LDS whenever it has
+// searched below its last one, so lanes that finish early take more.  The
+// best total found by any lane is shared through LDS.
+constexpr int kSplitDepth = 3;
+
 template <int D>
-__device__ __forceinline__ void top(const Inst& I, Search& S, int32_t cost, int32_t* sb, int lane, int32_t& q) {
+__device__ __forceinline__ void top(const Inst& I, Search& S, int32_t cost, int32_t* sb, int32_t* cnt,
+                                    int32_t& leaf, int32_t& claim) {
   const int32_t lo = (D > 0 && ((I.same >> D) & 1u)) ? S.c[D > 0 ? D - 1 : 0] - I.o[D > 0 ? D - 1 : 0] : I.a[D];
   for (int32_t pd = lo; pd <= I.horizon; ++pd) {
     ++S.nodes;
@@ -164,7 +169,7 @@ __device__ __forceinline__ void top(const Inst& I, Search& S, int32_t cost, int3
     }
     if (!ok || mend > I.M) continue;
     if (D == I.n - 1) {
-      // a complete schedule at the top (n <= 2): the same in every lane
+      // a complete schedule above the split (n <= kSplitDepth): the same in every lane
       S.best = c < S.best ? c : S.best;
       return;
     }
@@ -175,14 +180,16 @@ __device__ __forceinline__ void top(const Inst& I, Search& S, int32_t cost, int3
       if (cr >= pd && cr <= end) S.mem[r] += I.s[D] + (cr - pd);
     }
     S.mem[D] = mend;
-    if constexpr (D == 1) {
-      if ((q++ & 63) == lane && c + I.rem[2] < S.best) {
+    if constexpr (D == kSplitDepth - 1) {
+      if (leaf == claim) {
         const int32_t g = __hip_atomic_load(sb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         S.best = g < S.best ? g : S.best;
-        place<2, true>(I, S, c, sb);
+        if (c + I.rem[D + 1] < S.best) place<D + 1, true>(I, S, c, sb);
+        claim = atomicAdd(cnt, 1);
       }
+      ++leaf;
     } else {
-      top<D + 1>(I, S, c, sb, lane, q);
+      top<D + 1>(I, S, c, sb, cnt, leaf, claim);
     }
 #pragma unroll
     for (int r = 0; r < D; ++r) {
@@ -301,7 +308,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
 __global__ __launch_bounds__(64) void k_optimum_split(OptParams P) {
   const int k = blockIdx.x;
   if (P.status[k] != kSplit) return;
-  __shared__ int32_t sbest;
+  __shared__ int32_t sbest, scount;
   const int lane = static_cast<int>(threadIdx.x);
   Search S;
   S.nodes = 0;
@@ -310,10 +317,13 @@ __global__ __launch_bounds__(64) void k_optimum_split(OptParams P) {
   Inst I;
   (void)setup(P, k, I, S);  // valid: the first pass searched it
   S.best = static_cast<int32_t>(P.total_latency[k]);
-  if (lane == 0) sbest = S.best;
+  if (lane == 0) {
+    sbest = S.best;
+    scount = 0;
+  }
   __syncthreads();
-  int32_t q = 0;
-  top<0>(I, S, 0, &sbest, lane, q);
+  int32_t leaf = 0, claim = atomicAdd(&scount, 1);
+  top<0>(I, S, 0, &sbest, &scount, leaf, claim);
   atomicMin(&sbest, S.best);
   __syncthreads();
   const bool cut = __builtin_amdgcn_ballot_w64(S.stop) != 0ull;
