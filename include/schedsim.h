@@ -229,13 +229,13 @@ int sched_validate(const sched_instances_t* instances, int32_t algo, int64_t M, 
 /* The hindsight optimum of tiny instances (n_k <= 8): the minimum total
  * latency (equation (3)) over every non-preemptive schedule that knows the
  * true outputs and keeps equation (1) (the OPT of the competitive analysis,
- * Section 2), by exhaustive branch and bound: a first launch searches every
- * instance on one GPU lane for at most min(node_cap, 2^16) nodes; an instance
- * not finished by then is searched again by a whole wave, its search tree cut
- * at the starts of its first three requests into pieces that the 64 lanes
- * claim one at a time, each lane with at most node_cap nodes and the best
- * total found by any lane shared through LDS (the first launch's best is the
- * starting bound).  Reads offsets, arrival (NULL = all 0), prompt and output of `instances`
+ * Section 2), by exhaustive branch and bound on the GPU: a first launch gives
+ * every instance one wave (its 64 lanes test 64 start steps of a request at
+ * once) and min(node_cap, 2^20) nodes; an instance not finished by then is
+ * searched again by a workgroup of 16 waves that claim the pieces below the
+ * starts of its first two requests one at a time, each wave with at most
+ * node_cap nodes and the best total found shared through LDS (the first
+ * launch's best is the starting bound).  Reads offsets, arrival (NULL = all 0), prompt and output of `instances`
  * (device pointers; lower, upper and priority are ignored).  upper_bound
  * (device, [K] or NULL) may give, per instance, the total latency of a known
  * feasible schedule (e.g. a policy's), which only speeds the search up
@@ -244,10 +244,10 @@ int sched_validate(const sched_instances_t* instances, int32_t algo, int64_t M, 
  * instance, total_latency[K] and status[K] (SCHED_OK, SCHED_E_ARRIVAL,
  * SCHED_E_INTERVAL for o < 1 or s < 0, SCHED_E_TOO_BIG for s + o > M,
  * SCHED_E_INVAL for bad offsets, SCHED_E_UNSUPPORTED when max a + sum(o + 1)
- * reaches 2^27, SCHED_E_STEP_CAP when a lane's search exceeded node_cap nodes
+ * reaches 2^27, SCHED_E_STEP_CAP when a wave's search exceeded node_cap nodes
  * (total_latency then holds the best schedule found, an upper bound)), and,
- * if nodes is not NULL, nodes[K] searched (both launches, all lanes).
- * node_cap <= 0 selects 2^22; larger
+ * if nodes is not NULL, nodes[K] searched (start steps tested, both launches).
+ * node_cap <= 0 selects 2^26; larger
  * budgets are clamped to 2^31 - 1.  Returns SCHED_E_UNSUPPORTED if max_requests > 8 (nothing
  * queued), SCHED_E_INVAL for NULL pointers or M outside (0, 2^30). */
 int sched_optimum(const sched_instances_t* instances, int64_t M, const int64_t* upper_bound,

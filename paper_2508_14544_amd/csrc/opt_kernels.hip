@@ -1,19 +1,23 @@
-// opt_kernels.hip -- gfx950 kernel of the hindsight optimum on tiny instances.
+// opt_kernels.hip -- gfx950 kernels of the hindsight optimum on tiny instances.
 //
 // The hindsight optimum (the OPT of the competitive analysis, Section 2) is
 // the minimum total latency (equation (3)) over every non-preemptive schedule
 // that knows the true output lengths: request i starts at some p_i >= a_i,
 // holds s_i + (tau - p_i) tokens for tau in [p_i, p_i + o_i], and the total
-// may never exceed M (equation (1)).  One lane searches one instance (n <= 8)
+// may never exceed M (equation (1)).  A wave searches one instance (n <= 8)
 // by depth-first branch and bound over start steps in request order:
+//   * at every node the 64 lanes test 64 consecutive starts of the next
+//     request at once; a ballot gives the feasible ones and the wave descends
+//     into them in order, so the wave follows one path of the tree (no lane
+//     divergence) and visits the nodes one lane would, in the same order;
 //   * a start is feasible iff the total stays <= M at the completion step of
 //     every placed run that overlaps the new one and at the new run's own
 //     completion (between two completions the set of present runs only grows
 //     and each run's memory grows, so the maximum is at a completion).  The
 //     memory at each placed run's completion is kept up to date as runs are
 //     placed and removed, so a test costs O(depth);
-//   * each depth is its own template instance, so every array index is a
-//     compile-time constant and the search state stays in registers;
+//   * each depth is its own template instance, so every index into the search
+//     state is a compile-time constant and the state stays in registers;
 //   * the cost of a partial assignment plus the remaining requests' output
 //     lengths bounds any completion from below, and the cost grows with the
 //     start, so the first start that reaches the best total ends the level;
@@ -25,10 +29,11 @@
 //   * starts range over [a_i, max a + sum(o + 1) + 1], a horizon within which
 //     the sequential schedule already finishes every request (an instance
 //     whose horizon reaches 2^27 is not searched: SCHED_E_UNSUPPORTED).
-// A node budget per lane guarantees every lane reaches the exit.  Instances
-// that the one-lane first pass does not finish within a short budget are
-// searched again by one wave each, split over its lanes (k_optimum_split).
-// The first pass keeps 2 VGPRs in scratch (12 bytes per lane).
+// A first launch gives every instance one wave and a short node budget; an
+// instance not finished by then is searched again by a workgroup of 16 waves
+// that claim the pieces below the starts of its first two requests one at a
+// time and share the best total through LDS.  Node budgets guarantee every
+// wave reaches the exit.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -54,13 +59,16 @@ struct OptParams {
   int64_t* total_latency;
   int32_t* status;
   int64_t* nodes;
-  int32_t unfinished;       // first pass: status of an instance not finished within node_cap
+  int32_t unfinished;       // first launch: status of an instance not finished within node_cap
 };
 
-// status of an instance left to the second pass
+// status of an instance left to the second launch
 constexpr int kSplit = -100;
-// nodes of the first pass (one lane per instance)
-constexpr int64_t kFirstPassNodes = int64_t(1) << 16;
+// nodes of the first launch (one wave per instance)
+constexpr int64_t kFirstPassNodes = int64_t(1) << 20;
+// waves of a second-launch workgroup, and the depth below which they split
+constexpr int kGroupWaves = 16;
+constexpr int kSplitDepth = 2;
 
 // One instance, sorted into search order.
 struct Inst {
@@ -84,33 +92,25 @@ struct Search {
   bool stop;
 };
 
-// Level D places request D, runs 0..D-1 being placed at total cost `cost`.
-// Every array index below is a compile-time constant, so the state stays in
-// registers.
-template <int D, bool SHARED = false>
-__device__ __forceinline__ void place(const Inst& I, Search& S, int32_t cost, int32_t* sb = nullptr) {
+// The search below a node at depth D (runs 0..D-1 placed at total cost
+// `cost`), the lanes of the wave testing 64 starts at a time.  SHARED: the
+// best total is also shared with the other waves of the workgroup through *sb
+// (read at every chunk of starts, lowered whenever this wave improves it).
+// Nodes are counted per start tested.
+template <int D, bool SHARED>
+__device__ __forceinline__ void wplace(const Inst& I, Search& S, int32_t cost, int lane, int32_t* sb) {
   if constexpr (D < kMaxN) {
     const int32_t lo = (D > 0 && ((I.same >> D) & 1u)) ? S.c[D > 0 ? D - 1 : 0] - I.o[D > 0 ? D - 1 : 0] : I.a[D];
-    for (int32_t pd = lo;; ++pd) {
-      // the placed runs are re-read every iteration rather than hoisted out of
-      // the loop: hoisted copies would stay live across every deeper level
-#pragma unroll
-      for (int q = 0; q < D; ++q) asm volatile("" : "+v"(S.c[q]), "+v"(S.mem[q]));
-      if (++S.nodes > S.cap) {
-        S.stop = true;
-        return;
-      }
+    for (int32_t base = lo; base <= I.horizon; base += 64) {
       if constexpr (SHARED) {
-        // every 256 nodes: the best total that any lane of the wave has found
-        if ((S.nodes & 255) == 0) {
-          const int32_t g = __hip_atomic_load(sb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-          S.best = g < S.best ? g : S.best;
-        }
+        const int32_t g = __hip_atomic_load(sb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        S.best = g < S.best ? g : S.best;
       }
+      const int32_t pd = base + lane;
       const int32_t c = cost + (pd + I.o[D] - I.a[D]);
-      if (pd > I.horizon || c + I.rem[D + 1] >= S.best) return;  // later starts only cost more
+      const bool live = pd <= I.horizon && c + I.rem[D + 1] < S.best;
       const int32_t end = pd + I.o[D];
-      bool ok = true;
+      bool ok = live;
       int32_t mend = I.s[D] + I.o[D];
 #pragma unroll
       for (int q = 0; q < D; ++q) {
@@ -118,42 +118,58 @@ __device__ __forceinline__ void place(const Inst& I, Search& S, int32_t cost, in
         if (cq >= pd && cq <= end) ok = ok && S.mem[q] + I.s[D] + (cq - pd) <= I.M;
         if (pq <= end && end <= cq) mend += I.s[q] + (end - pq);
       }
-      if (!ok || mend > I.M) continue;
-      if (D == I.n - 1) {
-        S.best = c;  // a complete schedule; later starts here cost more
-        if constexpr (SHARED) atomicMin(sb, c);
+      ok = ok && mend <= I.M;
+      uint64_t m = __builtin_amdgcn_ballot_w64(ok);
+      const uint64_t lv = __builtin_amdgcn_ballot_w64(live);
+      S.nodes += __builtin_popcountll(lv) + (lv != ~0ull ? 1 : 0);
+      if (S.nodes > S.cap) {
+        S.stop = true;
         return;
       }
-      S.c[D] = end;
+      while (m) {
+        const int j = __builtin_ctzll(m);
+        m &= m - 1;
+        const int32_t pj = base + j;
+        const int32_t cj = cost + (pj + I.o[D] - I.a[D]);
+        if (cj + I.rem[D + 1] >= S.best) return;  // the bound improved below an earlier start
+        if (D == I.n - 1) {
+          S.best = cj;  // a complete schedule; later starts here cost more
+          if constexpr (SHARED) {
+            if (lane == 0) atomicMin(sb, cj);
+          }
+          return;
+        }
+        const int32_t ej = pj + I.o[D];
+        const int32_t mj = __builtin_amdgcn_readlane(mend, j);
+        S.c[D] = ej;
 #pragma unroll
-      for (int q = 0; q < D; ++q) {
-        const int32_t cq = S.c[q];
-        if (cq >= pd && cq <= end) S.mem[q] += I.s[D] + (cq - pd);
-      }
-      S.mem[D] = mend;
-      place<D + 1, SHARED>(I, S, c, sb);
+        for (int q = 0; q < D; ++q) {
+          const int32_t cq = S.c[q];
+          if (cq >= pj && cq <= ej) S.mem[q] += I.s[D] + (cq - pj);
+        }
+        S.mem[D] = mj;
+        wplace<D + 1, SHARED>(I, S, cj, lane, sb);
 #pragma unroll
-      for (int q = 0; q < D; ++q) {
-        const int32_t cq = S.c[q];
-        if (cq >= pd && cq <= end) S.mem[q] -= I.s[D] + (cq - pd);
+        for (int q = 0; q < D; ++q) {
+          const int32_t cq = S.c[q];
+          if (cq >= pj && cq <= ej) S.mem[q] -= I.s[D] + (cq - pj);
+        }
+        if (S.stop) return;
       }
-      if (S.stop) return;
+      if (lv != ~0ull) return;
     }
   }
 }
 
-// The first kSplitDepth levels of a search split over the 64 lanes of a wave:
-// every lane walks the same feasible starts of the first kSplitDepth requests
-// (without the bound's pruning, so that the walk, and the numbering of its
-// leaves, is the same in every lane) and searches below the leaves it claims:
-// a lane claims the next unclaimed leaf from a counter in LDS whenever it has
-// searched below its last one, so lanes that finish early take more.  The
-// best total found by any lane is shared through LDS.
-constexpr int kSplitDepth = 3;
-
+// The first kSplitDepth levels for the waves of a workgroup: every wave walks
+// the same feasible starts of the first kSplitDepth requests (without the
+// bound's pruning, so that the walk, and the numbering of its leaves, is the
+// same in every wave) and searches below the leaves it claims: a wave claims
+// the next unclaimed leaf from a counter in LDS whenever it has searched below
+// its last one.
 template <int D>
-__device__ __forceinline__ void top(const Inst& I, Search& S, int32_t cost, int32_t* sb, int32_t* cnt,
-                                    int32_t& leaf, int32_t& claim) {
+__device__ __forceinline__ void wtop(const Inst& I, Search& S, int32_t cost, int lane, int32_t* sb, int32_t* cnt,
+                                     int32_t& leaf, int32_t& claim) {
   const int32_t lo = (D > 0 && ((I.same >> D) & 1u)) ? S.c[D > 0 ? D - 1 : 0] - I.o[D > 0 ? D - 1 : 0] : I.a[D];
   for (int32_t pd = lo; pd <= I.horizon; ++pd) {
     ++S.nodes;
@@ -169,7 +185,7 @@ __device__ __forceinline__ void top(const Inst& I, Search& S, int32_t cost, int3
     }
     if (!ok || mend > I.M) continue;
     if (D == I.n - 1) {
-      // a complete schedule above the split (n <= kSplitDepth): the same in every lane
+      // a complete schedule above the split (n <= kSplitDepth): the same in every wave
       S.best = c < S.best ? c : S.best;
       return;
     }
@@ -184,12 +200,14 @@ __device__ __forceinline__ void top(const Inst& I, Search& S, int32_t cost, int3
       if (leaf == claim) {
         const int32_t g = __hip_atomic_load(sb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         S.best = g < S.best ? g : S.best;
-        if (c + I.rem[D + 1] < S.best) place<D + 1, true>(I, S, c, sb);
-        claim = atomicAdd(cnt, 1);
+        if (c + I.rem[D + 1] < S.best) wplace<D + 1, true>(I, S, c, lane, sb);
+        int32_t nx = 0;
+        if (lane == 0) nx = atomicAdd(cnt, 1);
+        claim = __builtin_amdgcn_readfirstlane(nx);
       }
       ++leaf;
     } else {
-      top<D + 1>(I, S, c, sb, cnt, leaf, claim);
+      wtop<D + 1>(I, S, c, lane, sb, cnt, leaf, claim);
     }
 #pragma unroll
     for (int r = 0; r < D; ++r) {
@@ -280,12 +298,12 @@ __device__ __forceinline__ int setup(const OptParams& P, const int k, Inst& I, S
   return status;
 }
 
-// First pass: one lane per instance, at most P.node_cap nodes; an instance
-// not finished within them gets P.unfinished (the second pass's mark, with
+// First launch: one wave per instance, at most P.node_cap nodes; an instance
+// not finished within them gets P.unfinished (the second launch's mark, with
 // the best total found as its bound, or SCHED_E_STEP_CAP).
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_optimum(OptParams P) {
-  const int k = blockIdx.x * 64 + threadIdx.x;
-  if (k >= P.K) return;
+__global__ __launch_bounds__(64) void k_optimum(OptParams P) {
+  const int k = blockIdx.x;
+  const int lane = static_cast<int>(threadIdx.x);
   Search S;
   S.nodes = 0;
   S.cap = static_cast<int32_t>(P.node_cap < 0x7FFFFFFF ? P.node_cap : 0x7FFFFFFF);
@@ -293,46 +311,54 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
   Inst I;
   int status = setup(P, k, I, S);
   if (status == SCHED_OK && I.n > 0) {
-    place<0>(I, S, 0);
+    wplace<0, false>(I, S, 0, lane, nullptr);
     if (S.stop) status = P.unfinished;
   }
   if (status != SCHED_OK && status != SCHED_E_STEP_CAP && status != kSplit) S.best = 0;
-  P.total_latency[k] = S.best;
-  P.status[k] = status;
-  if (P.nodes) P.nodes[k] = S.nodes;
+  if (lane == 0) {
+    P.total_latency[k] = S.best;
+    P.status[k] = status;
+    if (P.nodes) P.nodes[k] = S.nodes;
+  }
 }
 
-// Second pass: one wave per instance that the first pass left unfinished,
-// its search split over the lanes (see top), each lane with at most
-// P.node_cap nodes; the first pass's best total is the first bound.
-__global__ __launch_bounds__(64) void k_optimum_split(OptParams P) {
+// Second launch: a workgroup of kGroupWaves waves per instance that the first
+// left unfinished (see wtop), each wave with at most P.node_cap nodes; the
+// first launch's best total is the starting bound.
+__global__ __launch_bounds__(64 * kGroupWaves) void k_optimum_group(OptParams P) {
   const int k = blockIdx.x;
   if (P.status[k] != kSplit) return;
-  __shared__ int32_t sbest, scount;
-  const int lane = static_cast<int>(threadIdx.x);
+  __shared__ int32_t sbest, scount, sstop;
+  __shared__ unsigned long long snodes;
+  const int lane = static_cast<int>(threadIdx.x & 63u);
   Search S;
   S.nodes = 0;
   S.cap = static_cast<int32_t>(P.node_cap < 0x7FFFFFFF ? P.node_cap : 0x7FFFFFFF);
   S.stop = false;
   Inst I;
-  (void)setup(P, k, I, S);  // valid: the first pass searched it
+  (void)setup(P, k, I, S);  // valid: the first launch searched it
   S.best = static_cast<int32_t>(P.total_latency[k]);
-  if (lane == 0) {
+  if (threadIdx.x == 0) {
     sbest = S.best;
     scount = 0;
+    sstop = 0;
+    snodes = 0ull;
   }
   __syncthreads();
-  int32_t leaf = 0, claim = atomicAdd(&scount, 1);
-  top<0>(I, S, 0, &sbest, &scount, leaf, claim);
-  atomicMin(&sbest, S.best);
-  __syncthreads();
-  const bool cut = __builtin_amdgcn_ballot_w64(S.stop) != 0ull;
-  int64_t nodes = S.nodes;
-  for (int off = 32; off >= 1; off >>= 1) nodes += __shfl_xor(nodes, off, 64);
+  int32_t first = 0;
+  if (lane == 0) first = atomicAdd(&scount, 1);
+  int32_t leaf = 0, claim = __builtin_amdgcn_readfirstlane(first);
+  wtop<0>(I, S, 0, lane, &sbest, &scount, leaf, claim);
   if (lane == 0) {
+    atomicMin(&sbest, S.best);
+    atomicAdd(&snodes, static_cast<unsigned long long>(S.nodes));
+    if (S.stop) atomicOr(&sstop, 1);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
     P.total_latency[k] = sbest;
-    P.status[k] = cut ? SCHED_E_STEP_CAP : SCHED_OK;
-    if (P.nodes) P.nodes[k] += nodes;
+    P.status[k] = sstop ? SCHED_E_STEP_CAP : SCHED_OK;
+    if (P.nodes) P.nodes[k] += static_cast<int64_t>(snodes);
   }
 }
 
@@ -355,20 +381,20 @@ extern "C" int sched_optimum(const sched_instances_t* in, int64_t M, const int64
   P.prompt = in->prompt;
   P.output = in->output;
   P.M = static_cast<int32_t>(M);
-  const int64_t cap = node_cap > 0 ? node_cap : (int64_t(1) << 22);
+  const int64_t cap = node_cap > 0 ? node_cap : (int64_t(1) << 26);
   P.upper_bound = upper_bound;
   P.total_latency = total_latency;
   P.status = status;
   P.nodes = nodes;
-  // a short first pass, then the unfinished instances one wave each
+  // a first launch with a short budget, then the unfinished instances on workgroups
   const bool split = cap > opt::kFirstPassNodes;
   P.node_cap = split ? opt::kFirstPassNodes : cap;
   P.unfinished = split ? opt::kSplit : SCHED_E_STEP_CAP;
   const hipStream_t st = static_cast<hipStream_t>(stream);
-  hipLaunchKernelGGL(opt::k_optimum, dim3((P.K + 63) / 64), dim3(64), 0, st, P);
+  hipLaunchKernelGGL(opt::k_optimum, dim3(P.K), dim3(64), 0, st, P);
   if (split && hipGetLastError() == hipSuccess) {
     P.node_cap = cap;
-    hipLaunchKernelGGL(opt::k_optimum_split, dim3(P.K), dim3(64), 0, st, P);
+    hipLaunchKernelGGL(opt::k_optimum_group, dim3(P.K), dim3(64 * opt::kGroupWaves), 0, st, P);
   }
   return hipGetLastError() == hipSuccess ? SCHED_OK : SCHED_E_HIP;
 }
