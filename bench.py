@@ -228,8 +228,8 @@ def cpu_baseline(batch, algo, g_out, target_s: float, threads: int):
     O.simulate_batch(batch, algo, instances=probe, threads=threads)
     per = (time.perf_counter() - t0) / max(1, len(probe))  # wall per instance with `threads` in flight
     want = int(max(threads, min(K, target_s / max(per, 1e-6))))
-    stride = max(1, K // want)
-    sample = list(range(0, K, stride))[:want]
+    # evenly spread over the batch (its instances come in blocks of alpha)
+    sample = sorted({int(round(i * (K - 1) / max(1, want - 1))) for i in range(want)}) if want < K else list(range(K))
     t0 = time.perf_counter()
     ref = O.simulate_batch(batch, algo, instances=sample, threads=threads)
     wall = time.perf_counter() - t0
@@ -250,7 +250,7 @@ def cpu_baseline(batch, algo, g_out, target_s: float, threads: int):
         "value": rs / wall, "unit": "request-steps/s", "cores": threads, "kind": "oracle",
         "threads": threads, "cpus_available": avail, "cpu_model": model,
         "sample": (f"{len(sample)} of {K} instances ("
-                   + (f"one in {stride}" if stride > 1 else "the first, in index order")
+                   + ("evenly spaced in index order" if len(sample) < K else "all")
                    + f"), {rs} request-steps in {wall:.1f} s on {threads} host threads"),
     }, bool(ok), (w_ratio, len(sub))
 
