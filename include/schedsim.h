@@ -206,7 +206,10 @@ int sched_simulate_opts(const sched_instances_t* instances, int32_t algo, int64_
  * policies on `stream`).  The workspace needs 20 bytes per request plus 8 per
  * instance, 16 more per request with tie keys, and 8 more per request for
  * A_l and the adaptive policy or when n_max exceeds the LDS room of A_min's
- * cancelled set; a call that needs more returns
+ * cancelled set, and, for A_min when n_max exceeds 1024 (workgroup launches
+ * whose waves keep cancelled sets in global memory), up to 64 MiB more
+ * (8 * W * n_max bytes per workgroup of W waves, for at most as many
+ * workgroups as fit in 64 MiB); a call that needs more returns
  * SCHED_E_SCRATCH before queueing anything (e.g. at most about 5.0 million
  * requests without tie keys).  Every call on a device shares that device's
  * array: calls whose work overlaps on one device (other streams, other host
