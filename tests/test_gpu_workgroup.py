@@ -154,3 +154,36 @@ def test_workgroup_option_checks(B):
     for ww in (0, 1):
         g = gpu_run(B, batch, O.AMIN, workgroup_waves=ww)
         assert_parity(batch, g, oracle_run(batch, O.AMIN))
+
+
+@pytest.mark.parametrize("ww", [2, 4])
+@pytest.mark.parametrize("cap", [3, 17])
+def test_workgroup_step_cap(B, ww, cap):
+    # a step cap ends every wave of the workgroup at the same step, with the
+    # oracle's partial outputs
+    batch = _growth_sweep(1, K=12)
+    for algo in (O.AMIN, O.AMAX, O.HSF):
+        ref = oracle_run(batch, algo, step_cap=cap)
+        assert (ref["status"] == O.E_STEP_CAP).any()
+        assert_parity(batch, gpu_run(B, batch, algo, step_cap=cap, workgroup_waves=ww), ref)
+
+
+def test_workgroup_launches_without_allocation(B):
+    # the no-allocation entry point with workgroups: from the start (global
+    # cancelled sets) and as the tier above 1024 runs; twice, the second batch
+    # smaller, against the allocating entry point
+    import torch
+    burst = _wide_instances()[0]
+    small = _growth_sweep(2, K=6)
+    pick = lambda b, k: {f: b.instance(k)[f] for f in ("arrival", "prompt", "output", "lower", "upper", "priority")}
+    big = W.from_lists(2000, [pick(small, k) for k in range(6)] + [pick(burst, 0)], name="noalloc_wide")
+    for batch in (big, W.from_lists(2000, [pick(small, k) for k in range(3)], name="noalloc_small")):
+        db = B.to_device(batch)
+        for kw in ({}, {"workgroup_waves": 4, "evicted_lds_limit": 1}):
+            ref = B.simulate(db, B.AMIN, **kw)
+            out = B.alloc_results(db)
+            B.simulate_into(db, B.AMIN, out, no_alloc=True, **kw)
+            torch.cuda.synchronize()
+            for f in ("status", "tel", "makespan", "request_steps", "total_evictions", "completion", "evictions"):
+                assert torch.equal(out[f], ref[f]), (batch.name, kw, f)
+            assert (out["status"] == 0).all()
