@@ -187,3 +187,21 @@ def test_workgroup_launches_without_allocation(B):
             for f in ("status", "tel", "makespan", "request_steps", "total_evictions", "completion", "evictions"):
                 assert torch.equal(out[f], ref[f]), (batch.name, kw, f)
             assert (out["status"] == 0).all()
+
+
+@pytest.mark.parametrize("ww", [2, 4])
+def test_workgroup_statuses_and_empty_instances(B, ww):
+    # invalid and empty instances next to valid ones: the same statuses and
+    # outputs as one wave per instance
+    good = {"arrival": [0, 1, 1], "prompt": [1, 2, 1], "output": [3, 2, 4], "lower": [1, 2, 2], "upper": [4, 2, 6]}
+    insts = [good, dict(good, lower=[4, 2, 2]), dict(good, output=[0, 2, 4]), dict(good, prompt=[1, 2, 9]),
+             dict(good, arrival=[1, 0, 1]), {"arrival": [], "prompt": [], "output": [], "lower": [], "upper": []},
+             dict(good, upper=[2, 2, 6]), good]
+    batch = W.from_lists(10, insts, name="wg_statuses")
+    for algo in (O.AMAX, O.AMIN, O.HSF):
+        g1 = gpu_run(B, batch, algo)
+        g = gpu_run(B, batch, algo, workgroup_waves=ww)
+        for f in FIELDS:
+            assert np.array_equal(g[f], g1[f]), (algo, f)
+        ok = [k for k in range(batch.num_instances) if g["status"][k] == 0]
+        assert_parity(batch, g, oracle_run(batch, algo, instances=ok), instances=ok)
