@@ -32,6 +32,31 @@ extern template __global__ void k_simulate_group<SCHED_AMIN, 4, 4, true>(Params)
 extern template __global__ void k_simulate_group<SCHED_AMIN, 4, 16, false>(Params);
 extern template __global__ void k_simulate_group<SCHED_AMIN, 4, 16, true>(Params);
 extern template __global__ void k_simulate_group<SCHED_AMIN, 8, 16, true>(Params);
+
+// Issue-priority classes (A_min with upper bounds, from k_prepare): kept only
+// where they differ between the instances of the batch; a batch whose
+// instances share one class keeps the priority by unfinished work alone.
+__global__ __launch_bounds__(256) void k_prio_classes(Params P) {
+  __shared__ int lo_s, hi_s;
+  if (threadIdx.x == 0) {
+    lo_s = 3;
+    hi_s = -1;
+  }
+  __syncthreads();
+  int lo = 3, hi = -1;
+  for (int k = threadIdx.x; k < P.K; k += 256) {
+    const int c = P.pclass[k];
+    if (c < 3) {
+      lo = c < lo ? c : lo;
+      hi = c > hi ? c : hi;
+    }
+  }
+  atomicMin(&lo_s, lo);
+  atomicMax(&hi_s, hi);
+  __syncthreads();
+  if (lo_s >= hi_s)
+    for (int k = threadIdx.x; k < P.K; k += 256) P.pclass[k] = -1;
+}
 }  // namespace sk
 
 // ---------------------------------------------------------------------------
@@ -452,6 +477,15 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   const size_t o_es = off; off = align_up(off + (tie && out->evictions ? 4 * N : 0), 256);
   const size_t o_vg = off; off = align_up(off + (any_global ? 8 * N : 0), 256);
   const size_t o_gv = off; off = align_up(off + 8 * static_cast<size_t>(group_words), 256);
+  // Priority classes only where every instance of the batch is resident at
+  // once (16 waves a CU), so that the launch lasts as long as its slowest
+  // instance; a batch served in several rounds of waves keeps the priority by
+  // unfinished work.
+  int n_cu = 0;
+  if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return SCHED_E_HIP;
+  const bool pcl = (algo == SCHED_AMIN || algo == SCHED_ADAPTIVE) && in->upper != nullptr && in->total_requests > 0 &&
+                   static_cast<int64_t>(K) <= 16 * static_cast<int64_t>(n_cu);
+  const size_t o_pc = off; off = align_up(off + (pcl ? 4 * K : 0), 256);
   // every workspace array is written before it is read (nothing needs clearing)
   void* ws = nullptr;
   if (no_alloc) {
@@ -485,6 +519,7 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   P.ev_st = tie && out->evictions ? reinterpret_cast<int32_t*>(base + o_es) : nullptr;
   P.vglob = any_global ? reinterpret_cast<uint64_t*>(base + o_vg) : nullptr;
   P.vgroup = group_words ? reinterpret_cast<uint64_t*>(base + o_gv) : nullptr;
+  P.pclass = pcl ? reinterpret_cast<int32_t*>(base + o_pc) : nullptr;
   P.nw_max = nw;
   P.nw1_max = nw1;
   P.run_cap = forced_rows > 0 ? forced_rows * 64 : INT32_MAX;
@@ -500,6 +535,10 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
     default: hipLaunchKernelGGL((sk::k_prepare<SCHED_ADAPTIVE>), grid, block, 0, st, P); break;
   }
   err = hipGetLastError();
+  if (err == hipSuccess && P.pclass) {
+    hipLaunchKernelGGL(sk::k_prio_classes, dim3(1), dim3(256), 0, st, P);
+    err = hipGetLastError();
+  }
   // Staging the completion steps in LDS (written out coalesced at the end of
   // an instance instead of one scattered store per completion) when it fits
   // without costing occupancy: at most the LDS share of the waves a CU holds

@@ -124,6 +124,10 @@ struct Params {
   // workgroup passes with global cancelled sets: n_max entries per wave of
   // each workgroup of the launch
   uint64_t* vgroup;
+  // A_min with upper bounds (alone or in the adaptive policy): each instance's
+  // issue-priority class (0-2 by the width of its intervals; 3: none), or -1
+  // when all instances share a class
+  int32_t* pclass;
 };
 
 // Internal statuses of an instance handed to a later pass: its running set
@@ -347,8 +351,24 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
     P.cap[k] = static_cast<int32_t>(cap);
     if (P.algo_of) P.algo_of[k] = algo;
     if (P.algo_used) P.algo_used[k] = algo;
+    if (P.pclass) P.pclass[k] = 3;
   }
   if (status != SCHED_OK || n == 0) return;
+  if (P.pclass && algo == SCHED_AMIN) {
+    // wide intervals mean more cancellations, so longer simulations: the
+    // class by sum(u - l) / sum(l) (< 0.3, < 0.75, above)
+    int64_t w = 0, l = 0;
+    for (int c = 0; c < n; c += 64) {
+      const int i = c + lane;
+      if (i < n) {
+        w += P.upper[b + i] - P.lower[b + i];
+        l += P.lower[b + i];
+      }
+    }
+    w = wave::sum_i64(w);
+    l = wave::sum_i64(l);
+    if (lane == 0) P.pclass[k] = 4 * w >= 3 * l ? 2 : 10 * w >= 3 * l ? 1 : 0;
+  }
 
   // ---- tie keys: each request's rank in the order (tie key, index) (A_l:
   // (arrival, tie key, index), its fresh-queue order) is its identity in the
@@ -922,11 +942,14 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     // Issue priority among the waves of a SIMD: the more requests an instance
     // still has to complete, the higher (four levels by the unfinished
     // fraction), so the instances that bound the launch are not slowed by
-    // their SIMD-mates.  Outputs do not depend on it.
+    // their SIMD-mates; where a batch mixes interval widths (A_min with upper
+    // bounds), the static class of the instance and whether half of it is
+    // done instead.  Outputs do not depend on it.
     int prio = -1;
+    const int pcls = (ALGO == SCHED_AMIN && P.pclass) ? P.pclass[k] : -1;
 #define SK_SET_PRIORITY()                                                            \
   do {                                                                               \
-    const int lv_ = (4 * (n - n_done) - 1) / n;                                      \
+    const int lv_ = pcls >= 0 ? pcls + (2 * (n - n_done) > n ? 1 : 0) : (4 * (n - n_done) - 1) / n; \
     if (lv_ != prio) {                                                               \
       prio = lv_;                                                                    \
       if (lv_ >= 3) __builtin_amdgcn_s_setprio(3);                                   \
