@@ -235,11 +235,15 @@ int sched_validate(const sched_instances_t* instances, int32_t algo, int64_t M, 
  * true outputs and keeps equation (1) (the OPT of the competitive analysis,
  * Section 2), by exhaustive branch and bound on the GPU: a first launch gives
  * every instance one wave (its 64 lanes test 64 start steps of a request at
- * once) and min(node_cap, 2^20) nodes; an instance not finished by then is
- * searched again by a workgroup of 16 waves that claim the pieces below the
- * starts of its first two requests one at a time, each wave with at most
- * node_cap nodes and the best total found shared through LDS (the first
- * launch's best is the starting bound).  Reads offsets, arrival (NULL = all 0), prompt and output of `instances`
+ * once) and min(node_cap, 2^17) nodes; the instances not finished by then are
+ * searched again by a second launch of as many 16-wave workgroups as the
+ * device holds at once, whose waves claim the pieces below the starts of an
+ * instance's first two requests one at a time from any unfinished instance
+ * (the first launch's best is the starting bound; best totals are shared in
+ * global memory at every claim and in LDS within a workgroup), each wave with
+ * at most node_cap nodes per instance it works on.  The second launch takes a
+ * stream-ordered workspace of 16 bytes per instance (hipMallocAsync).  Reads
+ * offsets, arrival (NULL = all 0), prompt and output of `instances`
  * (device pointers; lower, upper and priority are ignored).  upper_bound
  * (device, [K] or NULL) may give, per instance, the total latency of a known
  * feasible schedule (e.g. a policy's), which only speeds the search up

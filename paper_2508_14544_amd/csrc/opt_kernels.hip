@@ -29,11 +29,16 @@
 //   * starts range over [a_i, max a + sum(o + 1) + 1], a horizon within which
 //     the sequential schedule already finishes every request (an instance
 //     whose horizon reaches 2^27 is not searched: SCHED_E_UNSUPPORTED).
-// A first launch gives every instance one wave and a short node budget; an
-// instance not finished by then is searched again by a workgroup of 16 waves
-// that claim the pieces below the starts of its first two requests one at a
-// time and share the best total through LDS.  Node budgets guarantee every
-// wave reaches the exit.
+// A first launch gives every instance one wave and a short node budget.  The
+// instances it leaves unfinished are listed, and a second launch of as many
+// 16-wave workgroups as the device holds at once searches them together: the
+// pieces of an instance (the subtrees below the starts of its first two
+// requests) are claimed one at a time from a counter in global memory, so
+// every workgroup that has finished its own instance joins the ones still
+// open and the hardest instance ends up spread over the whole device.  The
+// best total of an instance is kept in global memory (exchanged at every
+// claim) and in LDS for the waves of a workgroup (read at every chunk of
+// starts).  Node budgets guarantee every wave reaches the exit.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -60,15 +65,20 @@ struct OptParams {
   int32_t* status;
   int64_t* nodes;
   int32_t unfinished;       // first launch: status of an instance not finished within node_cap
+  // second launch: [0] the number U of unfinished instances, then four arrays
+  // of K entries: the instances, their piece counters, best totals and flags
+  // (bit 0: every piece claimed; bit 1: a wave ran out of nodes)
+  int32_t* pool;
 };
 
 // status of an instance left to the second launch
 constexpr int kSplit = -100;
 // nodes of the first launch (one wave per instance)
-constexpr int64_t kFirstPassNodes = int64_t(1) << 20;
+constexpr int64_t kFirstPassNodes = int64_t(1) << 17;
 // waves of a second-launch workgroup, and the depth below which they split
 constexpr int kGroupWaves = 16;
 constexpr int kSplitDepth = 2;
+constexpr int kFlagClaimed = 1, kFlagStop = 2;
 
 // One instance, sorted into search order.
 struct Inst {
@@ -161,15 +171,17 @@ __device__ __forceinline__ void wplace(const Inst& I, Search& S, int32_t cost, i
   }
 }
 
-// The first kSplitDepth levels for the waves of a workgroup: every wave walks
-// the same feasible starts of the first kSplitDepth requests (without the
-// bound's pruning, so that the walk, and the numbering of its leaves, is the
-// same in every wave) and searches below the leaves it claims: a wave claims
-// the next unclaimed leaf from a counter in LDS whenever it has searched below
-// its last one.
+// The first kSplitDepth levels for the waves that share an instance: every
+// wave walks the same feasible starts of the first kSplitDepth requests
+// (without the bound's pruning, so that the walk, and the numbering of its
+// leaves, is the same in every wave) and searches below the leaves it claims:
+// a wave claims the next unclaimed leaf from the instance's counter in global
+// memory (*cnt) whenever it has searched below its last one, and at every
+// claim trades best totals with the instance's global best (*gb) and its
+// workgroup's (*sb).
 template <int D>
 __device__ __forceinline__ void wtop(const Inst& I, Search& S, int32_t cost, int lane, int32_t* sb, int32_t* cnt,
-                                     int32_t& leaf, int32_t& claim) {
+                                     int32_t* gb, int32_t& leaf, int32_t& claim) {
   const int32_t lo = (D > 0 && ((I.same >> D) & 1u)) ? S.c[D > 0 ? D - 1 : 0] - I.o[D > 0 ? D - 1 : 0] : I.a[D];
   for (int32_t pd = lo; pd <= I.horizon; ++pd) {
     ++S.nodes;
@@ -201,13 +213,19 @@ __device__ __forceinline__ void wtop(const Inst& I, Search& S, int32_t cost, int
         const int32_t g = __hip_atomic_load(sb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         S.best = g < S.best ? g : S.best;
         if (c + I.rem[D + 1] < S.best) wplace<D + 1, true>(I, S, c, lane, sb);
-        int32_t nx = 0;
-        if (lane == 0) nx = atomicAdd(cnt, 1);
+        int32_t nx = 0, gbv = 0;
+        if (lane == 0) {
+          nx = atomicAdd(cnt, 1);
+          gbv = atomicMin(gb, S.best);
+        }
         claim = __builtin_amdgcn_readfirstlane(nx);
+        gbv = __builtin_amdgcn_readfirstlane(gbv);
+        if (gbv < S.best) S.best = gbv;
+        if (lane == 0) atomicMin(sb, S.best);
       }
       ++leaf;
     } else {
-      wtop<D + 1>(I, S, c, lane, sb, cnt, leaf, claim);
+      wtop<D + 1>(I, S, c, lane, sb, cnt, gb, leaf, claim);
     }
 #pragma unroll
     for (int r = 0; r < D; ++r) {
@@ -322,44 +340,80 @@ __global__ __launch_bounds__(64) void k_optimum(OptParams P) {
   }
 }
 
-// Second launch: a workgroup of kGroupWaves waves per instance that the first
-// left unfinished (see wtop), each wave with at most P.node_cap nodes; the
-// first launch's best total is the starting bound.
-__global__ __launch_bounds__(64 * kGroupWaves) void k_optimum_group(OptParams P) {
-  const int k = blockIdx.x;
-  if (P.status[k] != kSplit) return;
-  __shared__ int32_t sbest, scount, sstop;
-  __shared__ unsigned long long snodes;
+// Between the launches: the list of unfinished instances (in no particular
+// order) and their search state.  k_pool_reset clears the count first.
+__global__ __launch_bounds__(64) void k_pool_reset(OptParams P) {
+  if (threadIdx.x == 0) P.pool[0] = 0;
+}
+
+__global__ __launch_bounds__(256) void k_pool_list(OptParams P) {
+  const int k = blockIdx.x * 256 + static_cast<int>(threadIdx.x);
+  if (k >= P.K || P.status[k] != kSplit) return;
+  int32_t* list = P.pool + 1;
+  const int j = atomicAdd(P.pool, 1);
+  list[j] = k;
+  list[P.K + j] = 0;                                           // piece counter
+  list[2 * P.K + j] = static_cast<int32_t>(P.total_latency[k]);  // best so far
+  list[3 * P.K + j] = 0;                                       // flags
+}
+
+// Second launch: workgroups of kGroupWaves waves, as many as the device holds
+// at once.  A workgroup starts at its own place in the list and goes through
+// it once: at every instance whose pieces are not all claimed yet, its waves
+// claim and search pieces (wtop) until none is left, then meet at a barrier
+// and move on.  Each wave has at most P.node_cap nodes per instance it works
+// on; a wave that runs out marks the instance stopped, and no more pieces of
+// it are handed out.
+__global__ __launch_bounds__(64 * kGroupWaves) void k_optimum_pool(OptParams P) {
+  __shared__ int32_t sbest, sflag;
+  const int U = P.pool[0];
+  if (U <= 0) return;
+  const int32_t* list = P.pool + 1;
+  int32_t* cnt = P.pool + 1 + P.K;
+  int32_t* gbest = P.pool + 1 + 2 * P.K;
+  int32_t* flags = P.pool + 1 + 3 * P.K;
   const int lane = static_cast<int>(threadIdx.x & 63u);
-  Search S;
-  S.nodes = 0;
-  S.cap = static_cast<int32_t>(P.node_cap < 0x7FFFFFFF ? P.node_cap : 0x7FFFFFFF);
-  S.stop = false;
-  Inst I;
-  (void)setup(P, k, I, S);  // valid: the first launch searched it
-  S.best = static_cast<int32_t>(P.total_latency[k]);
-  if (threadIdx.x == 0) {
-    sbest = S.best;
-    scount = 0;
-    sstop = 0;
-    snodes = 0ull;
+  const int j0 = static_cast<int>((static_cast<int64_t>(blockIdx.x) * U) / gridDim.x);
+  for (int step = 0; step < U; ++step) {
+    const int j = j0 + step < U ? j0 + step : j0 + step - U;
+    if (threadIdx.x == 0) {
+      sflag = __hip_atomic_load(&flags[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      sbest = __hip_atomic_load(&gbest[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    if (sflag == 0) {
+      const int k = list[j];
+      Search S;
+      S.nodes = 0;
+      S.cap = static_cast<int32_t>(P.node_cap < 0x7FFFFFFF ? P.node_cap : 0x7FFFFFFF);
+      S.stop = false;
+      Inst I;
+      (void)setup(P, k, I, S);  // valid: the first launch searched it
+      S.best = sbest;
+      int32_t first = 0;
+      if (lane == 0) first = atomicAdd(&cnt[j], 1);
+      int32_t leaf = 0, claim = __builtin_amdgcn_readfirstlane(first);
+      wtop<0>(I, S, 0, lane, &sbest, &cnt[j], &gbest[j], leaf, claim);
+      if (lane == 0) {
+        atomicMin(&gbest[j], S.best);
+        if (P.nodes) atomicAdd(reinterpret_cast<unsigned long long*>(&P.nodes[k]),
+                               static_cast<unsigned long long>(S.nodes));
+        // a walk that ends finds every piece claimed; a stopped one gives up
+        atomicOr(&flags[j], S.stop ? (kFlagClaimed | kFlagStop) : kFlagClaimed);
+      }
+    }
+    __syncthreads();  // sflag and sbest are rewritten for the next instance
   }
-  __syncthreads();
-  int32_t first = 0;
-  if (lane == 0) first = atomicAdd(&scount, 1);
-  int32_t leaf = 0, claim = __builtin_amdgcn_readfirstlane(first);
-  wtop<0>(I, S, 0, lane, &sbest, &scount, leaf, claim);
-  if (lane == 0) {
-    atomicMin(&sbest, S.best);
-    atomicAdd(&snodes, static_cast<unsigned long long>(S.nodes));
-    if (S.stop) atomicOr(&sstop, 1);
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    P.total_latency[k] = sbest;
-    P.status[k] = sstop ? SCHED_E_STEP_CAP : SCHED_OK;
-    if (P.nodes) P.nodes[k] += static_cast<int64_t>(snodes);
-  }
+}
+
+// After the second launch: the results of the instances it searched.
+__global__ __launch_bounds__(256) void k_pool_finish(OptParams P) {
+  const int j = blockIdx.x * 256 + static_cast<int>(threadIdx.x);
+  if (j >= P.pool[0]) return;
+  const int32_t* list = P.pool + 1;
+  const int k = list[j];
+  P.total_latency[k] = list[2 * P.K + j];
+  P.status[k] = (list[3 * P.K + j] & kFlagStop) ? SCHED_E_STEP_CAP : SCHED_OK;
 }
 
 }  // namespace opt
@@ -391,10 +445,34 @@ extern "C" int sched_optimum(const sched_instances_t* in, int64_t M, const int64
   P.node_cap = split ? opt::kFirstPassNodes : cap;
   P.unfinished = split ? opt::kSplit : SCHED_E_STEP_CAP;
   const hipStream_t st = static_cast<hipStream_t>(stream);
-  hipLaunchKernelGGL(opt::k_optimum, dim3(P.K), dim3(64), 0, st, P);
-  if (split && hipGetLastError() == hipSuccess) {
-    P.node_cap = cap;
-    hipLaunchKernelGGL(opt::k_optimum_group, dim3(P.K), dim3(64 * opt::kGroupWaves), 0, st, P);
+  // the second launch's grid: as many workgroups as the device holds at once
+  int dev = 0, n_cu = 0, per_cu = 0;
+  if (split) {
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, opt::k_optimum_pool, 64 * opt::kGroupWaves, 0) !=
+            hipSuccess)
+      return SCHED_E_HIP;
+    if (per_cu < 1) per_cu = 1;
+    // workspace: the count, then four arrays of K entries
+    if (hipMallocAsync(reinterpret_cast<void**>(&P.pool), sizeof(int32_t) * (1 + 4 * static_cast<size_t>(P.K)), st) !=
+        hipSuccess)
+      return SCHED_E_HIP;
   }
-  return hipGetLastError() == hipSuccess ? SCHED_OK : SCHED_E_HIP;
+  hipLaunchKernelGGL(opt::k_optimum, dim3(P.K), dim3(64), 0, st, P);
+  hipError_t err = hipGetLastError();
+  if (split) {
+    const dim3 g256((P.K + 255) / 256);
+    if (err == hipSuccess) {
+      hipLaunchKernelGGL(opt::k_pool_reset, dim3(1), dim3(64), 0, st, P);
+      hipLaunchKernelGGL(opt::k_pool_list, g256, dim3(256), 0, st, P);
+      P.node_cap = cap;
+      hipLaunchKernelGGL(opt::k_optimum_pool, dim3(n_cu * per_cu), dim3(64 * opt::kGroupWaves), 0, st, P);
+      hipLaunchKernelGGL(opt::k_pool_finish, g256, dim3(256), 0, st, P);
+      err = hipGetLastError();
+    }
+    const hipError_t ferr = hipFreeAsync(P.pool, st);
+    if (err == hipSuccess) err = ferr;
+  }
+  return err == hipSuccess ? SCHED_OK : SCHED_E_HIP;
 }

@@ -84,3 +84,53 @@ def test_statuses_and_node_cap(B):
     hit = capped["status"] == O.E_STEP_CAP
     assert hit.any()
     assert (capped["tel"][hit] >= full["tel"][hit]).all()   # an upper bound when the search was cut
+
+
+def _pool_golden():
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "opt_pool_tiny8.json")))
+    insts = [{f: i[f] for f in ("arrival", "prompt", "output")} for i in g["instances"]]
+    return g, insts
+
+
+def test_device_wide_second_search(B):
+    # eight-request instances whose search outlasts the first launch's budget
+    # (2^17 start steps per wave): their optimum comes from the second launch,
+    # in which every workgroup claims pieces of any unfinished instance.  The
+    # oracle's values are stored (tests/golden/make_opt_pool.py); alone, among
+    # easy instances, and with a policy's total as the starting bound.
+    import torch
+    g, insts = _pool_golden()
+    ref = [i["opt_tel"] for i in g["instances"]]
+    r = gpu_opt(B, W.from_lists(g["M"], insts, name="opt_pool"))
+    assert (r["status"] == 0).all()
+    assert (r["nodes"] > (1 << 17)).all()
+    assert r["tel"].tolist() == ref
+    easy = W.random_small(7, 300, 6, s_max=3, o_max=5, M=g["M"], arrivals=False)
+    mixed = [{f: easy.instance(k)[f] for f in ("arrival", "prompt", "output")} for k in range(300)]
+    pos = list(range(0, 300, 300 // len(insts)))[:len(insts)]
+    for p, inst in zip(reversed(pos), reversed(insts)):
+        mixed.insert(p, inst)
+    b = W.from_lists(g["M"], mixed, name="opt_pool_mixed")
+    r = gpu_opt(B, b)
+    at = [p + i for i, p in enumerate(pos)]
+    assert (r["status"] == 0).all()
+    assert r["tel"][at].tolist() == ref
+    rest = [k for k in range(b.num_instances) if k not in at]
+    assert r["tel"][rest[:40]].tolist() == [O.opt_tel(b.instance(k), b.M) for k in rest[:40]]
+    hsf = O.simulate_batch(b, O.HSF)["tel"]
+    rb = gpu_opt(B, b, upper_bound=torch.from_numpy(hsf).cuda())
+    assert rb["tel"].tolist() == r["tel"].tolist()
+    assert (r["tel"] <= hsf).all()
+
+
+def test_device_wide_second_search_node_cap(B):
+    # a budget just above the first launch's: the second search may run out on
+    # some piece; an instance it gives up on reports SCHED_E_STEP_CAP with a
+    # schedule at least as long as the optimum, the others the optimum
+    g, insts = _pool_golden()
+    ref = np.array([i["opt_tel"] for i in g["instances"]])
+    r = gpu_opt(B, W.from_lists(g["M"], insts, name="opt_pool_cap"), node_cap=(1 << 17) + 64)
+    ok = r["status"] == 0
+    assert ((r["status"] == 0) | (r["status"] == O.E_STEP_CAP)).all()
+    assert (r["tel"][ok] == ref[ok]).all()
+    assert (r["tel"][~ok] >= ref[~ok]).all()
