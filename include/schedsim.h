@@ -204,7 +204,8 @@ int sched_simulate_opts(const sched_instances_t* instances, int32_t algo, int64_
  * device it runs on until the process ends, and nothing is allocated (no
  * hipMalloc, no stream or event creation: SCHED_ADAPTIVE runs both of its
  * policies on `stream`).  The workspace needs 20 bytes per request plus 8 per
- * instance (12 for A_min with upper bounds and the adaptive policy), 16 more
+ * instance (12 for A_min with upper bounds and the adaptive policy, 16 for A_min
+ * batches of more than 16 instances per CU, plus 256 bytes), 16 more
  * per request with tie keys, and 8 more per request for
  * A_l and the adaptive policy or when n_max exceeds the LDS room of A_min's
  * cancelled set, and, for A_min when n_max exceeds 1024 (workgroup launches

@@ -57,6 +57,29 @@ __global__ __launch_bounds__(256) void k_prio_classes(Params P) {
   if (lo_s >= hi_s)
     for (int k = threadIdx.x; k < P.K; k += 256) P.pclass[k] = -1;
 }
+
+// Launch order (A_min batches served in several rounds of waves): the
+// instances by decreasing key, so that the longest expected simulations are
+// not the last ones to start.  The order within a bucket is whatever the
+// atomics give; outputs do not depend on the order.
+__global__ __launch_bounds__(64) void k_order_clear(Params P) {
+  P.obucket[threadIdx.x] = 0;
+}
+__global__ __launch_bounds__(64) void k_order_scan(Params P) {
+  // bucket b starts after every bucket above it
+  if (threadIdx.x == 0) {
+    int32_t run = 0;
+    for (int b = kOrderBuckets - 1; b >= 0; --b) {
+      const int32_t c = P.obucket[b];
+      P.obucket[b] = run;
+      run += c;
+    }
+  }
+}
+__global__ __launch_bounds__(256) void k_order_scatter(Params P) {
+  const int k = blockIdx.x * 256 + static_cast<int>(threadIdx.x);
+  if (k < P.K) P.order[atomicAdd(&P.obucket[P.okey[k]], 1)] = k;
+}
 }  // namespace sk
 
 // ---------------------------------------------------------------------------
@@ -134,8 +157,10 @@ const void* group_kernel(int w, int rows, bool vglobal) {
 }
 
 template <int ALGO>
-const void* sim_kernel(const Tier& tr) {
+const void* sim_kernel(const Tier& tr, bool ordered) {
   if (tr.gw > 1) return group_kernel<ALGO>(tr.gw, tr.rows, tr.vglobal);
+  if constexpr (ALGO == SCHED_AMIN)
+    if (tr.grow && !tr.wide && ordered) return reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO, true>);
   if (tr.grow)
     return tr.wide ? reinterpret_cast<const void*>(&sk::k_simulate_ladder_wide<ALGO>)
                    : reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO>);
@@ -155,13 +180,14 @@ const void* sim_kernel(const Tier& tr) {
   }
 }
 
-const void* sim_kernel_any(int algo, const Tier& tr) {
+// ordered: A_min's narrow ladder takes the instances in the order P.order
+const void* sim_kernel_any(int algo, const Tier& tr, bool ordered = false) {
   switch (algo) {
-    case SCHED_AMAX: return sim_kernel<SCHED_AMAX>(tr);
-    case SCHED_AMIN: return sim_kernel<SCHED_AMIN>(tr);
-    case SCHED_HSF: return sim_kernel<SCHED_HSF>(tr);
-    case SCHED_ARANDOM: return sim_kernel<SCHED_ARANDOM>(tr);
-    default: return sim_kernel<SCHED_AELL>(tr);
+    case SCHED_AMAX: return sim_kernel<SCHED_AMAX>(tr, false);
+    case SCHED_AMIN: return sim_kernel<SCHED_AMIN>(tr, ordered);
+    case SCHED_HSF: return sim_kernel<SCHED_HSF>(tr, false);
+    case SCHED_ARANDOM: return sim_kernel<SCHED_ARANDOM>(tr, false);
+    default: return sim_kernel<SCHED_AELL>(tr, false);
   }
 }
 
@@ -486,6 +512,9 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   const bool pcl = (algo == SCHED_AMIN || algo == SCHED_ADAPTIVE) && in->upper != nullptr && in->total_requests > 0 &&
                    static_cast<int64_t>(K) <= 16 * static_cast<int64_t>(n_cu);
   const size_t o_pc = off; off = align_up(off + (pcl ? 4 * K : 0), 256);
+  // the launch order of A_min batches that take more than one round of waves
+  const bool ord = algo == SCHED_AMIN && in->total_requests > 0 && static_cast<int64_t>(K) > 16 * static_cast<int64_t>(n_cu);
+  const size_t o_or = off; off = align_up(off + (ord ? 8 * K + 4 * sk::kOrderBuckets : 0), 256);
   // every workspace array is written before it is read (nothing needs clearing)
   void* ws = nullptr;
   if (no_alloc) {
@@ -520,12 +549,16 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   P.vglob = any_global ? reinterpret_cast<uint64_t*>(base + o_vg) : nullptr;
   P.vgroup = group_words ? reinterpret_cast<uint64_t*>(base + o_gv) : nullptr;
   P.pclass = pcl ? reinterpret_cast<int32_t*>(base + o_pc) : nullptr;
+  P.order = ord ? reinterpret_cast<int32_t*>(base + o_or) : nullptr;
+  P.okey = ord ? P.order + K : nullptr;
+  P.obucket = ord ? P.okey + K : nullptr;
   P.nw_max = nw;
   P.nw1_max = nw1;
   P.run_cap = forced_rows > 0 ? forced_rows * 64 : INT32_MAX;
 
   hipError_t err = hipSuccess;
   const dim3 grid(P.K), block(64);
+  if (P.order) hipLaunchKernelGGL(sk::k_order_clear, dim3(1), dim3(sk::kOrderBuckets), 0, st, P);
   switch (algo) {
     case SCHED_AMAX: hipLaunchKernelGGL((sk::k_prepare<SCHED_AMAX>), grid, block, 0, st, P); break;
     case SCHED_AMIN: hipLaunchKernelGGL((sk::k_prepare<SCHED_AMIN>), grid, block, 0, st, P); break;
@@ -537,6 +570,11 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   err = hipGetLastError();
   if (err == hipSuccess && P.pclass) {
     hipLaunchKernelGGL(sk::k_prio_classes, dim3(1), dim3(256), 0, st, P);
+    err = hipGetLastError();
+  }
+  if (err == hipSuccess && P.order) {
+    hipLaunchKernelGGL(sk::k_order_scan, dim3(1), dim3(64), 0, st, P);
+    hipLaunchKernelGGL(sk::k_order_scatter, dim3((P.K + 255) / 256), dim3(256), 0, st, P);
     err = hipGetLastError();
   }
   // Staging the completion steps in LDS (written out coalesced at the end of
@@ -557,7 +595,7 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   for (int a = 0; a < n_sim && err == hipSuccess; ++a)
     for (int p = 0; p < n_tiers[a] && err == hipSuccess; ++p)
       if (lds_of(a, tiers[a][p]) > 65536)
-        err = hipFuncSetAttribute(sim_kernel_any(sim_algos[a], tiers[a][p]),
+        err = hipFuncSetAttribute(sim_kernel_any(sim_algos[a], tiers[a][p], P.order && tiers[a][p].grid <= 0),
                                   hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds_of(a, tiers[a][p])));
   if (err == hipSuccess && o.event_before) err = hipEventRecord(static_cast<hipEvent_t>(o.event_before), st);
   // adaptive: the A_l launches go to the side stream after the preparation,
@@ -583,7 +621,8 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
       q.stage_comp = t.stage;
       void* args[] = {&q};
       const dim3 tgrid(t.grid > 0 ? t.grid : P.K), tblock(64 * (t.gw > 1 ? t.gw : 1));
-      err = hipLaunchKernel(sim_kernel_any(sim_algos[a], t), tgrid, tblock, args, lds_of(a, t), sa);
+      // (a launch over every instance may take them in the launch order)
+      err = hipLaunchKernel(sim_kernel_any(sim_algos[a], t, P.order && t.grid <= 0), tgrid, tblock, args, lds_of(a, t), sa);
     }
   }
   if (side) {

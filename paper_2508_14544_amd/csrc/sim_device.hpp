@@ -128,7 +128,16 @@ struct Params {
   // issue-priority class (0-2 by the width of its intervals; 3: none), or -1
   // when all instances share a class
   int32_t* pclass;
+  // A_min batches served in several rounds of waves: the order in which the
+  // first launch takes the instances (longest expected first), built from a
+  // key per instance and kOrderBuckets counters (then the buckets' cursors)
+  int32_t* order;
+  int32_t* okey;
+  int32_t* obucket;
 };
+
+// buckets of the launch-order key
+constexpr int kOrderBuckets = 64;
 
 // Internal statuses of an instance handed to a later pass: its running set
 // outgrew the register rows, or its cancelled set outgrew its slots.  The
@@ -352,6 +361,10 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
     if (P.algo_of) P.algo_of[k] = algo;
     if (P.algo_used) P.algo_used[k] = algo;
     if (P.pclass) P.pclass[k] = 3;
+    if (P.okey && (status != SCHED_OK || n == 0)) {
+      P.okey[k] = 0;
+      atomicAdd(&P.obucket[0], 1);
+    }
   }
   if (status != SCHED_OK || n == 0) return;
   if (P.pclass && algo == SCHED_AMIN) {
@@ -368,6 +381,27 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
     w = wave::sum_i64(w);
     l = wave::sum_i64(l);
     if (lane == 0) P.pclass[k] = 4 * w >= 3 * l ? 2 : 10 * w >= 3 * l ? 1 : 0;
+  }
+  if (P.okey) {
+    // A_min cancels until its lower bounds have grown to the true lengths, so
+    // the instances whose lower bounds fall furthest below them run longest:
+    // the key is 16 * sum(o - l) / sum(l), at most kOrderBuckets - 1
+    int64_t w = 0, l = 0;
+    for (int c = 0; c < n; c += 64) {
+      const int i = c + lane;
+      if (i < n) {
+        w += P.output[b + i] - P.lower[b + i];
+        l += P.lower[b + i];
+      }
+    }
+    w = wave::sum_i64(w);
+    l = wave::sum_i64(l);
+    if (lane == 0) {
+      const int64_t q = l > 0 ? (16 * w) / l : 0;
+      const int key = q < kOrderBuckets - 1 ? static_cast<int>(q) : kOrderBuckets - 1;
+      P.okey[k] = key;
+      atomicAdd(&P.obucket[key], 1);
+    }
   }
 
   // ---- tie keys: each request's rank in the order (tie key, index) (A_l:
@@ -1909,9 +1943,11 @@ __device__ __forceinline__ void ladder_instance(const Params& P, const int k) {
 }
 
 // The narrow ladder, held to 128 VGPRs so that four waves share a SIMD.
-template <int ALGO>
+// ORDERED: workgroup g simulates instance P.order[g] (its own instance of the
+// kernel, so that the other launches compile as before).
+template <int ALGO, bool ORDERED = false>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_simulate_ladder(Params P) {
-  const int k = blockIdx.x;
+  const int k = ORDERED ? P.order[blockIdx.x] : static_cast<int>(blockIdx.x);
   if (P.algo_of && P.algo_of[k] != ALGO) return;
   const int st0 = P.status[k];
   if (st0 == SCHED_OK) {
