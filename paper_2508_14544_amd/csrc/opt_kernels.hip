@@ -362,8 +362,8 @@ __global__ __launch_bounds__(256) void k_pool_list(OptParams P) {
 // it once: at every instance whose pieces are not all claimed yet, its waves
 // claim and search pieces (wtop) until none is left, then meet at a barrier
 // and move on.  Each wave has at most P.node_cap nodes per instance it works
-// on; a wave that runs out marks the instance stopped, and no more pieces of
-// it are handed out.
+// on; a wave that runs out marks the instance stopped (its result is then an
+// upper bound), and workgroups that come to it later skip it.
 __global__ __launch_bounds__(64 * kGroupWaves) void k_optimum_pool(OptParams P) {
   __shared__ int32_t sbest, sflag;
   const int U = P.pool[0];
