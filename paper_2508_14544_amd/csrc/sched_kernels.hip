@@ -157,10 +157,13 @@ const void* group_kernel(int w, int rows, bool vglobal) {
 }
 
 template <int ALGO>
-const void* sim_kernel(const Tier& tr, bool ordered) {
+const void* sim_kernel(const Tier& tr, bool ordered, bool classes) {
   if (tr.gw > 1) return group_kernel<ALGO>(tr.gw, tr.rows, tr.vglobal);
-  if constexpr (ALGO == SCHED_AMIN)
+  if constexpr (ALGO == SCHED_AMIN) {
     if (tr.grow && !tr.wide && ordered) return reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO, true>);
+    if (tr.grow && !tr.wide && classes)
+      return reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO, false, true>);
+  }
   if (tr.grow)
     return tr.wide ? reinterpret_cast<const void*>(&sk::k_simulate_ladder_wide<ALGO>)
                    : reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO>);
@@ -180,14 +183,15 @@ const void* sim_kernel(const Tier& tr, bool ordered) {
   }
 }
 
-// ordered: A_min's narrow ladder takes the instances in the order P.order
-const void* sim_kernel_any(int algo, const Tier& tr, bool ordered = false) {
+// ordered: A_min's narrow ladder takes the instances in the order P.order;
+// classes: it sets issue priorities by P.pclass
+const void* sim_kernel_any(int algo, const Tier& tr, bool ordered = false, bool classes = false) {
   switch (algo) {
-    case SCHED_AMAX: return sim_kernel<SCHED_AMAX>(tr, false);
-    case SCHED_AMIN: return sim_kernel<SCHED_AMIN>(tr, ordered);
-    case SCHED_HSF: return sim_kernel<SCHED_HSF>(tr, false);
-    case SCHED_ARANDOM: return sim_kernel<SCHED_ARANDOM>(tr, false);
-    default: return sim_kernel<SCHED_AELL>(tr, false);
+    case SCHED_AMAX: return sim_kernel<SCHED_AMAX>(tr, false, false);
+    case SCHED_AMIN: return sim_kernel<SCHED_AMIN>(tr, ordered, classes);
+    case SCHED_HSF: return sim_kernel<SCHED_HSF>(tr, false, false);
+    case SCHED_ARANDOM: return sim_kernel<SCHED_ARANDOM>(tr, false, false);
+    default: return sim_kernel<SCHED_AELL>(tr, false, false);
   }
 }
 
@@ -595,7 +599,8 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   for (int a = 0; a < n_sim && err == hipSuccess; ++a)
     for (int p = 0; p < n_tiers[a] && err == hipSuccess; ++p)
       if (lds_of(a, tiers[a][p]) > 65536)
-        err = hipFuncSetAttribute(sim_kernel_any(sim_algos[a], tiers[a][p], P.order && tiers[a][p].grid <= 0),
+        err = hipFuncSetAttribute(sim_kernel_any(sim_algos[a], tiers[a][p], P.order && tiers[a][p].grid <= 0,
+                                                 P.pclass != nullptr),
                                   hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds_of(a, tiers[a][p])));
   if (err == hipSuccess && o.event_before) err = hipEventRecord(static_cast<hipEvent_t>(o.event_before), st);
   // adaptive: the A_l launches go to the side stream after the preparation,
@@ -622,7 +627,8 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
       void* args[] = {&q};
       const dim3 tgrid(t.grid > 0 ? t.grid : P.K), tblock(64 * (t.gw > 1 ? t.gw : 1));
       // (a launch over every instance may take them in the launch order)
-      err = hipLaunchKernel(sim_kernel_any(sim_algos[a], t, P.order && t.grid <= 0), tgrid, tblock, args, lds_of(a, t), sa);
+      err = hipLaunchKernel(sim_kernel_any(sim_algos[a], t, P.order && t.grid <= 0, P.pclass != nullptr), tgrid, tblock,
+                            args, lds_of(a, t), sa);
     }
   }
   if (side) {

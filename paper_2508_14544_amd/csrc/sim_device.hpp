@@ -621,7 +621,7 @@ __device__ __forceinline__ int32_t lanes_sum_i32(int32_t v) {
 // most it can hold).  CAPPED holds the running set to P.run_cap runs.  W > 1:
 // a workgroup of W waves simulates the instance (see group_exchange).
 template <int ALGO, int ROWS, bool FROM_STATE = false, bool TO_STATE = false, bool VGLOBAL = false,
-          bool CAPPED = false, typename ST = SimState, int W = 1>
+          bool CAPPED = false, typename ST = SimState, int W = 1, bool CLS = true>
 __device__ __forceinline__ int sim_instance(const Params& P, const int k, const int st0, const int retry_status,
                                            ST* st = nullptr) {
   constexpr int kStateRows = ST::kRows;
@@ -980,7 +980,9 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     // bounds), the static class of the instance and whether half of it is
     // done instead.  Outputs do not depend on it.
     int prio = -1;
-    const int pcls = (ALGO == SCHED_AMIN && P.pclass) ? P.pclass[k] : -1;
+    // (CLS false: an instance of the code without the class read, for the
+    // launches that never have classes)
+    const int pcls = CLS ? ((ALGO == SCHED_AMIN && P.pclass) ? P.pclass[k] : -1) : -1;
 #define SK_SET_PRIORITY()                                                            \
   do {                                                                               \
     const int lv_ = pcls >= 0 ? pcls + (2 * (n - n_done) > n ? 1 : 0) : (4 * (n - n_done) - 1) / n; \
@@ -1943,9 +1945,10 @@ __device__ __forceinline__ void ladder_instance(const Params& P, const int k) {
 }
 
 // The narrow ladder, held to 128 VGPRs so that four waves share a SIMD.
-// ORDERED: workgroup g simulates instance P.order[g] (its own instance of the
-// kernel, so that the other launches compile as before).
-template <int ALGO, bool ORDERED = false>
+// ORDERED: workgroup g simulates instance P.order[g]; CLS: issue priorities
+// by P.pclass.  Each is an instance of the kernel of its own, so that the
+// other launches compile without them.
+template <int ALGO, bool ORDERED = false, bool CLS = false>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_simulate_ladder(Params P) {
   const int k = ORDERED ? P.order[blockIdx.x] : static_cast<int>(blockIdx.x);
   if (P.algo_of && P.algo_of[k] != ALGO) return;
@@ -1982,11 +1985,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
   int r;
   do {
     switch (st.next_rows) {
-      case 2: r = sim_instance<ALGO, 2, true, true>(P, k, SCHED_OK, P.retry_status, &st); break;
-      case 3: r = sim_instance<ALGO, 3, true, true>(P, k, SCHED_OK, P.retry_status, &st); break;
-      case 5: r = sim_instance<ALGO, 5, true, true>(P, k, SCHED_OK, P.retry_status, &st); break;
-      case 8: r = sim_instance<ALGO, 8, true, true>(P, k, SCHED_OK, P.retry_status, &st); break;
-      default: r = sim_instance<ALGO, 10, true, true>(P, k, SCHED_OK, P.retry_status, &st); break;
+      case 2: r = sim_instance<ALGO, 2, true, true, false, false, SimState, 1, CLS>(P, k, SCHED_OK, P.retry_status, &st); break;
+      case 3: r = sim_instance<ALGO, 3, true, true, false, false, SimState, 1, CLS>(P, k, SCHED_OK, P.retry_status, &st); break;
+      case 5: r = sim_instance<ALGO, 5, true, true, false, false, SimState, 1, CLS>(P, k, SCHED_OK, P.retry_status, &st); break;
+      case 8: r = sim_instance<ALGO, 8, true, true, false, false, SimState, 1, CLS>(P, k, SCHED_OK, P.retry_status, &st); break;
+      default: r = sim_instance<ALGO, 10, true, true, false, false, SimState, 1, CLS>(P, k, SCHED_OK, P.retry_status, &st); break;
     }
   } while (r == kResume);
 }
