@@ -509,11 +509,13 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   const size_t o_gv = off; off = align_up(off + 8 * static_cast<size_t>(group_words), 256);
   // Priority classes only where every instance of the batch is resident at
   // once (16 waves a CU), so that the launch lasts as long as its slowest
-  // instance; a batch served in several rounds of waves keeps the priority by
-  // unfinished work.
+  // instance, and where waves share a SIMD at all (more than one wave on
+  // each of a CU's four SIMDs); a batch served in several rounds of waves
+  // keeps the priority by unfinished work.
   int n_cu = 0;
   if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return SCHED_E_HIP;
   const bool pcl = (algo == SCHED_AMIN || algo == SCHED_ADAPTIVE) && in->upper != nullptr && in->total_requests > 0 &&
+                   static_cast<int64_t>(K) > 4 * static_cast<int64_t>(n_cu) &&
                    static_cast<int64_t>(K) <= 16 * static_cast<int64_t>(n_cu);
   const size_t o_pc = off; off = align_up(off + (pcl ? 4 * K : 0), 256);
   // the launch order of A_min batches that take more than one round of waves
