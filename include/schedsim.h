@@ -154,8 +154,11 @@ typedef struct {
                                1024 in a retry launch; beyond that, workgroups as above)    */
   int32_t evicted_capacity; /* LDS slots of A_min's cancelled set in the first launch; 0:
                                default (min(n_max, 16384) for batches of at most 64 instances,
-                               else min(n_max, 512) for n_max <= 1024 and min(n_max, 1024)
-                               above; clipped to what a workgroup's LDS holds).  An instance
+                               else, for n_max <= 1024, min(n_max, the slots that a wave's
+                               share of a CU's LDS leaves beside its bitmaps and staged
+                               completion steps, at least 512 and at most 1024), and
+                               min(n_max, 1024) above; clipped to what a workgroup's LDS
+                               holds).  An instance
                                that outgrows them is simulated again with as many slots as the
                                LDS holds, and one that outgrows those with a set of n slots in
                                global memory (8 bytes of workspace per request when n_max

@@ -446,12 +446,20 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   int cap_fit = static_cast<int>((static_cast<size_t>(lds_max) - lds_bitmaps) / 8);
   if (o.evicted_lds_limit > 0) cap_fit = std::min(cap_fit, o.evicted_lds_limit);
   // the first pass's cancelled-set slots (A_min; A_l's promoted queue is an
-  // array of n entries in global memory).  A_min scans its set per
-  // admission, so it is kept small where many instances share a CU
+  // array of n entries in global memory).  Where many instances share a CU,
+  // at most 1024, and for n_max <= 1024 what the LDS share of a wave leaves
+  // next to the bitmaps and the staged completion steps (at least 512): an
+  // instance whose set outgrows its slots is simulated again by a later pass
+  const int64_t waves_cu = std::min<int64_t>(16, std::max<int64_t>(1, (in->num_instances + 255) / 256));
+  const int64_t share_room =
+      (static_cast<int64_t>(163840 / waves_cu) - 512 - static_cast<int64_t>(lds_bitmaps) - 4 * int64_t(nw) * 64) / 8;
   auto cap0_for = [&](int a) -> int {
     int64_t c = 0;
     if (a == SCHED_AMIN)
-      c = std::min<int64_t>(std::max<int64_t>(nmax, 1), in->num_instances <= 64 ? 16384 : nmax <= 1024 ? 512 : 1024);
+      c = std::min<int64_t>(std::max<int64_t>(nmax, 1),
+                            in->num_instances <= 64 ? 16384
+                            : nmax <= 1024          ? std::min<int64_t>(1024, std::max<int64_t>(512, share_room))
+                                                    : 1024);
     if (o.evicted_capacity > 0 && a == SCHED_AMIN) c = o.evicted_capacity;
     return static_cast<int>(std::min<int64_t>(c, cap_fit));
   };
