@@ -572,14 +572,18 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
 
   hipError_t err = hipSuccess;
   const dim3 grid(P.K), block(64);
+  // the preparation's key sort in LDS (two buffers of n_max keys) when they
+  // take at most 32 KiB; with tie keys its index sorts use the workspace
+  P.pre_lds = (!tie && algo != SCHED_AELL && 8 * nmax <= 32768) ? 1 : 0;
+  const size_t pre_bytes = P.pre_lds ? 8 * static_cast<size_t>(nmax) : 0;
   if (P.order) hipLaunchKernelGGL(sk::k_order_clear, dim3(1), dim3(sk::kOrderBuckets), 0, st, P);
   switch (algo) {
-    case SCHED_AMAX: hipLaunchKernelGGL((sk::k_prepare<SCHED_AMAX>), grid, block, 0, st, P); break;
-    case SCHED_AMIN: hipLaunchKernelGGL((sk::k_prepare<SCHED_AMIN>), grid, block, 0, st, P); break;
-    case SCHED_HSF: hipLaunchKernelGGL((sk::k_prepare<SCHED_HSF>), grid, block, 0, st, P); break;
-    case SCHED_AELL: hipLaunchKernelGGL((sk::k_prepare<SCHED_AELL>), grid, block, 0, st, P); break;
-    case SCHED_ARANDOM: hipLaunchKernelGGL((sk::k_prepare<SCHED_ARANDOM>), grid, block, 0, st, P); break;
-    default: hipLaunchKernelGGL((sk::k_prepare<SCHED_ADAPTIVE>), grid, block, 0, st, P); break;
+    case SCHED_AMAX: hipLaunchKernelGGL((sk::k_prepare<SCHED_AMAX>), grid, block, pre_bytes, st, P); break;
+    case SCHED_AMIN: hipLaunchKernelGGL((sk::k_prepare<SCHED_AMIN>), grid, block, pre_bytes, st, P); break;
+    case SCHED_HSF: hipLaunchKernelGGL((sk::k_prepare<SCHED_HSF>), grid, block, pre_bytes, st, P); break;
+    case SCHED_AELL: hipLaunchKernelGGL((sk::k_prepare<SCHED_AELL>), grid, block, pre_bytes, st, P); break;
+    case SCHED_ARANDOM: hipLaunchKernelGGL((sk::k_prepare<SCHED_ARANDOM>), grid, block, pre_bytes, st, P); break;
+    default: hipLaunchKernelGGL((sk::k_prepare<SCHED_ADAPTIVE>), grid, block, pre_bytes, st, P); break;
   }
   err = hipGetLastError();
   if (err == hipSuccess && P.pclass) {

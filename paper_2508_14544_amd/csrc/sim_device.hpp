@@ -134,6 +134,9 @@ struct Params {
   int32_t* order;
   int32_t* okey;
   int32_t* obucket;
+  // k_prepare: nonzero when its key sort runs in two LDS buffers of
+  // max_requests entries (dynamic LDS) instead of sort_a / sort_b
+  int32_t pre_lds;
 };
 
 // buckets of the launch-order key
@@ -429,7 +432,11 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
 
   // ---- keys (k0 << 17 | id), k0 = u (A_max), l (A_min, A_l), o (H-SF), the
   // priority (A_random, which plans with o); id = the index, or the tie rank,
-  // placed at position id so that the stable sort below keeps id order
+  // placed at position id so that the stable sort below keeps id order.  The
+  // two sort buffers are in LDS when the launch gave them room (P.pre_lds)
+  extern __shared__ uint32_t pre_buf[];
+  uint32_t* const ka = P.pre_lds ? pre_buf : P.sort_a + b;
+  uint32_t* const kb = P.pre_lds ? pre_buf + P.max_requests : P.sort_b + b;
   for (int c = 0; c < n; c += 64) {
     const int i = c + lane;
     if (i < n) {
@@ -438,15 +445,15 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
                     : (algo == SCHED_ARANDOM) ? P.priority[b + i]
                                            : P.lower[b + i];
       const uint32_t id = tie ? static_cast<uint32_t>(P.tr_of[b + i]) : static_cast<uint32_t>(i);
-      P.sort_a[b + id] = (static_cast<uint32_t>(est) << kIdxBits) | id;
+      ka[id] = (static_cast<uint32_t>(est) << kIdxBits) | id;
     }
   }
   __syncthreads();
   // ---- stable LSD radix sort on bits 17..24 then 25..31 (A_l's queue is in
   // id order: its ranks are the ids, no sort)
   for (int pass = 0; pass < (algo == SCHED_AELL ? 0 : 2); ++pass) {
-    const uint32_t* src = (pass == 0 ? P.sort_a : P.sort_b) + b;
-    uint32_t* dst = (pass == 0 ? P.sort_b : P.sort_a) + b;
+    const uint32_t* src = pass == 0 ? ka : kb;
+    uint32_t* dst = pass == 0 ? kb : ka;
     const int shift = kIdxBits + 8 * pass;
     radix_pass(hist, src, dst, n, [&](uint32_t key) { return (key >> shift) & 0xFFu; });
   }
@@ -454,7 +461,7 @@ __global__ __launch_bounds__(64) void k_prepare(Params P) {
   for (int c = 0; c < n; c += 64) {
     const int r = c + lane;
     if (r < n) {
-      const uint32_t key = P.sort_a[b + r];
+      const uint32_t key = ka[r];
       const uint32_t id = key & kIdxMask;
       const uint32_t idx = tie ? static_cast<uint32_t>(P.idx_of[b + id]) : id;
       const uint32_t s = static_cast<uint32_t>(P.prompt[b + idx]);
