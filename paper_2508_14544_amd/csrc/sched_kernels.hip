@@ -241,7 +241,7 @@ int64_t group_cap_fit(int algo, int w, int rows, const Room& rm) {
 // (4096 where eight waves' bitmaps do not fit the LDS), or above a caller's
 // forced running capacity, are refused.
 int build_tiers(int algo, int64_t nmax, int64_t K, int forced_rows, int cap0, int cap_fit, int ww, const Room& rm,
-                Tier* out) {
+                bool simd_each, Tier* out) {
   // (A_l's queue lives in global memory and never overflows)
   const bool has_v = algo == SCHED_AMIN;
   const int64_t need_v = has_v ? std::max<int64_t>(nmax, 1) : 0;
@@ -274,8 +274,12 @@ int build_tiers(int algo, int64_t nmax, int64_t K, int forced_rows, int cap0, in
     if (v_lds_short) out[m++] = Tier{16, false, false, true, true, 0, 2, 0, 0, 0, 0, 0};
   } else {
     // few instances of many requests start on the wide ladder (they would
-    // likely outgrow the narrow one, and the retry would simulate them again)
-    const bool wide0 = nmax > 4096 && K <= 256;
+    // likely outgrow the narrow one, and the retry would simulate them again);
+    // so does A_l where every wave has a SIMD to itself (simd_each), since it
+    // then costs no occupancy and A_l's window registers spill in the narrow
+    // one (one instance of 10^4 requests: 30.2 against 33.9 ms; A_min runs
+    // faster on the narrow ladder, 28.1 against 32.3 ms)
+    const bool wide0 = (nmax > 4096 && K <= 256) || (algo == SCHED_AELL && simd_each);
     out[m++] = Tier{0, true, wide0, false, false, cap0, 0, 0, 0, 0, 0, 0};
     const int mask = (!wide0 && nmax > 640 ? 1 : 0) | (v_retry ? 2 : 0);
     if (mask) out[m++] = Tier{0, true, true, true, false, cap1, mask, 0, 0, 0, 0, 0};
@@ -434,8 +438,9 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   hipStream_t st = static_cast<hipStream_t>(stream);
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return SCHED_E_HIP;
-  int lds_max = 0;
-  if (hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+  int lds_max = 0, n_cu = 0;
+  if (hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     return SCHED_E_HIP;
 
   const int nw = static_cast<int>((nmax + 63) / 64);
@@ -478,7 +483,7 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   int64_t group_words = 0;
   for (int a = 0; a < n_sim; ++a) {
     n_tiers[a] = build_tiers(sim_algos[a], nmax, in->num_instances, forced_rows, cap0_for(sim_algos[a]), cap_fit,
-                             ww, rm, tiers[a]);
+                             ww, rm, algo == SCHED_AELL && in->num_instances <= 4 * int64_t(n_cu), tiers[a]);
     for (int p = 0; p < n_tiers[a]; ++p) {
       Tier& t = tiers[a][p];
       if (t.gw > 1 && t.vglobal) {
@@ -520,8 +525,6 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   // instance, and where waves share a SIMD at all (more than one wave on
   // each of a CU's four SIMDs); a batch served in several rounds of waves
   // keeps the priority by unfinished work.
-  int n_cu = 0;
-  if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return SCHED_E_HIP;
   const bool pcl = (algo == SCHED_AMIN || algo == SCHED_ADAPTIVE) && in->upper != nullptr && in->total_requests > 0 &&
                    static_cast<int64_t>(K) > 4 * static_cast<int64_t>(n_cu) &&
                    static_cast<int64_t>(K) <= 16 * static_cast<int64_t>(n_cu);
