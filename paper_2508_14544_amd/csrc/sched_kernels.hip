@@ -275,11 +275,12 @@ int build_tiers(int algo, int64_t nmax, int64_t K, int forced_rows, int cap0, in
   } else {
     // few instances of many requests start on the wide ladder (they would
     // likely outgrow the narrow one, and the retry would simulate them again);
-    // so does A_l where every wave has a SIMD to itself (simd_each), since it
-    // then costs no occupancy and A_l's window registers spill in the narrow
-    // one (one instance of 10^4 requests: 30.2 against 33.9 ms; A_min runs
-    // faster on the narrow ladder, 28.1 against 32.3 ms)
-    const bool wide0 = (nmax > 4096 && K <= 256) || (algo == SCHED_AELL && simd_each);
+    // so do A_l, A_max and H-SF where every wave has a SIMD to itself
+    // (simd_each, set by the caller for those policies), since it then costs
+    // no occupancy and they run faster without the narrow bodies' spills (A_l
+    // on one instance of 10^4 requests: 30.2 against 33.9 ms); A_min and
+    // A_random run faster on the narrow ladder (28.1 against 32.3 ms for A_min)
+    const bool wide0 = (nmax > 4096 && K <= 256) || simd_each;
     out[m++] = Tier{0, true, wide0, false, false, cap0, 0, 0, 0, 0, 0, 0};
     const int mask = (!wide0 && nmax > 640 ? 1 : 0) | (v_retry ? 2 : 0);
     if (mask) out[m++] = Tier{0, true, true, true, false, cap1, mask, 0, 0, 0, 0, 0};
@@ -483,7 +484,10 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   int64_t group_words = 0;
   for (int a = 0; a < n_sim; ++a) {
     n_tiers[a] = build_tiers(sim_algos[a], nmax, in->num_instances, forced_rows, cap0_for(sim_algos[a]), cap_fit,
-                             ww, rm, algo == SCHED_AELL && in->num_instances <= 4 * int64_t(n_cu), tiers[a]);
+                             ww, rm,
+                             (algo == SCHED_AELL || algo == SCHED_AMAX || algo == SCHED_HSF) &&
+                                 in->num_instances <= 4 * int64_t(n_cu),
+                             tiers[a]);
     for (int p = 0; p < n_tiers[a]; ++p) {
       Tier& t = tiers[a][p];
       if (t.gw > 1 && t.vglobal) {
