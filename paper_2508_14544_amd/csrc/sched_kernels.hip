@@ -130,6 +130,7 @@ struct Tier {
   int stage;        // completion steps staged in LDS (1) or not (0)
   int gw;           // > 1: a workgroup of gw waves per instance (k_simulate_group)
   int grid;         // workgroups of the launch (0: one per instance)
+  int roomy;        // the narrow ladder with 256 VGPRs (k_simulate_ladder_roomy)
 };
 
 // The workgroup kernels that exist (sched_group.hip), else NULL.
@@ -164,6 +165,7 @@ const void* sim_kernel(const Tier& tr, bool ordered, bool classes) {
     if (tr.grow && !tr.wide && classes)
       return reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO, false, true>);
   }
+  if (tr.grow && !tr.wide && tr.roomy) return reinterpret_cast<const void*>(&sk::k_simulate_ladder_roomy<ALGO>);
   if (tr.grow)
     return tr.wide ? reinterpret_cast<const void*>(&sk::k_simulate_ladder_wide<ALGO>)
                    : reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO>);
@@ -275,13 +277,10 @@ int build_tiers(int algo, int64_t nmax, int64_t K, int forced_rows, int cap0, in
   } else {
     // few instances of many requests start on the wide ladder (they would
     // likely outgrow the narrow one, and the retry would simulate them again);
-    // so do A_l, A_max and H-SF where every wave has a SIMD to itself
-    // (simd_each, set by the caller for those policies), since it then costs
-    // no occupancy and they run faster without the narrow bodies' spills (A_l
-    // on one instance of 10^4 requests: 30.2 against 33.9 ms); A_min and
-    // A_random run faster on the narrow ladder (28.1 against 32.3 ms for A_min)
-    const bool wide0 = (nmax > 4096 && K <= 256) || simd_each;
-    out[m++] = Tier{0, true, wide0, false, false, cap0, 0, 0, 0, 0, 0, 0};
+    // where every wave has a SIMD to itself (simd_each) the narrow bodies get
+    // 256 VGPRs, which costs no occupancy there and spills less
+    const bool wide0 = nmax > 4096 && K <= 256;
+    out[m++] = Tier{0, true, wide0, false, false, cap0, 0, 0, 0, 0, 0, 0, !wide0 && simd_each ? 1 : 0};
     const int mask = (!wide0 && nmax > 640 ? 1 : 0) | (v_retry ? 2 : 0);
     if (mask) out[m++] = Tier{0, true, true, true, false, cap1, mask, 0, 0, 0, 0, 0};
     if (v_lds_short) out[m++] = Tier{16, false, false, true, true, 0, 2, 0, 0, 0, 0, 0};
@@ -484,10 +483,7 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
   int64_t group_words = 0;
   for (int a = 0; a < n_sim; ++a) {
     n_tiers[a] = build_tiers(sim_algos[a], nmax, in->num_instances, forced_rows, cap0_for(sim_algos[a]), cap_fit,
-                             ww, rm,
-                             (algo == SCHED_AELL || algo == SCHED_AMAX || algo == SCHED_HSF) &&
-                                 in->num_instances <= 4 * int64_t(n_cu),
-                             tiers[a]);
+                             ww, rm, in->num_instances <= 4 * int64_t(n_cu), tiers[a]);
     for (int p = 0; p < n_tiers[a]; ++p) {
       Tier& t = tiers[a][p];
       if (t.gw > 1 && t.vglobal) {

@@ -1951,55 +1951,68 @@ __device__ __forceinline__ void ladder_instance(const Params& P, const int k) {
   }
 }
 
-// The narrow ladder, held to 128 VGPRs so that four waves share a SIMD.
-// ORDERED: workgroup g simulates instance P.order[g]; CLS: issue priorities
-// by P.pclass.  Each is an instance of the kernel of its own, so that the
+// The narrow ladder: one wave per instance moving along the bodies of 2 to
+// 10 rows (the body of the two kernels below; ORDERED_: workgroup g simulates
+// instance P.order[g]; CLS_: issue priorities by P.pclass).
+#define SK_NARROW_LADDER(ORDERED_, CLS_)                                                                                               \
+  const int k = (ORDERED_) ? P.order[blockIdx.x] : static_cast<int>(blockIdx.x);                                                       \
+  if (P.algo_of && P.algo_of[k] != ALGO) return;                                                                                       \
+  const int st0 = P.status[k];                                                                                                         \
+  if (st0 == SCHED_OK) {                                                                                                               \
+    /* the bodies all resume from a state, so the bitmaps and staged outputs */                                                        \
+    /* are set up here */                                                                                                              \
+    extern __shared__ uint64_t lds64[];                                                                                                \
+    const int64_t b = P.offsets[k];                                                                                                    \
+    const int n = static_cast<int>(P.offsets[k + 1] - b);                                                                              \
+    const int nw = (n + 63) >> 6, nw1 = (nw + 63) >> 6;                                                                                \
+    for (int w = threadIdx.x; w < nw; w += 64) lds64[w] = 0;                                                                           \
+    for (int w = threadIdx.x; w < nw1; w += 64) lds64[P.nw_max + w] = 0;                                                               \
+    int32_t* lc = reinterpret_cast<int32_t*>(lds64 + P.nw_max + P.nw1_max + P.cap_v);                                                  \
+    if (P.stage_comp)                                                                                                                  \
+      for (int i = threadIdx.x; i < n; i += 64) lc[i] = -1;                                                                            \
+    __syncthreads();                                                                                                                   \
+  }                                                                                                                                    \
+  const bool empty = st0 == SCHED_OK && P.offsets[k + 1] == P.offsets[k];                                                              \
+  if (st0 != SCHED_OK || empty) {                                                                                                      \
+    /* nothing to simulate: zero totals (the per-request outputs were set by */                                                        \
+    /* the preparation) */                                                                                                             \
+    if (threadIdx.x == 0) {                                                                                                            \
+      P.total_latency[k] = 0;                                                                                                          \
+      if (P.makespan) P.makespan[k] = 0;                                                                                               \
+      if (P.request_steps) P.request_steps[k] = 0;                                                                                     \
+      if (P.total_evictions) P.total_evictions[k] = 0;                                                                                 \
+      P.status[k] = st0;                                                                                                               \
+    }                                                                                                                                  \
+    return;                                                                                                                            \
+  }                                                                                                                                    \
+  SimState st;                                                                                                                         \
+  fresh_state(st);                                                                                                                     \
+  int r;                                                                                                                               \
+  do {                                                                                                                                 \
+    switch (st.next_rows) {                                                                                                            \
+      case 2: r = sim_instance<ALGO, 2, true, true, false, false, SimState, 1, (CLS_)>(P, k, SCHED_OK, P.retry_status, &st); break;    \
+      case 3: r = sim_instance<ALGO, 3, true, true, false, false, SimState, 1, (CLS_)>(P, k, SCHED_OK, P.retry_status, &st); break;    \
+      case 5: r = sim_instance<ALGO, 5, true, true, false, false, SimState, 1, (CLS_)>(P, k, SCHED_OK, P.retry_status, &st); break;    \
+      case 8: r = sim_instance<ALGO, 8, true, true, false, false, SimState, 1, (CLS_)>(P, k, SCHED_OK, P.retry_status, &st); break;    \
+      default: r = sim_instance<ALGO, 10, true, true, false, false, SimState, 1, (CLS_)>(P, k, SCHED_OK, P.retry_status, &st); break;  \
+    }                                                                                                                                  \
+  } while (r == kResume);
+
+// The narrow ladder held to 128 VGPRs so that four waves share a SIMD; each
+// (ORDERED, CLS) pair is an instance of the kernel of its own, so that the
 // other launches compile without them.
 template <int ALGO, bool ORDERED = false, bool CLS = false>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_simulate_ladder(Params P) {
-  const int k = ORDERED ? P.order[blockIdx.x] : static_cast<int>(blockIdx.x);
-  if (P.algo_of && P.algo_of[k] != ALGO) return;
-  const int st0 = P.status[k];
-  if (st0 == SCHED_OK) {
-    // the bodies all resume from a state, so the bitmaps and staged outputs
-    // are set up here
-    extern __shared__ uint64_t lds64[];
-    const int64_t b = P.offsets[k];
-    const int n = static_cast<int>(P.offsets[k + 1] - b);
-    const int nw = (n + 63) >> 6, nw1 = (nw + 63) >> 6;
-    for (int w = threadIdx.x; w < nw; w += 64) lds64[w] = 0;
-    for (int w = threadIdx.x; w < nw1; w += 64) lds64[P.nw_max + w] = 0;
-    int32_t* lc = reinterpret_cast<int32_t*>(lds64 + P.nw_max + P.nw1_max + P.cap_v);
-    if (P.stage_comp)
-      for (int i = threadIdx.x; i < n; i += 64) lc[i] = -1;
-    __syncthreads();
-  }
-  const bool empty = st0 == SCHED_OK && P.offsets[k + 1] == P.offsets[k];
-  if (st0 != SCHED_OK || empty) {
-    // nothing to simulate: zero totals (the per-request outputs were set by
-    // the preparation)
-    if (threadIdx.x == 0) {
-      P.total_latency[k] = 0;
-      if (P.makespan) P.makespan[k] = 0;
-      if (P.request_steps) P.request_steps[k] = 0;
-      if (P.total_evictions) P.total_evictions[k] = 0;
-      P.status[k] = st0;
-    }
-    return;
-  }
-  SimState st;
-  fresh_state(st);
-  int r;
-  do {
-    switch (st.next_rows) {
-      case 2: r = sim_instance<ALGO, 2, true, true, false, false, SimState, 1, CLS>(P, k, SCHED_OK, P.retry_status, &st); break;
-      case 3: r = sim_instance<ALGO, 3, true, true, false, false, SimState, 1, CLS>(P, k, SCHED_OK, P.retry_status, &st); break;
-      case 5: r = sim_instance<ALGO, 5, true, true, false, false, SimState, 1, CLS>(P, k, SCHED_OK, P.retry_status, &st); break;
-      case 8: r = sim_instance<ALGO, 8, true, true, false, false, SimState, 1, CLS>(P, k, SCHED_OK, P.retry_status, &st); break;
-      default: r = sim_instance<ALGO, 10, true, true, false, false, SimState, 1, CLS>(P, k, SCHED_OK, P.retry_status, &st); break;
-    }
-  } while (r == kResume);
+  SK_NARROW_LADDER(ORDERED, CLS);
 }
+
+// The same bodies with 256 VGPRs (fewer spills), for batches in which every
+// wave has a SIMD to itself.
+template <int ALGO>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void k_simulate_ladder_roomy(Params P) {
+  SK_NARROW_LADDER(false, false);
+}
+#undef SK_NARROW_LADDER
 
 // The wide ladder (up to 1024 runs): for batches of few instances, where
 // registers matter more than occupancy, and for the instances that outgrow
