@@ -1,9 +1,13 @@
-"""A_min batches with more instances than the device holds at once take their
-instances in a launch order (the widest gaps between the lower bounds and the
-outputs first).  The outputs must not depend on it: every instance equals the
-oracle (Algorithm 2 with equation (2)), invalid and empty instances keep
-their statuses, the batch reversed gives the same outputs per instance, and
-the no-allocation entry point gives the same bits."""
+"""Launch shapes.  A_min batches with more instances than the device holds at
+once take their instances in a launch order (the widest gaps between the
+lower bounds and the outputs first), batches of at most four instances per CU
+run the 256-VGPR bodies, and A_min batches in between may set issue
+priorities by class.  The outputs must not depend on any of it: every
+instance equals the oracle (Algorithm 2 with equation (2)), invalid and
+empty instances keep their statuses, the batch reversed gives the same
+outputs per instance, the no-allocation entry point gives the same bits, and
+the same instances alone or inside a larger batch give the same outputs under
+every policy."""
 import numpy as np
 import pytest
 
@@ -52,3 +56,22 @@ def test_launch_order_many_instances(B):
         torch.cuda.synchronize()
         for f in ("status", "tel", "makespan", "request_steps", "total_evictions", "completion", "evictions"):
             assert torch.equal(out[f], ref_t[f]), f
+
+
+@pytest.mark.parametrize("algo", ["amin", "amax", "hsf", "aell", "adaptive", "arandom"])
+def test_same_instances_in_every_launch_shape(B, algo):
+    # 300 instances of the benchmark batch alone (a batch of at most 4 per CU:
+    # the 256-VGPR bodies) and inside the whole 4096-instance batch (the
+    # 128-VGPR bodies; A_min with issue-priority classes): the same outputs
+    a = O.ALGOS[algo]
+    full = W.generate("batch4096_n1000_m16384", 0)
+    if algo == "arandom":
+        full = W.with_random_order(full, seed=1)   # A_random's per-request order
+    ks = list(range(2800, 3100))
+    g = gpu_run(B, full, a)
+    s = gpu_run(B, full.subset(ks), a)
+    for f in FIELDS:
+        assert np.array_equal(s[f], g[f][ks]), (algo, f)
+    sel = np.concatenate([np.arange(full.offsets[k], full.offsets[k + 1]) for k in ks])
+    for f in ("completion", "evictions"):
+        assert np.array_equal(s[f], g[f][sel]), (algo, f)
