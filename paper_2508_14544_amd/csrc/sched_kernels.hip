@@ -158,14 +158,17 @@ const void* group_kernel(int w, int rows, bool vglobal) {
 }
 
 template <int ALGO>
-const void* sim_kernel(const Tier& tr, bool ordered, bool classes) {
+const void* sim_kernel(const Tier& tr, bool ordered, bool classes, bool rounds) {
   if (tr.gw > 1) return group_kernel<ALGO>(tr.gw, tr.rows, tr.vglobal);
   if constexpr (ALGO == SCHED_AMIN) {
-    if (tr.grow && !tr.wide && ordered) return reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO, true>);
+    if (tr.grow && !tr.wide && ordered)
+      return reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO, true, false, false>);
     if (tr.grow && !tr.wide && classes)
       return reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO, false, true>);
   }
   if (tr.grow && !tr.wide && tr.roomy) return reinterpret_cast<const void*>(&sk::k_simulate_ladder_roomy<ALGO>);
+  if (tr.grow && !tr.wide && rounds)
+    return reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO, false, false, false>);
   if (tr.grow)
     return tr.wide ? reinterpret_cast<const void*>(&sk::k_simulate_ladder_wide<ALGO>)
                    : reinterpret_cast<const void*>(&sk::k_simulate_ladder<ALGO>);
@@ -186,14 +189,16 @@ const void* sim_kernel(const Tier& tr, bool ordered, bool classes) {
 }
 
 // ordered: A_min's narrow ladder takes the instances in the order P.order;
-// classes: it sets issue priorities by P.pclass
-const void* sim_kernel_any(int algo, const Tier& tr, bool ordered = false, bool classes = false) {
+// classes: it sets issue priorities by P.pclass; rounds: the batch is served
+// in rounds of waves (the narrow ladder without issue priorities)
+const void* sim_kernel_any(int algo, const Tier& tr, bool ordered = false, bool classes = false,
+                           bool rounds = false) {
   switch (algo) {
-    case SCHED_AMAX: return sim_kernel<SCHED_AMAX>(tr, false, false);
-    case SCHED_AMIN: return sim_kernel<SCHED_AMIN>(tr, ordered, classes);
-    case SCHED_HSF: return sim_kernel<SCHED_HSF>(tr, false, false);
-    case SCHED_ARANDOM: return sim_kernel<SCHED_ARANDOM>(tr, false, false);
-    default: return sim_kernel<SCHED_AELL>(tr, false, false);
+    case SCHED_AMAX: return sim_kernel<SCHED_AMAX>(tr, false, false, rounds);
+    case SCHED_AMIN: return sim_kernel<SCHED_AMIN>(tr, ordered, classes, rounds);
+    case SCHED_HSF: return sim_kernel<SCHED_HSF>(tr, false, false, rounds);
+    case SCHED_ARANDOM: return sim_kernel<SCHED_ARANDOM>(tr, false, false, rounds);
+    default: return sim_kernel<SCHED_AELL>(tr, false, false, rounds);
   }
 }
 
@@ -530,7 +535,8 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
                    static_cast<int64_t>(K) <= 16 * static_cast<int64_t>(n_cu);
   const size_t o_pc = off; off = align_up(off + (pcl ? 4 * K : 0), 256);
   // the launch order of A_min batches that take more than one round of waves
-  const bool ord = algo == SCHED_AMIN && in->total_requests > 0 && static_cast<int64_t>(K) > 16 * static_cast<int64_t>(n_cu);
+  const bool rounds = static_cast<int64_t>(K) > 16 * static_cast<int64_t>(n_cu);
+  const bool ord = algo == SCHED_AMIN && in->total_requests > 0 && rounds;
   const size_t o_or = off; off = align_up(off + (ord ? 8 * K + 4 * sk::kOrderBuckets : 0), 256);
   // every workspace array is written before it is read (nothing needs clearing)
   void* ws = nullptr;
@@ -617,7 +623,7 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
     for (int p = 0; p < n_tiers[a] && err == hipSuccess; ++p)
       if (lds_of(a, tiers[a][p]) > 65536)
         err = hipFuncSetAttribute(sim_kernel_any(sim_algos[a], tiers[a][p], P.order && tiers[a][p].grid <= 0,
-                                                 P.pclass != nullptr),
+                                                 P.pclass != nullptr, rounds),
                                   hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds_of(a, tiers[a][p])));
   if (err == hipSuccess && o.event_before) err = hipEventRecord(static_cast<hipEvent_t>(o.event_before), st);
   // adaptive: the A_l launches go to the side stream after the preparation,
@@ -644,8 +650,8 @@ int simulate_impl(const sched_instances_t* in, int32_t algo, int64_t M, const sc
       void* args[] = {&q};
       const dim3 tgrid(t.grid > 0 ? t.grid : P.K), tblock(64 * (t.gw > 1 ? t.gw : 1));
       // (a launch over every instance may take them in the launch order)
-      err = hipLaunchKernel(sim_kernel_any(sim_algos[a], t, P.order && t.grid <= 0, P.pclass != nullptr), tgrid, tblock,
-                            args, lds_of(a, t), sa);
+      err = hipLaunchKernel(sim_kernel_any(sim_algos[a], t, P.order && t.grid <= 0, P.pclass != nullptr, rounds), tgrid,
+                            tblock, args, lds_of(a, t), sa);
     }
   }
   if (side) {

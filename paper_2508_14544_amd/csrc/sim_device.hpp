@@ -628,7 +628,7 @@ __device__ __forceinline__ int32_t lanes_sum_i32(int32_t v) {
 // most it can hold).  CAPPED holds the running set to P.run_cap runs.  W > 1:
 // a workgroup of W waves simulates the instance (see group_exchange).
 template <int ALGO, int ROWS, bool FROM_STATE = false, bool TO_STATE = false, bool VGLOBAL = false,
-          bool CAPPED = false, typename ST = SimState, int W = 1, bool CLS = true>
+          bool CAPPED = false, typename ST = SimState, int W = 1, bool CLS = true, bool PRIO = true>
 __device__ __forceinline__ int sim_instance(const Params& P, const int k, const int st0, const int retry_status,
                                            ST* st = nullptr) {
   constexpr int kStateRows = ST::kRows;
@@ -985,13 +985,14 @@ __device__ __forceinline__ int sim_instance(const Params& P, const int k, const 
     // fraction), so the instances that bound the launch are not slowed by
     // their SIMD-mates; where a batch mixes interval widths (A_min with upper
     // bounds), the static class of the instance and whether half of it is
-    // done instead.  Outputs do not depend on it.
+    // done instead (PRIO false: none).  Outputs do not depend on it.
     int prio = -1;
     // (CLS false: an instance of the code without the class read, for the
     // launches that never have classes)
     const int pcls = CLS ? ((ALGO == SCHED_AMIN && P.pclass) ? P.pclass[k] : -1) : -1;
 #define SK_SET_PRIORITY()                                                            \
   do {                                                                               \
+    if (!PRIO) break;                                                                \
     const int lv_ = pcls >= 0 ? pcls + (2 * (n - n_done) > n ? 1 : 0) : (4 * (n - n_done) - 1) / n; \
     if (lv_ != prio) {                                                               \
       prio = lv_;                                                                    \
@@ -1953,8 +1954,11 @@ __device__ __forceinline__ void ladder_instance(const Params& P, const int k) {
 
 // The narrow ladder: one wave per instance moving along the bodies of 2 to
 // 10 rows (the body of the two kernels below; ORDERED_: workgroup g simulates
-// instance P.order[g]; CLS_: issue priorities by P.pclass).
-#define SK_NARROW_LADDER(ORDERED_, CLS_)                                                                                               \
+// instance P.order[g]; CLS_: issue priorities by P.pclass; PRIO_ false: the
+// waves keep the default issue priority, for batches in which priorities
+// cannot help (a wave per SIMD, or rounds of waves) but would cost scalar
+// instructions).
+#define SK_NARROW_LADDER(ORDERED_, CLS_, PRIO_)                                                                                               \
   const int k = (ORDERED_) ? P.order[blockIdx.x] : static_cast<int>(blockIdx.x);                                                       \
   if (P.algo_of && P.algo_of[k] != ALGO) return;                                                                                       \
   const int st0 = P.status[k];                                                                                                         \
@@ -1990,27 +1994,27 @@ __device__ __forceinline__ void ladder_instance(const Params& P, const int k) {
   int r;                                                                                                                               \
   do {                                                                                                                                 \
     switch (st.next_rows) {                                                                                                            \
-      case 2: r = sim_instance<ALGO, 2, true, true, false, false, SimState, 1, (CLS_)>(P, k, SCHED_OK, P.retry_status, &st); break;    \
-      case 3: r = sim_instance<ALGO, 3, true, true, false, false, SimState, 1, (CLS_)>(P, k, SCHED_OK, P.retry_status, &st); break;    \
-      case 5: r = sim_instance<ALGO, 5, true, true, false, false, SimState, 1, (CLS_)>(P, k, SCHED_OK, P.retry_status, &st); break;    \
-      case 8: r = sim_instance<ALGO, 8, true, true, false, false, SimState, 1, (CLS_)>(P, k, SCHED_OK, P.retry_status, &st); break;    \
-      default: r = sim_instance<ALGO, 10, true, true, false, false, SimState, 1, (CLS_)>(P, k, SCHED_OK, P.retry_status, &st); break;  \
+      case 2: r = sim_instance<ALGO, 2, true, true, false, false, SimState, 1, (CLS_), (PRIO_)>(P, k, SCHED_OK, P.retry_status, &st); break;    \
+      case 3: r = sim_instance<ALGO, 3, true, true, false, false, SimState, 1, (CLS_), (PRIO_)>(P, k, SCHED_OK, P.retry_status, &st); break;    \
+      case 5: r = sim_instance<ALGO, 5, true, true, false, false, SimState, 1, (CLS_), (PRIO_)>(P, k, SCHED_OK, P.retry_status, &st); break;    \
+      case 8: r = sim_instance<ALGO, 8, true, true, false, false, SimState, 1, (CLS_), (PRIO_)>(P, k, SCHED_OK, P.retry_status, &st); break;    \
+      default: r = sim_instance<ALGO, 10, true, true, false, false, SimState, 1, (CLS_), (PRIO_)>(P, k, SCHED_OK, P.retry_status, &st); break;  \
     }                                                                                                                                  \
   } while (r == kResume);
 
 // The narrow ladder held to 128 VGPRs so that four waves share a SIMD; each
-// (ORDERED, CLS) pair is an instance of the kernel of its own, so that the
-// other launches compile without them.
-template <int ALGO, bool ORDERED = false, bool CLS = false>
+// (ORDERED, CLS, PRIO) choice is an instance of the kernel of its own, so
+// that the other launches compile without it.
+template <int ALGO, bool ORDERED = false, bool CLS = false, bool PRIO = true>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_simulate_ladder(Params P) {
-  SK_NARROW_LADDER(ORDERED, CLS);
+  SK_NARROW_LADDER(ORDERED, CLS, PRIO);
 }
 
 // The same bodies with 256 VGPRs (fewer spills), for batches in which every
-// wave has a SIMD to itself.
+// wave has a SIMD to itself (so without issue priorities).
 template <int ALGO>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void k_simulate_ladder_roomy(Params P) {
-  SK_NARROW_LADDER(false, false);
+  SK_NARROW_LADDER(false, false, false);
 }
 #undef SK_NARROW_LADDER
 
