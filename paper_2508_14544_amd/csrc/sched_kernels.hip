@@ -77,8 +77,26 @@ __global__ __launch_bounds__(64) void k_order_scan(Params P) {
   }
 }
 __global__ __launch_bounds__(256) void k_order_scatter(Params P) {
+  // one atomic per distinct key of a wave (neighbouring instances mostly
+  // share their key), the lanes of a key placed in lane order
   const int k = blockIdx.x * 256 + static_cast<int>(threadIdx.x);
-  if (k < P.K) P.order[atomicAdd(&P.obucket[P.okey[k]], 1)] = k;
+  const int lane = static_cast<int>(threadIdx.x & 63u);
+  const bool act = k < P.K;
+  const int key = act ? P.okey[k] : -1;
+  uint64_t left = __builtin_amdgcn_ballot_w64(act);
+  while (left) {
+    const int lead = __builtin_ctzll(left);
+    const int lkey = __builtin_amdgcn_readlane(key, lead);
+    const uint64_t same = __builtin_amdgcn_ballot_w64(act && key == lkey) & left;
+    int base = 0;
+    if (lane == lead) base = atomicAdd(&P.obucket[lkey], __builtin_popcountll(same));
+    base = __builtin_amdgcn_readlane(base, lead);
+    if ((same >> lane) & 1ull) {
+      const int below = __builtin_popcountll(same & ((1ull << lane) - 1ull));
+      P.order[base + below] = k;
+    }
+    left &= ~same;
+  }
 }
 }  // namespace sk
 
