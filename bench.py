@@ -24,7 +24,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 # MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = int32 VALU lane-operations per second
-PEAK_INT32_LANE_OPS = 256 * 4 * 16 * 2.4e9
+N_CU = 256
+CLOCK_HZ = 2.4e9
+PEAK_INT32_LANE_OPS = N_CU * 4 * 16 * CLOCK_HZ
 PEAK_LDS_BYTES = 256 * 128 * 2.4e9
 # widest LDS access of the simulation kernel: ds_read_b64 over 64 lanes
 LDS_BYTES_PER_INST_MAX = 64 * 8
@@ -82,6 +84,11 @@ def load_hardware_fraction(workload: str, algo: str, kernel_ms: float = 0.0):
            "valu_busy_pct": d["valu_busy_pct"], "valu_utilization_pct": d["valu_utilization_pct"],
            "lds_bank_conflict_pct": d.get("lds_bank_conflict_pct"),
            "source": "rocprofv3 --pmc VALUBusy VALUUtilization (committed summary of this kernel source)"}
+    if "salu_insts_per_launch" in d and kernel_ms > 0:
+        # a CU issues at most one scalar and one vector instruction per cycle
+        cu_cycles = N_CU * CLOCK_HZ * kernel_ms / 1e3
+        out["issue_per_cu_cycle"] = {"salu": d["salu_insts_per_launch"] / cu_cycles,
+                                     "valu": d["valu_insts_per_launch"] / cu_cycles, "limit": 1.0}
     if "lds_insts_per_launch" in d and kernel_ms > 0:
         lds_bytes = d["lds_insts_per_launch"] * LDS_BYTES_PER_INST_MAX
         out["lds_bytes_per_launch_max"] = lds_bytes
